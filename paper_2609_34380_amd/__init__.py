@@ -1,0 +1,22 @@
+"""MI355X (gfx950) implementation of the nested-precision linear layer of
+Dual-Mode Precision Serving: FP16 weights held as an FP8 E5M2 upper-byte plane
+plus a chunked low-byte residual plane, contracted in fast mode (upper plane
+only) or full mode (exact FP16 rebuilt in registers).
+
+The compute lives in libdps.so (HIP kernels behind a C ABI, include/dps.h);
+``paper_2609_34380_amd.dps`` is its thin Python binding.  Importing this
+package does not load the library; the first call into ``dps`` does, and
+fails loudly if it is not built.
+"""
+
+__all__ = ["dps", "workloads"]
+
+
+def __getattr__(name):
+    if name == "dps":
+        from . import dps as _dps
+        return _dps
+    if name == "workloads":
+        from . import workloads as _w
+        return _w
+    raise AttributeError(name)
