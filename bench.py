@@ -1,0 +1,308 @@
+"""Benchmark of the nested-precision linear layer on one MI355X.
+
+Workload (the metric's configuration): the hidden-4096 decode layer set --
+QKV 4096->6144, O 4096->4096, gate+up 4096->2x14336, down 14336->4096 --
+FP16 weights ~ N(0, 0.02) split into an E5M2 upper-byte plane and a residual
+plane in 2 MiB chunks, activations ~ N(0, 1), token batch M in
+{1, 8, 32, 128, 256}.  One step runs every layer at every M in fast mode and
+in full mode (40 nested-linear calls), captured once per weight copy as a
+HIP graph (the paper replays one captured graph per mode and batch size).
+
+value = effective weight GB/s over the step: weight-plane bytes the modes
+must read (fast N*K, full 2*N*K per call) / step time.  Four independent
+weight copies (1.7 GB) are rotated step to step so that reads come from HBM
+and not from the 256 MB Infinity Cache.
+
+Also printed on the same JSON line: the roofline of the dominant call
+(HIP events around back-to-back launches of that call on its stream), the
+CPU oracle timed on a bounded sample on the host cores, a per-call
+breakdown, and secondary figures (prefill TFLOPS on FP8/FP16 matrix cores).
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = ("nested-linear effective weight GB/s (decode) + TFLOPS (prefill), "
+          "fast vs full mode")
+HBM_PEAK_GBS = 8000.0
+MFMA_F16_TFLOPS = 2500.0
+MFMA_FP8_TFLOPS = 5000.0
+LOG2_CHUNK = 21
+COPIES = 4
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-secondary", action="store_true")
+    ap.add_argument("--roofline-reps", type=int, default=40)
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the nested linear layer is built and "
+              "measured on a single MI355X (no sharding, no collectives); "
+              "run it with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2609_34380_amd import dps, workloads
+
+    if not os.path.exists(dps.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    dps.load_library()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.Stream()
+
+    layers = workloads.H4096_SET
+    ms = workloads.DECODE_M
+    modes = (("fast", dps.MODE_FAST), ("full", dps.MODE_FULL))
+
+    # ---- weights: COPIES independent nested copies of the layer set ------------
+    copies = []
+    with torch.cuda.stream(stream):
+        for c in range(COPIES):
+            nws = []
+            for li, (name, n, k) in enumerate(layers):
+                w = workloads.weight_fp16(n, k, seed=1000 * c + li, device=dev)
+                res = dps.make_residual(n * k, LOG2_CHUNK, dev)
+                nws.append(dps.split(w, res))
+                del w
+            copies.append(nws)
+        xs = {m: {k: workloads.activations_fp16(m, k, seed=m * 7 + k, device=dev)
+                  for k in sorted({k for _, _, k in layers})} for m in ms}
+        ys = {m: {n: torch.empty((m, n), dtype=torch.float16, device=dev)
+                  for n in sorted({n for _, n, _ in layers})} for m in ms}
+        ws_bytes = max(dps.workspace_bytes(mode, 0, m, n, k)
+                       for m in ms for _, mode in modes for _, n, k in layers)
+        ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+
+    calls = [(m, mname, mode, li) for m in ms for mname, mode in modes
+             for li in range(len(layers))]
+
+    def run_call(copy, m, mode, li):
+        name, n, k = layers[li]
+        dps.linear(xs[m][k], copies[copy][li], mode, out=ys[m][n], workspace=ws)
+
+    def weight_bytes(mode, li):
+        _, n, k = layers[li]
+        return n * k * (1 if mode == dps.MODE_FAST else 2)
+
+    step_bytes = sum(weight_bytes(mode, li) for _, _, mode, li in calls)
+
+    # ---- one graph per weight copy ----------------------------------------------
+    graphs = []
+    with torch.cuda.stream(stream):
+        for c in range(COPIES):          # eager warm-up (also loads kernels)
+            for (m, _, mode, li) in calls:
+                run_call(c, m, mode, li)
+    stream.synchronize()
+    for c in range(COPIES):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            for (m, _, mode, li) in calls:
+                run_call(c, m, mode, li)
+        graphs.append(g)
+    torch.cuda.synchronize()
+
+    # ---- timed region ---------------------------------------------------------------
+    with torch.cuda.stream(stream):
+        for i in range(args.warmup):
+            graphs[i % COPIES].replay()
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    t_wall0 = time.perf_counter()
+    with torch.cuda.stream(stream):
+        ev0.record(stream)
+        for i in range(args.steps):
+            graphs[i % COPIES].replay()
+        ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall0
+    ms_per_step = ev0.elapsed_time(ev1) / args.steps
+    value = step_bytes / (ms_per_step * 1e-3) / 1e9
+    print("timed %d steps: %.3f ms/step, %.1f GB/s effective weight (wall %.2fs)"
+          % (args.steps, ms_per_step, value, wall), file=sys.stderr, flush=True)
+
+    # ---- per-call breakdown (events around each call, rotating copies) -------------
+    reps = 8
+    breakdown = []
+    with torch.cuda.stream(stream):
+        for (m, mname, mode, li) in calls:
+            evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                   for _ in range(reps)]
+            for r in range(reps):
+                evs[r][0].record(stream)
+                run_call(r % COPIES, m, mode, li)
+                evs[r][1].record(stream)
+            stream.synchronize()
+            ts = sorted(a.elapsed_time(b) for a, b in evs)
+            t = ts[len(ts) // 2] * 1e-3
+            name, n, k = layers[li]
+            wb = weight_bytes(mode, li)
+            alg = wb + 2 * m * k + 2 * m * n
+            flops = 2.0 * m * n * k
+            bound_t = max(alg / (HBM_PEAK_GBS * 1e9), flops / (MFMA_F16_TFLOPS * 1e12))
+            breakdown.append({"layer": name, "M": m, "mode": mname, "us": round(t * 1e6, 2),
+                              "eff_weight_GBs": round(wb / t / 1e9, 1),
+                              "alg_GBs": round(alg / t / 1e9, 1),
+                              "TFLOPs": round(flops / t / 1e12, 2),
+                              "roofline_frac": round(bound_t / t, 3)})
+
+    # ---- dominant call: back-to-back launches between events ----------------------
+    dom = max(breakdown, key=lambda b: b["us"])
+    dm, dmode = dom["M"], dps.MODE_FAST if dom["mode"] == "fast" else dps.MODE_FULL
+    dli = [l[0] for l in layers].index(dom["layer"])
+    _, dn, dk = layers[dli]
+    g_dom = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g_dom, stream=stream):
+        for r in range(args.roofline_reps):
+            run_call(r % COPIES, dm, dmode, dli)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        g_dom.replay()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        g_dom.replay()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    t_launch = e0.elapsed_time(e1) * 1e-3 / args.roofline_reps
+    alg_bytes = weight_bytes(dmode, dli) + 2 * dm * dk + 2 * dm * dn
+    flops = 2.0 * dm * dn * dk
+    hbm_t = alg_bytes / (HBM_PEAK_GBS * 1e9)
+    mfma_t = flops / (MFMA_F16_TFLOPS * 1e12)
+    if hbm_t >= mfma_t:
+        roof = {"bound": "hbm", "achieved": round(alg_bytes / t_launch / 1e9, 1),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    else:
+        roof = {"bound": "mfma", "achieved": round(flops / t_launch / 1e12, 1),
+                "peak": MFMA_F16_TFLOPS, "unit": "TFLOP/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["traffic"] = None
+    roof["kernel"] = ("%s layer %dx%d, M=%d, %s mode" % (dom["layer"], dn, dk, dm, dom["mode"]))
+    roof["us_per_launch"] = round(t_launch * 1e6, 2)
+    roof["algorithmic_bytes_per_launch"] = alg_bytes
+
+    # ---- secondary: prefill TFLOPS (FP8 fast, FP16 full) ---------------------------
+    secondary = {}
+    if not args.no_secondary:
+        secondary = prefill_secondary(torch, dps, workloads, copies[0], layers, stream)
+    del graphs, g_dom
+    torch.cuda.synchronize()
+
+    # ---- CPU oracle baseline --------------------------------------------------------
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(workloads)
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {"workload": "decode_h4096",
+                   "layers": {name: [n, k] for name, n, k in layers},
+                   "M": list(ms), "modes": ["fast", "full"], "chunk_bytes": 1 << LOG2_CHUNK,
+                   "weight_copies_rotated": COPIES,
+                   "calls_per_step": len(calls), "weight_bytes_per_step": step_bytes},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "breakdown": breakdown,
+        "secondary": secondary,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def prefill_secondary(torch, dps, workloads, nws, layers, stream):
+    """Prefill (M = 2048) over the layer set: fast mode on FP8 matrix cores
+    (row-quantized activations), full mode on FP16 matrix cores."""
+    dev = torch.device("cuda:0")
+    m = 2048
+    res = {}
+    with torch.cuda.stream(stream):
+        xs = {k: workloads.activations_fp16(m, k, seed=k + 5, outlier_frac=0.01,
+                                            outlier_scale=20.0, device=dev)
+              for k in sorted({k for _, _, k in layers})}
+        ys = {n: torch.empty((m, n), dtype=torch.float16, device=dev)
+              for n in sorted({n for _, n, _ in layers})}
+        need = max(dps.workspace_bytes(mode, act, m, n, k) for _, n, k in layers
+                   for mode, act in ((dps.MODE_FAST, 1), (dps.MODE_FULL, 0)))
+        ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+        for label, mode, act, peak in (("fast_fp8", dps.MODE_FAST, "fp8", MFMA_FP8_TFLOPS),
+                                       ("full_f16", dps.MODE_FULL, "fp16", MFMA_F16_TFLOPS)):
+            def one():
+                for li, (name, n, k) in enumerate(layers):
+                    dps.linear(xs[k], nws[li], mode, act=act, out=ys[n], workspace=ws)
+            one()
+            stream.synchronize()
+            reps = 5
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                one()
+            e1.record(stream)
+            stream.synchronize()
+            t = e0.elapsed_time(e1) * 1e-3 / reps
+            flops = sum(2.0 * m * n * k for _, n, k in layers)
+            res[label] = {"M": m, "ms": round(t * 1e3, 3), "TFLOPs": round(flops / t / 1e12, 1),
+                          "frac_of_peak": round(flops / t / 1e12 / peak, 3)}
+    return res
+
+
+def cpu_baseline(workloads):
+    """The CPU oracle on a bounded sample of the same workload: the O layer
+    (4096x4096) at every M in {1, 8, 32, 128, 256}, fast and full mode."""
+    import numpy as np
+
+    import oracle
+
+    n = k = 4096
+    w = workloads.weight_fp16(n, k, seed=77).numpy().view(np.uint16)
+    c = 1 << LOG2_CHUNK
+    n_chunks = -(-n * k // c)
+    res = oracle.Residual(np.zeros(n_chunks * c, np.uint8), np.arange(n_chunks, dtype=np.int32),
+                          LOG2_CHUNK)
+    hi = oracle.split(w, res)
+    t0 = time.perf_counter()
+    wbytes = 0
+    for m in workloads.DECODE_M:
+        x = workloads.activations_fp16(m, k, seed=m).numpy().view(np.uint16)
+        oracle.linear(oracle.FAST, x, hi, None)
+        oracle.linear(oracle.FULL, x, hi, res)
+        wbytes += n * k * 3
+    t = time.perf_counter() - t0
+    return {"value": round(wbytes / t / 1e9, 4), "unit": "GB/s", "cores": oracle.num_threads(),
+            "kind": "oracle", "seconds": round(t, 2),
+            "sample": "O layer 4096x4096 at M in {1,8,32,128,256}, fast and full mode "
+                      "(fp64 oracle, OpenMP over output features)"}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,188 @@
+/*
+ * dps.h -- C ABI of libdps, the MI355X (gfx950) nested-precision linear layer
+ * of Dual-Mode Precision Serving (DPS).
+ *
+ * The method (Sec. IV of the paper) keeps every FP16 weight as two bytes held
+ * in two places:
+ *   - the upper byte -- sign, all five exponent bits and the two leading
+ *     mantissa bits, i.e. the FP16 value truncated to FP8 E5M2 -- in a
+ *     persistent region (Sec. IV-B "Persistent Region");
+ *   - the lower byte, the residual, in a shared region whose physical memory
+ *     is made of relocatable units that may instead hold paged KV-cache
+ *     blocks (Sec. IV-B "Shared Region"; Sec. IV-C, restoration paragraph).
+ * Full mode rebuilds the original FP16 weights from both bytes during the
+ * product; fast mode reads the upper byte only and never touches the
+ * residual, whose memory may hold KV data at that time (Sec. IV-C "Overall
+ * concept").  One kernel family serves dense layers and MoE expert groups
+ * (Sec. IV-C, GroupedGEMM paragraph).
+ *
+ * Conventions for every entry point:
+ *   - Tensor pointers are HIP device memory owned by the caller; the library
+ *     never allocates, frees, synchronizes or keeps a pointer after return.
+ *     Buffers must stay alive until the enqueued work completes.
+ *   - `stream` is a hipStream_t (NULL = the legacy default stream).  All work
+ *     is enqueued on it, asynchronously.
+ *   - Arguments are validated on the host before anything is enqueued; on
+ *     any error nothing is launched and a status other than DPS_OK is
+ *     returned (dps_last_error() then names the offending argument).
+ *   - Faults inside kernels surface at the caller's next synchronization.
+ *   - Calls are reentrant.  Two calls that share a workspace must be
+ *     ordered (same stream, or synchronized).
+ *   - Matrices are row-major.  Y = X . W^T: X is [m][k], W is [n][k],
+ *     Y is [m][n].
+ */
+#ifndef DPS_H
+#define DPS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    DPS_OK = 0,
+    DPS_ERR_INVALID_ARG = 1, /* null/negative/inconsistent argument         */
+    DPS_ERR_ALIGNMENT = 2,   /* a tensor pointer is not 16-byte aligned      */
+    DPS_ERR_UNSUPPORTED = 3, /* valid request this build does not implement  */
+    DPS_ERR_WORKSPACE = 4,   /* workspace missing or smaller than required   */
+    DPS_ERR_HIP = 5          /* the HIP runtime reported an error on launch  */
+} dps_status;
+
+/* Precision mode of one call; a whole forward pass runs in one mode
+ * (batch-aligned switching, Sec. IV-C "Overall concept" and "Granularity of
+ * the precision switch"). */
+typedef enum {
+    DPS_MODE_FULL = 0, /* FP16 rebuilt from upper byte + residual byte       */
+    DPS_MODE_FAST = 1  /* FP8 E5M2 upper byte only; residual never read      */
+} dps_mode;
+
+/* Nested encodings (Sec. IV-B "Persistent Region"): E5M2 keeps all five
+ * exponent bits.  The E4M3 variant for small-range layers is not built. */
+enum { DPS_ENC_E5M2 = 0 };
+
+/* Activation handling, `flags` argument of the linear calls.
+ *   DPS_ACT_FP16: activations stay FP16; weights enter the FP16 matrix cores
+ *     (fast mode: the E5M2 byte is the upper byte of an exact FP16 word).
+ *   DPS_ACT_FP8_ROWSCALE (fast mode only): each activation row is first
+ *     quantized to OCP FP8 E4M3 with its own power-of-two scale (see
+ *     dps_quant_rows_e4m3) and the product runs on the FP8 matrix cores with
+ *     the weights' E5M2 byte as the second operand. */
+enum { DPS_ACT_FP16 = 0u, DPS_ACT_FP8_ROWSCALE = 1u };
+
+/* Residual plane of one weight tensor (Sec. IV-B "Shared Region": physical
+ * units behind one contiguous virtual tensor).  The residual bytes form a
+ * logical stream in the weight's row-major element order; the stream is cut
+ * into chunks of C = 2^log2_chunk bytes and logical chunk c is stored in
+ * pool slot slots[c], i.e. logical byte i lives at
+ *     pool + slots[i >> log2_chunk] * C + (i & (C - 1)).
+ * Other pool slots may hold anything (e.g. paged KV blocks).
+ *   pool        device, 16-byte aligned, pool_bytes bytes.
+ *   pool_bytes  >= C; slots address pool_bytes / C whole chunks.
+ *   slots       device int32[n_chunks].  Entries should be distinct; an entry
+ *               outside [0, pool_bytes / C) is never dereferenced: reads
+ *               through it return zero bytes and writes through it are
+ *               dropped.
+ *   n_chunks    >= ceil(numel / C) for the tensor it describes.
+ *   log2_chunk  4..30 (chunks of 16 B .. 1 GiB).
+ * In fast mode the whole descriptor is ignored and may be zero/NULL. */
+typedef struct {
+    uint8_t *pool;
+    int64_t pool_bytes;
+    const int32_t *slots;
+    int64_t n_chunks;
+    int32_t log2_chunk;
+} dps_residual;
+
+/* A nested weight: `experts` stacked [n][k] matrices (experts = 1 for a dense
+ * layer).  Element (e, r, c) is logical element (e * n + r) * k + c of both
+ * the upper-byte plane `hi` and the residual stream.
+ *   hi   device uint8[experts][n][k], 16-byte aligned.
+ *   k    multiple of 16, > 0.   n > 0.   experts >= 1.
+ *   enc  DPS_ENC_E5M2. */
+typedef struct {
+    const uint8_t *hi;
+    dps_residual res;
+    int64_t experts;
+    int64_t n;
+    int64_t k;
+    int32_t enc;
+} dps_weight;
+
+/* Split FP16 weights into the nested pair (Sec. IV-A "Dynamic Networks and a
+ * Nested Model"; Sec. IV-B "Persistent Region"): hi[i] = w[i] >> 8 (the E5M2
+ * truncation), residual byte i = w[i] & 0xFF written through the chunk table.
+ *   w      device uint16 (FP16 bit patterns) [numel], 16-byte aligned.
+ *   hi     device uint8[numel], 16-byte aligned.
+ *   res    host pointer to the residual descriptor (its pool is written).
+ * numel == 0 is a no-op.  Bit-exact. */
+dps_status dps_split(const uint16_t *w, int64_t numel, uint8_t *hi,
+                     const dps_residual *res, void *stream);
+
+/* Rebuild the original FP16 words (Sec. IV-C "Overall concept": full mode
+ * reconstructs the original FP16 values): w_out[i] = hi[i] << 8 | residual
+ * byte i.  Same layouts as dps_split.  Bit-exact. */
+dps_status dps_merge(const uint8_t *hi, const dps_residual *res, int64_t numel,
+                     uint16_t *w_out, void *stream);
+
+/* Per-row FP8 quantization of activations for fast-mode prefill (this
+ * build's reading of the dynamic per-token activations of Sec. V-A
+ * "Baselines"): for row r, a = max_k |x[r][k]|, scale[r] = the smallest power
+ * of two s with a <= 448 * s (1 when a == 0), xq[r][k] = OCP E4M3 nearest to
+ * x[r][k] / s, ties to even.  The division is exact, so this is bit-exact.
+ *   x      device FP16 [m][k], 16-byte aligned, finite values.
+ *   xq     device uint8 [m][k] (E4M3 codes), 16-byte aligned.
+ *   scale  device float [m].
+ * k must be a multiple of 16. */
+dps_status dps_quant_rows_e4m3(const uint16_t *x, int64_t m, int64_t k,
+                               uint8_t *xq, float *scale, void *stream);
+
+/* Workspace bytes that dps_linear (experts == 1, rows = m) or
+ * dps_linear_grouped (rows = total routed rows) needs for these arguments on
+ * the current device.  0 means no workspace is needed.  The workspace is
+ * scratch: its contents on entry do not matter. */
+size_t dps_workspace_bytes(int mode, uint32_t flags, int64_t rows, int64_t n,
+                           int64_t k, int64_t experts);
+
+/* Nested linear layer, dense (Sec. IV-C, GroupedGEMM paragraph, dense case):
+ *   full mode: Y = X . merge(hi, residual)^T   (exact FP16 weights)
+ *   fast mode: Y = X . E5M2(hi)^T              (residual not read)
+ * fp32 accumulation, Y rounded to FP16 (round to nearest even).
+ *   mode   DPS_MODE_FULL or DPS_MODE_FAST.
+ *   flags  DPS_ACT_FP16, or DPS_ACT_FP8_ROWSCALE with DPS_MODE_FAST.
+ *   x      device FP16 [m][w->k], 16-byte aligned.   m >= 0 (0: no-op).
+ *   w      host pointer; w->experts must be 1.
+ *   y      device FP16 [m][w->n], 16-byte aligned.
+ *   ws     device scratch of ws_bytes >= dps_workspace_bytes(...), 256-byte
+ *          aligned; may be NULL when that is 0. */
+dps_status dps_linear(int mode, uint32_t flags, const uint16_t *x, int64_t m,
+                      const dps_weight *w, uint16_t *y, void *ws, size_t ws_bytes,
+                      void *stream);
+
+/* Grouped nested linear for MoE experts (Sec. IV-C, GroupedGEMM paragraph,
+ * MoE case): rows [offsets[e], offsets[e+1]) of x_sorted are multiplied by
+ * expert e's weights; Y rows follow the same order.
+ *   x_sorted  device FP16 [rows][w->k], rows grouped by expert.
+ *   offsets   device int32[w->experts + 1]; offsets[0] = 0, nondecreasing,
+ *             offsets[experts] = rows.  Read on the device only, so the call
+ *             does not synchronize; rows outside [0, rows) are never touched
+ *             even if the array breaks this contract.
+ *   y         device FP16 [rows][w->n].
+ * Other arguments as dps_linear.  DPS_ACT_FP8_ROWSCALE is not supported
+ * here (DPS_ERR_UNSUPPORTED). */
+dps_status dps_linear_grouped(int mode, uint32_t flags, const uint16_t *x_sorted,
+                              const int32_t *offsets, int64_t rows, const dps_weight *w,
+                              uint16_t *y, void *ws, size_t ws_bytes, void *stream);
+
+/* Static description of a status code. */
+const char *dps_status_str(dps_status s);
+
+/* Detail of the last error returned on the calling thread ("" if none). */
+const char *dps_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DPS_H */

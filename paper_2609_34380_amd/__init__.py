@@ -13,10 +13,7 @@ __all__ = ["dps", "workloads"]
 
 
 def __getattr__(name):
-    if name == "dps":
-        from . import dps as _dps
-        return _dps
-    if name == "workloads":
-        from . import workloads as _w
-        return _w
+    if name in __all__:
+        import importlib
+        return importlib.import_module(__name__ + "." + name)
     raise AttributeError(name)

@@ -1,0 +1,332 @@
+// dps_api.hip -- the C ABI of libdps: argument validation, kernel planning and
+// launches.  Nothing here allocates device memory or synchronizes.
+#include <stdio.h>
+#include <string.h>
+
+#include "dps.h"
+#include "dps_internal.h"
+
+#define DPS_EXPORT extern "C" __attribute__((visibility("default")))
+
+namespace dps {
+int skinny_rows_per_block(int variant);
+int skinny_k_per_batch(int variant);
+int gemm_rows_per_block();
+int gemm_tokens_per_block();
+}  // namespace dps
+
+namespace {
+
+thread_local char g_err[256] = "";
+
+dps_status fail(dps_status s, const char *fmt, const char *what)
+{
+    snprintf(g_err, sizeof(g_err), fmt, what);
+    return s;
+}
+
+#define REQUIRE(cond, status, what)                        \
+    do {                                                   \
+        if (!(cond))                                       \
+            return fail(status, "%s", what);               \
+    } while (0)
+
+bool aligned(const void *p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+int64_t round_up(int64_t a, int64_t b) { return cdiv(a, b) * b; }
+size_t align256(int64_t bytes) { return (size_t)round_up(bytes, 256); }
+
+int current_cu_count()
+{
+    static int cache[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0)
+        return 256;
+    if (dev < 64 && cache[dev] > 0)
+        return cache[dev];
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+        cus = 256;
+    if (dev < 64)
+        cache[dev] = cus;
+    return cus;
+}
+
+// Residual descriptor checks shared by split, merge and full-mode linears.
+dps_status check_residual(const dps_residual *r, int64_t numel)
+{
+    REQUIRE(r != nullptr, DPS_ERR_INVALID_ARG, "residual descriptor is NULL");
+    REQUIRE(r->pool != nullptr, DPS_ERR_INVALID_ARG, "residual pool is NULL");
+    REQUIRE(r->slots != nullptr, DPS_ERR_INVALID_ARG, "residual slot table is NULL");
+    REQUIRE(aligned(r->pool, 16), DPS_ERR_ALIGNMENT, "residual pool is not 16-byte aligned");
+    REQUIRE(aligned(r->slots, 4), DPS_ERR_ALIGNMENT, "residual slot table is not 4-byte aligned");
+    REQUIRE(r->log2_chunk >= 4 && r->log2_chunk <= 30, DPS_ERR_INVALID_ARG,
+            "log2_chunk must be in 4..30");
+    const int64_t c = int64_t(1) << r->log2_chunk;
+    REQUIRE(r->pool_bytes >= c, DPS_ERR_INVALID_ARG, "pool_bytes is smaller than one chunk");
+    REQUIRE(r->n_chunks >= 0, DPS_ERR_INVALID_ARG, "n_chunks is negative");
+    REQUIRE(r->n_chunks >= cdiv(numel, c), DPS_ERR_INVALID_ARG,
+            "n_chunks does not cover the tensor");
+    return DPS_OK;
+}
+
+dps::ResidualView view_of(const dps_residual *r)
+{
+    dps::ResidualView v;
+    v.pool = r->pool;
+    v.slots = r->slots;
+    v.log2c = r->log2_chunk;
+    v.n_pool_slots = r->pool_bytes >> r->log2_chunk;
+    v.n_chunks = r->n_chunks;
+    return v;
+}
+
+dps_status launched(hipError_t e)
+{
+    if (e != hipSuccess) {
+        snprintf(g_err, sizeof(g_err), "HIP launch failed: %s", hipGetErrorString(e));
+        return DPS_ERR_HIP;
+    }
+    return DPS_OK;
+}
+
+dps_status check_weight(const dps_weight *w, int mode)
+{
+    REQUIRE(w != nullptr, DPS_ERR_INVALID_ARG, "weight descriptor is NULL");
+    REQUIRE(w->enc == DPS_ENC_E5M2, DPS_ERR_UNSUPPORTED, "only the E5M2 nested encoding is built");
+    REQUIRE(w->experts >= 1 && w->experts <= 65535, DPS_ERR_INVALID_ARG,
+            "experts must be in 1..65535");
+    REQUIRE(w->n > 0, DPS_ERR_INVALID_ARG, "n must be positive");
+    REQUIRE(w->k > 0 && w->k % 16 == 0, DPS_ERR_INVALID_ARG, "k must be a positive multiple of 16");
+    REQUIRE(w->hi != nullptr, DPS_ERR_INVALID_ARG, "upper-byte plane is NULL");
+    REQUIRE(aligned(w->hi, 16), DPS_ERR_ALIGNMENT, "upper-byte plane is not 16-byte aligned");
+    if (mode == DPS_MODE_FULL) {
+        dps_status s = check_residual(&w->res, w->experts * w->n * w->k);
+        if (s != DPS_OK)
+            return s;
+    }
+    return DPS_OK;
+}
+
+}  // namespace
+
+namespace dps {
+
+LinearPlan plan_linear(int mode, uint32_t flags, int64_t rows, int64_t n, int64_t k,
+                       int64_t experts, int log2c, int cu_count, bool grouped)
+{
+    LinearPlan p;
+    memset(&p, 0, sizeof(p));
+    const int64_t target = 2 * (int64_t)cu_count;  // blocks we aim to have in flight
+    const int64_t rows_per_expert = grouped ? cdiv(rows, experts) : rows;
+    if (flags & DPS_ACT_FP8_ROWSCALE) {
+        p.kind = KIND_GEMM_FP8;
+        const int64_t tiles = cdiv(n, gemm_rows_per_block()) * cdiv(rows, gemm_tokens_per_block());
+        int64_t s = cdiv(target, tiles);
+        const int64_t smax = k / 1024 > 1 ? k / 1024 : 1;
+        s = s < 1 ? 1 : (s > smax ? smax : s);
+        p.ksplit = round_up(cdiv(k, s), 128);
+        p.splits = (int)cdiv(k, p.ksplit);
+        p.ws_quant = align256(rows * k) + align256(rows * 4);
+    } else if (rows_per_expert <= 64) {
+        p.kind = KIND_SKINNY;
+        p.variant = 0;
+        const int64_t kpb = skinny_k_per_batch(p.variant);
+        const int64_t blocks = cdiv(n, skinny_rows_per_block(p.variant)) * experts;
+        int64_t s = cdiv(target, blocks);
+        const int64_t smax = k / kpb > 1 ? k / kpb : 1;
+        s = s < 1 ? 1 : (s > smax ? smax : s);
+        p.ksplit = round_up(cdiv(k, s), kpb);
+        p.splits = (int)cdiv(k, p.ksplit);
+    } else {
+        p.kind = KIND_GEMM_F16;
+        const int64_t tiles =
+            cdiv(n, gemm_rows_per_block()) * cdiv(rows, gemm_tokens_per_block());
+        int64_t s = cdiv(target, tiles);
+        const int64_t smax = k / 512 > 1 ? k / 512 : 1;
+        s = s < 1 ? 1 : (s > smax ? smax : s);
+        p.ksplit = round_up(cdiv(k, s), 64);
+        p.splits = (int)cdiv(k, p.ksplit);
+    }
+    p.range_addr = mode == MODE_FULL && p.ksplit <= (int64_t(1) << log2c);
+    p.ws_partial = p.splits > 1 ? align256((int64_t)p.splits * rows * n * 4) : 0;
+    return p;
+}
+
+}  // namespace dps
+
+DPS_EXPORT const char *dps_status_str(dps_status s)
+{
+    switch (s) {
+    case DPS_OK: return "ok";
+    case DPS_ERR_INVALID_ARG: return "invalid argument";
+    case DPS_ERR_ALIGNMENT: return "misaligned pointer";
+    case DPS_ERR_UNSUPPORTED: return "unsupported";
+    case DPS_ERR_WORKSPACE: return "workspace too small";
+    case DPS_ERR_HIP: return "HIP error";
+    }
+    return "unknown status";
+}
+
+DPS_EXPORT const char *dps_last_error(void) { return g_err; }
+
+DPS_EXPORT dps_status dps_split(const uint16_t *w, int64_t numel, uint8_t *hi,
+                                const dps_residual *res, void *stream)
+{
+    g_err[0] = 0;
+    REQUIRE(numel >= 0, DPS_ERR_INVALID_ARG, "numel is negative");
+    if (numel == 0)
+        return DPS_OK;
+    REQUIRE(w != nullptr && hi != nullptr, DPS_ERR_INVALID_ARG, "w or hi is NULL");
+    REQUIRE(aligned(w, 16) && aligned(hi, 16), DPS_ERR_ALIGNMENT, "w or hi is not 16-byte aligned");
+    dps_status s = check_residual(res, numel);
+    if (s != DPS_OK)
+        return s;
+    return launched(dps::launch_split(w, numel, hi, view_of(res), (hipStream_t)stream));
+}
+
+DPS_EXPORT dps_status dps_merge(const uint8_t *hi, const dps_residual *res, int64_t numel,
+                                uint16_t *w_out, void *stream)
+{
+    g_err[0] = 0;
+    REQUIRE(numel >= 0, DPS_ERR_INVALID_ARG, "numel is negative");
+    if (numel == 0)
+        return DPS_OK;
+    REQUIRE(w_out != nullptr && hi != nullptr, DPS_ERR_INVALID_ARG, "hi or w_out is NULL");
+    REQUIRE(aligned(w_out, 16) && aligned(hi, 16), DPS_ERR_ALIGNMENT,
+            "hi or w_out is not 16-byte aligned");
+    dps_status s = check_residual(res, numel);
+    if (s != DPS_OK)
+        return s;
+    return launched(dps::launch_merge(hi, view_of(res), numel, w_out, (hipStream_t)stream));
+}
+
+DPS_EXPORT dps_status dps_quant_rows_e4m3(const uint16_t *x, int64_t m, int64_t k, uint8_t *xq,
+                                          float *scale, void *stream)
+{
+    g_err[0] = 0;
+    REQUIRE(m >= 0 && m <= 0x7fffffff, DPS_ERR_INVALID_ARG, "m must be in 0..2^31-1");
+    REQUIRE(k > 0 && k % 16 == 0, DPS_ERR_INVALID_ARG, "k must be a positive multiple of 16");
+    if (m == 0)
+        return DPS_OK;
+    REQUIRE(x != nullptr && xq != nullptr && scale != nullptr, DPS_ERR_INVALID_ARG,
+            "x, xq or scale is NULL");
+    REQUIRE(aligned(x, 16) && aligned(xq, 16) && aligned(scale, 4), DPS_ERR_ALIGNMENT,
+            "x/xq not 16-byte aligned or scale not 4-byte aligned");
+    return launched(dps::launch_quant_rows(x, m, k, xq, scale, (hipStream_t)stream));
+}
+
+DPS_EXPORT size_t dps_workspace_bytes(int mode, uint32_t flags, int64_t rows, int64_t n,
+                                      int64_t k, int64_t experts)
+{
+    if (rows <= 0 || n <= 0 || k <= 0 || experts < 1)
+        return 0;
+    const dps::LinearPlan p =
+        dps::plan_linear(mode, flags, rows, n, k, experts, 30, current_cu_count(), experts > 1);
+    return p.ws_partial + p.ws_quant;
+}
+
+namespace {
+
+dps_status run_linear(int mode, uint32_t flags, const uint16_t *x, const int32_t *offsets,
+                      int64_t rows, const dps_weight *w, uint16_t *y, void *ws, size_t ws_bytes,
+                      hipStream_t stream, bool grouped)
+{
+    const dps::LinearPlan plan =
+        dps::plan_linear(mode, flags, rows, w->n, w->k, w->experts,
+                         mode == DPS_MODE_FULL ? w->res.log2_chunk : 30, current_cu_count(),
+                         grouped);
+    const size_t need = plan.ws_partial + plan.ws_quant;
+    if (need > 0) {
+        REQUIRE(ws != nullptr && ws_bytes >= need, DPS_ERR_WORKSPACE,
+                "workspace is smaller than dps_workspace_bytes()");
+        REQUIRE(aligned(ws, 256), DPS_ERR_ALIGNMENT, "workspace is not 256-byte aligned");
+    }
+    const int64_t token_tiles = (rows + dps::gemm_tokens_per_block() - 1) /
+                                    dps::gemm_tokens_per_block() + (grouped ? w->experts : 0);
+    REQUIRE(token_tiles <= 65535, DPS_ERR_UNSUPPORTED, "too many rows for one call");
+    REQUIRE(plan.splits <= 65535, DPS_ERR_UNSUPPORTED, "k too large for one call");
+
+    float *partial = plan.splits > 1 ? static_cast<float *>(ws) : nullptr;
+    dps::LinearProblem p;
+    p.mode = mode;
+    p.x = x;
+    p.offsets = offsets;
+    p.rows = rows;
+    p.experts = w->experts;
+    p.n = w->n;
+    p.k = w->k;
+    p.hi = w->hi;
+    p.res = mode == DPS_MODE_FULL ? view_of(&w->res) : dps::ResidualView{nullptr, nullptr, 0, 0, 0};
+    p.y = y;
+
+    dps_status st;
+    if (plan.kind == dps::KIND_GEMM_FP8) {
+        uint8_t *xq = static_cast<uint8_t *>(ws) + plan.ws_partial;
+        float *scale = reinterpret_cast<float *>(xq + align256(rows * w->k));
+        st = launched(dps::launch_quant_rows(x, rows, w->k, xq, scale, stream));
+        if (st != DPS_OK)
+            return st;
+        st = launched(dps::launch_gemm_fp8(xq, scale, rows, w->n, w->k, w->hi, y, plan, partial,
+                                           stream));
+    } else if (plan.kind == dps::KIND_SKINNY) {
+        st = launched(dps::launch_skinny(p, plan, partial, stream));
+    } else {
+        st = launched(dps::launch_gemm_f16(p, plan, partial, stream));
+    }
+    if (st != DPS_OK || plan.splits == 1)
+        return st;
+    return launched(dps::launch_splitk_reduce(partial, plan.splits, rows, w->n, y, stream));
+}
+
+}  // namespace
+
+DPS_EXPORT dps_status dps_linear(int mode, uint32_t flags, const uint16_t *x, int64_t m,
+                                 const dps_weight *w, uint16_t *y, void *ws, size_t ws_bytes,
+                                 void *stream)
+{
+    g_err[0] = 0;
+    REQUIRE(mode == DPS_MODE_FULL || mode == DPS_MODE_FAST, DPS_ERR_INVALID_ARG, "unknown mode");
+    REQUIRE(flags == DPS_ACT_FP16 || flags == DPS_ACT_FP8_ROWSCALE, DPS_ERR_INVALID_ARG,
+            "unknown flags");
+    REQUIRE(!(flags == DPS_ACT_FP8_ROWSCALE && mode != DPS_MODE_FAST), DPS_ERR_INVALID_ARG,
+            "FP8 activations need fast mode");
+    dps_status s = check_weight(w, mode);
+    if (s != DPS_OK)
+        return s;
+    REQUIRE(w->experts == 1, DPS_ERR_INVALID_ARG, "dps_linear takes a dense weight (experts == 1)");
+    REQUIRE(m >= 0, DPS_ERR_INVALID_ARG, "m is negative");
+    if (m == 0)
+        return DPS_OK;
+    REQUIRE(x != nullptr && y != nullptr, DPS_ERR_INVALID_ARG, "x or y is NULL");
+    REQUIRE(aligned(x, 16) && aligned(y, 16), DPS_ERR_ALIGNMENT, "x or y is not 16-byte aligned");
+    return run_linear(mode, flags, x, nullptr, m, w, y, ws, ws_bytes, (hipStream_t)stream, false);
+}
+
+DPS_EXPORT dps_status dps_linear_grouped(int mode, uint32_t flags, const uint16_t *x_sorted,
+                                         const int32_t *offsets, int64_t rows,
+                                         const dps_weight *w, uint16_t *y, void *ws,
+                                         size_t ws_bytes, void *stream)
+{
+    g_err[0] = 0;
+    REQUIRE(mode == DPS_MODE_FULL || mode == DPS_MODE_FAST, DPS_ERR_INVALID_ARG, "unknown mode");
+    REQUIRE(flags == DPS_ACT_FP16 || flags == DPS_ACT_FP8_ROWSCALE, DPS_ERR_INVALID_ARG,
+            "unknown flags");
+    REQUIRE(flags == DPS_ACT_FP16, DPS_ERR_UNSUPPORTED,
+            "grouped linear supports FP16 activations only");
+    dps_status s = check_weight(w, mode);
+    if (s != DPS_OK)
+        return s;
+    REQUIRE(rows >= 0, DPS_ERR_INVALID_ARG, "rows is negative");
+    if (rows == 0)
+        return DPS_OK;
+    REQUIRE(offsets != nullptr, DPS_ERR_INVALID_ARG, "offsets is NULL");
+    REQUIRE(aligned(offsets, 4), DPS_ERR_ALIGNMENT, "offsets is not 4-byte aligned");
+    REQUIRE(x_sorted != nullptr && y != nullptr, DPS_ERR_INVALID_ARG, "x_sorted or y is NULL");
+    REQUIRE(aligned(x_sorted, 16) && aligned(y, 16), DPS_ERR_ALIGNMENT,
+            "x_sorted or y is not 16-byte aligned");
+    return run_linear(mode, flags, x_sorted, offsets, rows, w, y, ws, ws_bytes,
+                      (hipStream_t)stream, true);
+}

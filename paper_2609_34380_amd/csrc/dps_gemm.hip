@@ -1,0 +1,413 @@
+// dps_gemm.hip -- prefill-shaped nested linear on the matrix cores (gfx950).
+//
+// gemm_f16_kernel: Y = X . W^T with W's upper-byte tile (and, in full mode,
+// its residual-byte tile) staged in LDS as bytes -- half the LDS bytes of an
+// FP16 tile each -- and merged into FP16 operands in registers right before
+// v_mfma_f32_16x16x32_f16 (Sec. IV-C: reconstruction during computation).
+// gemm_fp8_kernel: fast mode with FP8 activations; the E5M2 upper bytes are
+// used as-is as the A operand of v_mfma_f32_16x16x128_f8f6f4 against E4M3
+// activations, and the row scale is applied to the fp32 accumulator.
+//
+// Block tile 128 (weight rows) x 128 (tokens), 4 waves in a 2 x 2 grid, each
+// wave 64 x 64 = 4 x 4 MFMA tiles.  Global -> register -> LDS double
+// buffering: tile t+1 is fetched while tile t is multiplied, one barrier per
+// K tile.  The weight rows are the MFMA A operand, so a lane ends up holding
+// four consecutive output features of one token (8-byte FP16 stores).
+// Grouped (MoE) calls map grid.y onto (expert, token tile) by scanning the
+// device offsets, so only `experts` blocks at most find no work.
+#include "dps_internal.h"
+
+namespace dps {
+
+namespace {
+
+constexpr int BM = 128;  // tokens per block
+constexpr int BN = 128;  // weight rows per block
+
+struct GemmArgs {
+    const void *x;  // FP16 [rows][k] or E4M3 [rows][k]
+    const int32_t *offsets;
+    int64_t rows;
+    int64_t experts;
+    const uint8_t *hi;
+    ResidualView res;
+    int64_t n, k, ksplit;
+    int splits;
+    uint16_t *y;
+    float *partial;
+    const float *scale;
+};
+
+// Token range of this block: dense calls use grid.y as the token tile;
+// grouped calls walk the experts' tile counts.  Returns false if no work.
+__device__ __forceinline__ bool block_rows(const GemmArgs &a, int64_t &e, int64_t &m0,
+                                           int64_t &m1)
+{
+    const int64_t t = blockIdx.y;
+    if (!a.offsets) {
+        e = 0;
+        m0 = t * BM;
+        m1 = m0 + BM < a.rows ? m0 + BM : a.rows;
+        return m0 < m1;
+    }
+    int64_t cum = 0;
+    int64_t prev = 0;
+    for (int64_t ex = 0; ex < a.experts; ++ex) {
+        int64_t o1 = a.offsets[ex + 1];
+        o1 = o1 < prev ? prev : (o1 > a.rows ? a.rows : o1);
+        const int64_t tiles = (o1 - prev + BM - 1) / BM;
+        if (t < cum + tiles) {
+            e = ex;
+            m0 = prev + (t - cum) * BM;
+            m1 = m0 + BM < o1 ? m0 + BM : o1;
+            return true;
+        }
+        cum += tiles;
+        prev = o1;
+    }
+    return false;
+}
+
+__device__ __forceinline__ void store_tile_out(const GemmArgs &a, int s, int64_t m, int64_t n0,
+                                               f32x4 v, int64_t m1)
+{
+    if (m >= m1 || n0 >= a.n)
+        return;
+    if (a.splits == 1) {
+        uint16_t *yp = a.y + m * a.n + n0;
+        if (n0 + 3 < a.n && (a.n & 3) == 0) {
+            typedef _Float16 half4 __attribute__((ext_vector_type(4)));
+            half4 hv = {(_Float16)v.x, (_Float16)v.y, (_Float16)v.z, (_Float16)v.w};
+            *reinterpret_cast<half4 *>(yp) = hv;
+        } else {
+            const float vv[4] = {v.x, v.y, v.z, v.w};
+            for (int r = 0; r < 4 && n0 + r < a.n; ++r)
+                yp[r] = __builtin_bit_cast(uint16_t, (_Float16)vv[r]);
+        }
+    } else {
+        float *pp = a.partial + ((int64_t)s * a.rows + m) * a.n + n0;
+        if (n0 + 3 < a.n && (a.n & 3) == 0) {
+            *reinterpret_cast<f32x4 *>(pp) = v;
+        } else {
+            const float vv[4] = {v.x, v.y, v.z, v.w};
+            for (int r = 0; r < 4 && n0 + r < a.n; ++r)
+                pp[r] = vv[r];
+        }
+    }
+}
+
+// ------------------------------------------------------------------------------
+// FP16 matrix cores, weights merged in registers
+// ------------------------------------------------------------------------------
+constexpr int BK16 = 64;          // K elements per tile
+constexpr int XP16 = BK16 + 8;    // X tile pitch, halfs (144 B)
+constexpr int WP16 = BK16 + 16;   // weight byte tile pitch (80 B)
+
+template <int MODE, bool RANGE>
+__global__ __launch_bounds__(256) void gemm_f16_kernel(GemmArgs a)
+{
+    __shared__ __attribute__((aligned(16))) uint16_t xs[2][BM * XP16];
+    __shared__ __attribute__((aligned(16))) uint8_t hs[2][BN * WP16];
+    __shared__ __attribute__((aligned(16))) uint8_t ls[MODE == MODE_FULL ? 2 : 1][BN * WP16];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int li = lane & 15;
+    const int lg = lane >> 4;
+
+    int64_t e, mrow0, mrow1;
+    if (!block_rows(a, e, mrow0, mrow1))
+        return;
+    const int ntile = blockIdx.x / a.splits;
+    const int s = blockIdx.x % a.splits;
+    const int64_t n0 = (int64_t)ntile * BN;
+    const int64_t kb0 = (int64_t)s * a.ksplit;
+    const int64_t ke = kb0 + a.ksplit < a.k ? kb0 + a.ksplit : a.k;
+    const uint16_t *x = static_cast<const uint16_t *>(a.x);
+
+    // global load assignment (fixed rows per thread)
+    const int64_t xr0 = tid >> 3;                // + 32 * j, j < 4
+    const int xc = (tid & 7) * 8;                // halfs
+    const int64_t wr0 = tid >> 2;                // + 64 * j, j < 2
+    const int wc = (tid & 3) * 16;               // bytes
+    int64_t lrow[2];
+    bool wok[2];
+    RangeResidual rr[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int64_t nr = n0 + wr0 + 64 * j;
+        wok[j] = nr < a.n;
+        lrow[j] = (e * a.n + nr) * a.k;
+        if (MODE == MODE_FULL && RANGE) {
+            rr[j].ok0 = rr[j].ok1 = false;
+            rr[j].delta0 = rr[j].delta1 = 0;
+            rr[j].bnd = 0;
+            if (wok[j] && ke > kb0)
+                rr[j] = range_residual(a.res, lrow[j] + kb0, lrow[j] + ke);
+        }
+    }
+
+    u32x4 xreg[4], hreg[2], lreg[2];
+    auto gload = [&](int64_t kt) {
+        const u32x4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t m = mrow0 + xr0 + 32 * j;
+            xreg[j] = z;
+            if (m < mrow1 && kt + xc < ke)
+                xreg[j] = load16(x + m * a.k + kt + xc);
+        }
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            hreg[j] = z;
+            lreg[j] = z;
+            if (wok[j] && kt + wc < ke) {
+                hreg[j] = load16(a.hi + lrow[j] + kt + wc);
+                if (MODE == MODE_FULL)
+                    lreg[j] = RANGE ? load_lo_range(a.res, rr[j], lrow[j] + kt + wc)
+                                    : load_lo_lookup(a.res, lrow[j] + kt + wc);
+            }
+        }
+    };
+    auto sstore = [&](int b) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            *reinterpret_cast<u32x4 *>(&xs[b][(xr0 + 32 * j) * XP16 + xc]) = xreg[j];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            *reinterpret_cast<u32x4 *>(&hs[b][(wr0 + 64 * j) * WP16 + wc]) = hreg[j];
+            if (MODE == MODE_FULL)
+                *reinterpret_cast<u32x4 *>(&ls[b][(wr0 + 64 * j) * WP16 + wc]) = lreg[j];
+        }
+    };
+
+    const int wn = wave & 1;
+    const int wm = wave >> 1;
+    f32x4 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int64_t ntk = ke > kb0 ? (ke - kb0 + BK16 - 1) / BK16 : 0;
+    if (ntk > 0) {
+        gload(kb0);
+        sstore(0);
+    }
+    __syncthreads();
+    for (int64_t t = 0; t < ntk; ++t) {
+        const int b = (int)(t & 1);
+        if (t + 1 < ntk)
+            gload(kb0 + (t + 1) * BK16);
+        half8 a0[4], a1[4];
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+            const int row = wn * 64 + nt * 16 + li;
+            const u32x4 h = *reinterpret_cast<const u32x4 *>(&hs[b][row * WP16 + lg * 16]);
+            u32x4 l = {0u, 0u, 0u, 0u};
+            if (MODE == MODE_FULL)
+                l = *reinterpret_cast<const u32x4 *>(&ls[b][row * WP16 + lg * 16]);
+            a0[nt] = merge8(h.x, h.y, l.x, l.y);
+            a1[nt] = merge8(h.z, h.w, l.z, l.w);
+        }
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) {
+            const int row = wm * 64 + mt * 16 + li;
+            const half8 b0 = as_half8(*reinterpret_cast<const u32x4 *>(&xs[b][row * XP16 + lg * 16]));
+            const half8 b1 =
+                as_half8(*reinterpret_cast<const u32x4 *>(&xs[b][row * XP16 + lg * 16 + 8]));
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt) {
+                acc[nt][mt] = mfma16x16x32(a0[nt], b0, acc[nt][mt]);
+                acc[nt][mt] = mfma16x16x32(a1[nt], b1, acc[nt][mt]);
+            }
+        }
+        if (t + 1 < ntk)
+            sstore(b ^ 1);
+        __syncthreads();
+    }
+
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+            store_tile_out(a, s, mrow0 + wm * 64 + mt * 16 + li, n0 + wn * 64 + nt * 16 + lg * 4,
+                           acc[nt][mt], mrow1);
+}
+
+// ------------------------------------------------------------------------------
+// FP8 matrix cores: E5M2 weights x E4M3 activations
+// ------------------------------------------------------------------------------
+constexpr int BK8 = 128;        // K elements (= bytes) per tile
+constexpr int P8 = BK8 + 16;    // tile pitch, bytes
+
+__global__ __launch_bounds__(256) void gemm_fp8_kernel(GemmArgs a)
+{
+    __shared__ __attribute__((aligned(16))) uint8_t xs[2][BM * P8];
+    __shared__ __attribute__((aligned(16))) uint8_t hs[2][BN * P8];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int li = lane & 15;
+    const int lg = lane >> 4;
+
+    int64_t e, mrow0, mrow1;
+    if (!block_rows(a, e, mrow0, mrow1))
+        return;
+    const int ntile = blockIdx.x / a.splits;
+    const int s = blockIdx.x % a.splits;
+    const int64_t n0 = (int64_t)ntile * BN;
+    const int64_t kb0 = (int64_t)s * a.ksplit;
+    const int64_t ke = kb0 + a.ksplit < a.k ? kb0 + a.ksplit : a.k;
+    const uint8_t *xq = static_cast<const uint8_t *>(a.x);
+
+    const int64_t r0 = tid >> 3;      // + 32 * j, j < 4 (both tiles)
+    const int c0 = (tid & 7) * 16;    // bytes
+    u32x4 xreg[4], hreg[4];
+    auto gload = [&](int64_t kt) {
+        const u32x4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t m = mrow0 + r0 + 32 * j;
+            const int64_t nr = n0 + r0 + 32 * j;
+            xreg[j] = z;
+            hreg[j] = z;
+            if (kt + c0 < ke) {
+                if (m < mrow1)
+                    xreg[j] = load16(xq + m * a.k + kt + c0);
+                if (nr < a.n)
+                    hreg[j] = load16(a.hi + (e * a.n + nr) * a.k + kt + c0);
+            }
+        }
+    };
+    auto sstore = [&](int b) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            *reinterpret_cast<u32x4 *>(&xs[b][(r0 + 32 * j) * P8 + c0]) = xreg[j];
+            *reinterpret_cast<u32x4 *>(&hs[b][(r0 + 32 * j) * P8 + c0]) = hreg[j];
+        }
+    };
+
+    const int wn = wave & 1;
+    const int wm = wave >> 1;
+    f32x4 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int64_t ntk = ke > kb0 ? (ke - kb0 + BK8 - 1) / BK8 : 0;
+    if (ntk > 0) {
+        gload(kb0);
+        sstore(0);
+    }
+    __syncthreads();
+    for (int64_t t = 0; t < ntk; ++t) {
+        const int b = (int)(t & 1);
+        if (t + 1 < ntk)
+            gload(kb0 + (t + 1) * BK8);
+        i32x8 av[4];
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+            const int row = wn * 64 + nt * 16 + li;
+            const u32x4 p = *reinterpret_cast<const u32x4 *>(&hs[b][row * P8 + lg * 32]);
+            const u32x4 q = *reinterpret_cast<const u32x4 *>(&hs[b][row * P8 + lg * 32 + 16]);
+            av[nt] = i32x8{(int)p.x, (int)p.y, (int)p.z, (int)p.w,
+                           (int)q.x, (int)q.y, (int)q.z, (int)q.w};
+        }
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) {
+            const int row = wm * 64 + mt * 16 + li;
+            const u32x4 p = *reinterpret_cast<const u32x4 *>(&xs[b][row * P8 + lg * 32]);
+            const u32x4 q = *reinterpret_cast<const u32x4 *>(&xs[b][row * P8 + lg * 32 + 16]);
+            const i32x8 bv = {(int)p.x, (int)p.y, (int)p.z, (int)p.w,
+                              (int)q.x, (int)q.y, (int)q.z, (int)q.w};
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt)
+                acc[nt][mt] = mfma16x16x128_bf8_fp8(av[nt], bv, acc[nt][mt]);
+        }
+        if (t + 1 < ntk)
+            sstore(b ^ 1);
+        __syncthreads();
+    }
+
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+        const int64_t m = mrow0 + wm * 64 + mt * 16 + li;
+        const float sc = m < mrow1 ? a.scale[m] : 0.f;
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt)
+            store_tile_out(a, s, m, n0 + wn * 64 + nt * 16 + lg * 4, acc[nt][mt] * sc, mrow1);
+    }
+}
+
+int64_t token_tiles(int64_t rows, int64_t experts, bool grouped)
+{
+    return grouped ? (rows + BM - 1) / BM + experts : (rows + BM - 1) / BM;
+}
+
+}  // namespace
+
+int gemm_rows_per_block() { return BN; }
+int gemm_tokens_per_block() { return BM; }
+
+hipError_t launch_gemm_f16(const LinearProblem &p, const LinearPlan &plan, float *partial,
+                           hipStream_t stream)
+{
+    GemmArgs a;
+    a.x = p.x;
+    a.offsets = p.offsets;
+    a.rows = p.rows;
+    a.experts = p.experts;
+    a.hi = p.hi;
+    a.res = p.res;
+    a.n = p.n;
+    a.k = p.k;
+    a.ksplit = plan.ksplit;
+    a.splits = plan.splits;
+    a.y = p.y;
+    a.partial = partial;
+    a.scale = nullptr;
+    const int64_t nt = (p.n + BN - 1) / BN;
+    dim3 grid((unsigned)(nt * plan.splits),
+              (unsigned)token_tiles(p.rows, p.experts, p.offsets != nullptr), 1);
+    if (p.mode == MODE_FULL) {
+        if (plan.range_addr)
+            hipLaunchKernelGGL((gemm_f16_kernel<MODE_FULL, true>), grid, dim3(256), 0, stream, a);
+        else
+            hipLaunchKernelGGL((gemm_f16_kernel<MODE_FULL, false>), grid, dim3(256), 0, stream, a);
+    } else {
+        hipLaunchKernelGGL((gemm_f16_kernel<MODE_FAST, false>), grid, dim3(256), 0, stream, a);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm_fp8(const uint8_t *xq, const float *scale, int64_t m, int64_t n,
+                           int64_t k, const uint8_t *hi, uint16_t *y, const LinearPlan &plan,
+                           float *partial, hipStream_t stream)
+{
+    GemmArgs a;
+    a.x = xq;
+    a.offsets = nullptr;
+    a.rows = m;
+    a.experts = 1;
+    a.hi = hi;
+    a.res = ResidualView{nullptr, nullptr, 0, 0, 0};
+    a.n = n;
+    a.k = k;
+    a.ksplit = plan.ksplit;
+    a.splits = plan.splits;
+    a.y = y;
+    a.partial = partial;
+    a.scale = scale;
+    const int64_t nt = (n + BN - 1) / BN;
+    dim3 grid((unsigned)(nt * plan.splits), (unsigned)token_tiles(m, 1, false), 1);
+    hipLaunchKernelGGL(gemm_fp8_kernel, grid, dim3(256), 0, stream, a);
+    return hipGetLastError();
+}
+
+}  // namespace dps

@@ -1,0 +1,246 @@
+"""Python binding of libdps (include/dps.h): argument marshalling only.
+
+Every computation runs in the HIP kernels of libdps.so; this module turns
+torch tensors into device pointers, passes torch's current HIP stream, and
+turns status codes into exceptions.  PyTorch provides device memory and
+streams, nothing else.  If libdps.so is not built, the first call raises.
+"""
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdps.so")
+
+MODE_FULL = 0
+MODE_FAST = 1
+ENC_E5M2 = 0
+ACT_FP16 = 0
+ACT_FP8_ROWSCALE = 1
+
+_STATUS = {0: "DPS_OK", 1: "DPS_ERR_INVALID_ARG", 2: "DPS_ERR_ALIGNMENT",
+           3: "DPS_ERR_UNSUPPORTED", 4: "DPS_ERR_WORKSPACE", 5: "DPS_ERR_HIP"}
+
+EXPORTED = ("dps_split", "dps_merge", "dps_quant_rows_e4m3", "dps_workspace_bytes",
+            "dps_linear", "dps_linear_grouped", "dps_status_str", "dps_last_error")
+
+
+class DpsError(RuntimeError):
+    def __init__(self, status, detail):
+        self.status = status
+        self.name = _STATUS.get(status, str(status))
+        super().__init__("%s: %s" % (self.name, detail))
+
+
+class CResidual(ctypes.Structure):
+    _fields_ = [("pool", ctypes.c_void_p), ("pool_bytes", ctypes.c_int64),
+                ("slots", ctypes.c_void_p), ("n_chunks", ctypes.c_int64),
+                ("log2_chunk", ctypes.c_int32)]
+
+
+class CWeight(ctypes.Structure):
+    _fields_ = [("hi", ctypes.c_void_p), ("res", CResidual), ("experts", ctypes.c_int64),
+                ("n", ctypes.c_int64), ("k", ctypes.c_int64), ("enc", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def load_library(path=LIB_PATH):
+    """Load libdps.so and declare its C signatures.  Raises if it is absent."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError("libdps.so is not built (%s); run __graft_entry__.build() or "
+                           "python -m paper_2609_34380_amd.csrc.build" % path)
+    lib = ctypes.CDLL(path)
+    P, I64, I32, U32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32
+    ST = ctypes.c_int
+    lib.dps_split.argtypes = [P, I64, P, ctypes.POINTER(CResidual), P]
+    lib.dps_split.restype = ST
+    lib.dps_merge.argtypes = [P, ctypes.POINTER(CResidual), I64, P, P]
+    lib.dps_merge.restype = ST
+    lib.dps_quant_rows_e4m3.argtypes = [P, I64, I64, P, P, P]
+    lib.dps_quant_rows_e4m3.restype = ST
+    lib.dps_workspace_bytes.argtypes = [ctypes.c_int, U32, I64, I64, I64, I64]
+    lib.dps_workspace_bytes.restype = ctypes.c_size_t
+    lib.dps_linear.argtypes = [ctypes.c_int, U32, P, I64, ctypes.POINTER(CWeight), P, P,
+                               ctypes.c_size_t, P]
+    lib.dps_linear.restype = ST
+    lib.dps_linear_grouped.argtypes = [ctypes.c_int, U32, P, P, I64, ctypes.POINTER(CWeight),
+                                       P, P, ctypes.c_size_t, P]
+    lib.dps_linear_grouped.restype = ST
+    lib.dps_status_str.argtypes = [ST]
+    lib.dps_status_str.restype = ctypes.c_char_p
+    lib.dps_last_error.argtypes = []
+    lib.dps_last_error.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def _check(status):
+    if status != 0:
+        detail = _lib.dps_last_error().decode()
+        raise DpsError(status, detail)
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _require_cuda(*tensors):
+    for t in tensors:
+        if t is not None and not t.is_cuda:
+            raise ValueError("libdps works on device tensors only")
+
+
+class Residual:
+    """Residual plane of one tensor: a shared pool (uint8 device tensor) plus
+    the int32 device table slots[chunk] = pool slot of that chunk."""
+
+    def __init__(self, pool, slots, log2_chunk):
+        _require_cuda(pool, slots)
+        assert pool.dtype == torch.uint8 and slots.dtype == torch.int32
+        self.pool = pool
+        self.slots = slots
+        self.log2_chunk = int(log2_chunk)
+
+    def c(self):
+        return CResidual(self.pool.data_ptr(), self.pool.numel(), self.slots.data_ptr(),
+                         self.slots.numel(), self.log2_chunk)
+
+
+def _null_residual():
+    return CResidual(None, 0, None, 0, 0)
+
+
+class NestedWeight:
+    """A nested weight: upper-byte plane hi ([n][k] or [experts][n][k], uint8)
+    and its residual (None when only fast mode will be used)."""
+
+    def __init__(self, hi, residual):
+        _require_cuda(hi)
+        assert hi.dtype == torch.uint8 and hi.is_contiguous()
+        self.hi = hi
+        self.residual = residual
+        if hi.dim() == 2:
+            self.experts, self.n, self.k = 1, hi.shape[0], hi.shape[1]
+        elif hi.dim() == 3:
+            self.experts, self.n, self.k = hi.shape
+        else:   # a plain byte plane (split / merge only)
+            self.experts, self.n, self.k = 1, 1, hi.numel()
+        self._c = None
+
+    def c(self):
+        if self._c is None:
+            res = self.residual.c() if self.residual is not None else _null_residual()
+            self._c = CWeight(self.hi.data_ptr(), res, self.experts, self.n, self.k, ENC_E5M2)
+        return self._c
+
+
+def split(w, residual, hi=None):
+    """FP16 weights -> NestedWeight; the residual bytes are written into
+    residual.pool through its chunk table (dps_split)."""
+    lib = load_library()
+    _require_cuda(w)
+    assert w.dtype == torch.float16 and w.is_contiguous()
+    if hi is None:
+        hi = torch.empty(w.shape, dtype=torch.uint8, device=w.device)
+    res = residual.c()
+    _check(lib.dps_split(_ptr(w), w.numel(), _ptr(hi), ctypes.byref(res), _stream()))
+    return NestedWeight(hi, residual)
+
+
+def merge(nw, out=None):
+    """NestedWeight -> the original FP16 weights (dps_merge)."""
+    lib = load_library()
+    if out is None:
+        out = torch.empty(nw.hi.shape, dtype=torch.float16, device=nw.hi.device)
+    res = nw.residual.c()
+    _check(lib.dps_merge(_ptr(nw.hi), ctypes.byref(res), nw.hi.numel(), _ptr(out), _stream()))
+    return out
+
+
+def quant_rows_e4m3(x):
+    """FP16 [m][k] -> (E4M3 codes uint8 [m][k], float32 power-of-two row scale [m])."""
+    lib = load_library()
+    _require_cuda(x)
+    assert x.dtype == torch.float16 and x.dim() == 2 and x.is_contiguous()
+    m, k = x.shape
+    xq = torch.empty((m, k), dtype=torch.uint8, device=x.device)
+    scale = torch.empty(m, dtype=torch.float32, device=x.device)
+    _check(lib.dps_quant_rows_e4m3(_ptr(x), m, k, _ptr(xq), _ptr(scale), _stream()))
+    return xq, scale
+
+
+def workspace_bytes(mode, act, rows, n, k, experts=1):
+    lib = load_library()
+    return lib.dps_workspace_bytes(mode, act, rows, n, k, experts)
+
+
+def _act_flag(act):
+    if act in ("fp16", ACT_FP16):
+        return ACT_FP16
+    if act in ("fp8", ACT_FP8_ROWSCALE):
+        return ACT_FP8_ROWSCALE
+    raise ValueError("act must be 'fp16' or 'fp8'")
+
+
+def _workspace(mode, flag, rows, nw, device, workspace):
+    need = workspace_bytes(mode, flag, rows, nw.n, nw.k, nw.experts)
+    if need == 0:
+        return None, 0
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=device)
+    return workspace, workspace.numel()
+
+
+def linear(x, nw, mode, act="fp16", out=None, workspace=None):
+    """Y = X . W^T through dps_linear; mode MODE_FULL or MODE_FAST."""
+    lib = load_library()
+    _require_cuda(x)
+    assert x.dtype == torch.float16 and x.dim() == 2 and x.is_contiguous()
+    flag = _act_flag(act)
+    m = x.shape[0]
+    if out is None:
+        out = torch.empty((m, nw.n), dtype=torch.float16, device=x.device)
+    ws, ws_bytes = _workspace(mode, flag, m, nw, x.device, workspace)
+    _check(lib.dps_linear(mode, flag, _ptr(x), m, ctypes.byref(nw.c()), _ptr(out), _ptr(ws),
+                          ws_bytes, _stream()))
+    return out
+
+
+def linear_grouped(x_sorted, offsets, nw, mode, out=None, workspace=None):
+    """MoE grouped linear through dps_linear_grouped; offsets is an int32
+    device tensor of experts + 1 row offsets."""
+    lib = load_library()
+    _require_cuda(x_sorted, offsets)
+    assert offsets.dtype == torch.int32 and offsets.numel() == nw.experts + 1
+    rows = x_sorted.shape[0]
+    if out is None:
+        out = torch.empty((rows, nw.n), dtype=torch.float16, device=x_sorted.device)
+    ws, ws_bytes = _workspace(mode, ACT_FP16, rows, nw, x_sorted.device, workspace)
+    _check(lib.dps_linear_grouped(mode, ACT_FP16, _ptr(x_sorted), _ptr(offsets), rows,
+                                  ctypes.byref(nw.c()), _ptr(out), _ptr(ws), ws_bytes,
+                                  _stream()))
+    return out
+
+
+def make_residual(numel, log2_chunk, device, slots=None, pool=None):
+    """A residual for `numel` weights: by default a pool of exactly the chunks
+    needed with the identity table."""
+    c = 1 << log2_chunk
+    n_chunks = max(1, -(-numel // c))
+    if slots is None:
+        slots = torch.arange(n_chunks, dtype=torch.int32)
+    slots = slots.to(device=device, dtype=torch.int32)
+    if pool is None:
+        pool = torch.zeros(max(n_chunks, int(slots.max().item()) + 1) * c, dtype=torch.uint8,
+                           device=device)
+    return Residual(pool, slots, log2_chunk)

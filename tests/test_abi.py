@@ -1,0 +1,124 @@
+"""C-ABI boundary checks that need no GPU: the library loads, exports every
+entry point include/dps.h declares, and rejects bad arguments on the host
+before launching anything."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_34380_amd import dps
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dps.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dps_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(dps.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    return dps.load_library()
+
+
+def test_header_declares_the_boundary():
+    names = _declared()
+    for expected in ("dps_split", "dps_merge", "dps_linear", "dps_linear_grouped",
+                     "dps_quant_rows_e4m3", "dps_workspace_bytes", "dps_status_str",
+                     "dps_last_error"):
+        assert expected in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in _declared():
+        assert hasattr(lib, name), name
+    assert set(_declared()) == set(dps.EXPORTED)
+
+
+def test_status_strings(lib):
+    for code in range(6):
+        assert lib.dps_status_str(code)
+    assert lib.dps_status_str(0) == b"ok"
+
+
+def _weight(n=64, k=64, experts=1, enc=0, hi=0x1000, pool=0x2000, slots=0x3000,
+            pool_bytes=1 << 16, n_chunks=1, log2=16):
+    res = dps.CResidual(pool, pool_bytes, slots, n_chunks, log2)
+    return dps.CWeight(hi, res, experts, n, k, enc)
+
+
+def _linear(lib, mode=0, flags=0, x=0x4000, m=4, w=None, y=0x5000, ws=None, ws_bytes=0):
+    w = w if w is not None else _weight()
+    return lib.dps_linear(mode, flags, x, m, ctypes.byref(w), y, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kwargs,status", [
+    (dict(mode=7), 1),
+    (dict(flags=9), 1),
+    (dict(mode=0, flags=1), 1),                      # FP8 activations need fast mode
+    (dict(w=_weight(k=40)), 1),                      # k % 16 != 0
+    (dict(w=_weight(n=0)), 1),
+    (dict(w=_weight(enc=1)), 3),                     # E4M3 nesting not built
+    (dict(w=_weight(experts=2)), 1),                 # dense call with stacked experts
+    (dict(w=_weight(hi=0x1001)), 2),                 # misaligned plane
+    (dict(x=0x4008), 2),
+    (dict(w=_weight(pool=0)), 1),                    # full mode needs a pool
+    (dict(w=_weight(slots=0)), 1),
+    (dict(w=_weight(log2=3)), 1),
+    (dict(w=_weight(pool_bytes=100)), 1),            # smaller than one chunk
+    (dict(w=_weight(n=1024, k=1024, n_chunks=1, log2=16)), 1),  # table too short
+    (dict(m=-1), 1),
+    (dict(x=0), 1),
+])
+def test_linear_rejects_bad_arguments(lib, kwargs, status):
+    assert _linear(lib, **kwargs) == status
+    assert lib.dps_last_error()
+
+
+def test_linear_zero_rows_is_a_noop(lib):
+    assert _linear(lib, m=0) == 0
+
+
+def test_fast_mode_ignores_residual_descriptor(lib):
+    # a fast-mode call with an empty residual fails only later (x is NULL here)
+    w = _weight(pool=0, slots=0, pool_bytes=0, n_chunks=0, log2=0)
+    assert _linear(lib, mode=1, x=0, w=w) == 1
+    assert b"x or y" in lib.dps_last_error()
+
+
+def test_grouped_rejects_bad_arguments(lib):
+    w = _weight(experts=4)
+    args = lambda **kw: (kw.get("mode", 1), kw.get("flags", 0), kw.get("x", 0x4000),
+                         kw.get("off", 0x6000), kw.get("rows", 8), ctypes.byref(w),
+                         kw.get("y", 0x5000), None, 0, None)
+    assert lib.dps_linear_grouped(*args(flags=1)) == 3
+    assert lib.dps_linear_grouped(*args(off=0)) == 1
+    assert lib.dps_linear_grouped(*args(off=0x6002)) == 2
+    assert lib.dps_linear_grouped(*args(rows=-3)) == 1
+    assert lib.dps_linear_grouped(*args(rows=0)) == 0
+
+
+def test_split_merge_reject_bad_arguments(lib):
+    # every call here fails validation (or is empty) before any launch
+    res = dps.CResidual(0x2000, 1 << 8, 0x3000, 4, 8)
+    bad = dps.CResidual(0x2000, 1 << 8, 0x3000, 3, 8)   # 3 chunks of 256 < 1024 bytes
+    assert lib.dps_split(0x1000, 1024, 0x4000, ctypes.byref(bad), None) == 1
+    assert lib.dps_split(0x1000, -1, 0x4000, ctypes.byref(res), None) == 1
+    assert lib.dps_split(0x1000, 0, 0x4000, ctypes.byref(res), None) == 0
+    assert lib.dps_split(0x1004, 1024, 0x4000, ctypes.byref(res), None) == 2
+    assert lib.dps_merge(0x4000, None, 1024, 0x1000, None) == 1
+    assert lib.dps_merge(0x4000, ctypes.byref(bad), 1024, 0x1000, None) == 1
+    assert lib.dps_quant_rows_e4m3(0x1000, 4, 24, 0x2000, 0x3000, None) == 1
+    assert lib.dps_quant_rows_e4m3(0x1000, 0, 32, 0x2000, 0x3000, None) == 0
+
+
+def test_workspace_query(lib):
+    assert lib.dps_workspace_bytes(0, 0, 0, 64, 64, 1) == 0
+    # FP8 activations always need room for the quantized copy
+    assert lib.dps_workspace_bytes(1, 1, 2048, 4096, 4096, 1) >= 2048 * 4096

@@ -1,0 +1,335 @@
+"""HIP path vs the CPU oracle, element by element, on seeded inputs.
+
+Bit-exact: split planes, merge, chunk addressing, E4M3 row quantization.
+Tolerance (relative Frobenius <= 1e-3 and max abs <= 2e-2 against the fp64
+oracle): every linear output.  Sizes span several tiles with ragged tails
+on N, K and M, both residual addressing paths (a row's K range within one or
+two chunks, and per-vector table lookups when chunks are small), scattered
+slot tables and pools whose other slots hold KV-like filler.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_helpers import DEV, Nested, assert_close, errors, u16
+from paper_2609_34380_amd import dps, workloads
+
+pytestmark = pytest.mark.gpu
+
+FAST, FULL = dps.MODE_FAST, dps.MODE_FULL
+
+
+def _omode(mode):
+    return oracle.FAST if mode == FAST else oracle.FULL
+
+
+# -----------------------------------------------------------------------------
+# split / merge / addressing: bit-exact
+# -----------------------------------------------------------------------------
+
+def test_split_merge_single_layer_identity_table():
+    """1024x1024 FP16, 64 KiB chunks, identity table (the single-layer workload)."""
+    w = workloads.weight_fp16(1024, 1024, seed=0)
+    nst = Nested(w, 16)
+    nst.check_planes()
+    back = dps.merge(nst.nw)
+    torch.cuda.synchronize()
+    assert torch.equal(back.cpu().view(torch.int16), w.view(torch.int16))
+
+
+def test_split_merge_all_patterns_scattered():
+    """All 65536 FP16 patterns plus a ragged tail of 13 words, 256-byte chunks at
+    random slots of a pool whose other slots hold KV filler."""
+    rng = np.random.default_rng(3)
+    bits = np.concatenate([np.arange(65536, dtype=np.uint32).astype(np.uint16),
+                           rng.integers(0, 65536, 13).astype(np.uint16)])
+    w = torch.from_numpy(bits.view(np.int16).copy()).view(torch.float16)
+    nst = Nested(w, 8, n_slots=600, slot_seed=4, filler_seed=5)
+    nst.check_planes()
+    back = dps.merge(nst.nw)
+    torch.cuda.synchronize()
+    assert np.array_equal(back.cpu().view(torch.int16).numpy().view(np.uint16), bits)
+
+
+@pytest.mark.parametrize("numel,log2c,n_slots", [(1_000_003, 12, 400), (4096 * 14336, 21, 64),
+                                                  (17, 4, 8)])
+def test_split_scattered_pool(numel, log2c, n_slots):
+    rng = np.random.default_rng(numel)
+    bits = rng.integers(0, 65536, numel).astype(np.uint16)
+    w = torch.from_numpy(bits.view(np.int16)).view(torch.float16)
+    nst = Nested(w, log2c, n_slots=n_slots, slot_seed=7, filler_seed=8)
+    nst.check_planes()
+    back = dps.merge(nst.nw)
+    torch.cuda.synchronize()
+    assert np.array_equal(back.cpu().view(torch.int16).numpy().view(np.uint16), bits)
+
+
+def test_out_of_range_slot_is_never_dereferenced():
+    """A slot entry outside the pool: the split drops those residual bytes, the
+    merge reads them as zero, and nothing else changes."""
+    log2c = 8
+    numel = 4 * 256
+    bits = np.random.default_rng(9).integers(0, 65536, numel).astype(np.uint16)
+    w = torch.from_numpy(bits.view(np.int16)).view(torch.float16).to(DEV)
+    pool = torch.full((4 * 256,), 0xA5, dtype=torch.uint8, device=DEV)
+    slots = torch.tensor([2, 1000, 0, -5], dtype=torch.int32, device=DEV)
+    res = dps.Residual(pool, slots, log2c)
+    nw = dps.split(w, res)
+    back = dps.merge(nw)
+    torch.cuda.synchronize()
+    p = pool.cpu().numpy().reshape(4, 256)
+    low = bits.view(np.uint8)[0::2].reshape(4, 256)
+    assert np.array_equal(p[2], low[0]) and np.array_equal(p[0], low[2])
+    assert (p[1] == 0xA5).all() and (p[3] == 0xA5).all()
+    want = bits.copy().reshape(4, 256)
+    want[1] &= 0xFF00
+    want[3] &= 0xFF00
+    assert np.array_equal(back.cpu().view(torch.int16).numpy().view(np.uint16), want.ravel())
+
+
+# -----------------------------------------------------------------------------
+# FP8 row quantization: bit-exact
+# -----------------------------------------------------------------------------
+
+def test_quant_rows_bit_exact():
+    x = workloads.activations_fp16(37, 4096, seed=11, outlier_frac=0.01, outlier_scale=20.0)
+    x[0] = 0.0
+    x[1] = torch.linspace(-65504, 65504, 4096).half()
+    x[2] = (torch.randn(4096) * 1e-6).half()
+    x[3, :] = 0.0
+    x[3, 5] = 448.0
+    x[3, 6] = 0.0146484375    # a tie between E4M3 neighbours at scale 1
+    x[3, 7] = -0.0
+    xq, s = dps.quant_rows_e4m3(x.to(DEV))
+    torch.cuda.synchronize()
+    xq_ref, s_ref = oracle.act_quant(u16(x))
+    assert np.array_equal(s.cpu().numpy().astype(np.float64), s_ref)
+    assert np.array_equal(xq.cpu().numpy(), xq_ref)
+
+
+def test_quant_rows_every_fp16_value():
+    """Every finite FP16 value with |x| <= 448 in one row (scale 1)."""
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    v = bits.view(np.float16).astype(np.float64)
+    keep = bits[np.isfinite(v) & (np.abs(v) <= 448)]
+    pad = (-keep.size) % 16
+    row = np.concatenate([keep, np.zeros(pad, np.uint16)])
+    x = torch.from_numpy(row.view(np.int16).copy()).view(torch.float16).reshape(1, -1)
+    xq, s = dps.quant_rows_e4m3(x.to(DEV))
+    torch.cuda.synchronize()
+    xq_ref, s_ref = oracle.act_quant(row.reshape(1, -1))
+    assert s_ref[0] == 1.0 and s.item() == 1.0
+    assert np.array_equal(xq.cpu().numpy(), xq_ref)
+
+
+# -----------------------------------------------------------------------------
+# linear: tolerance against the fp64 oracle
+# -----------------------------------------------------------------------------
+
+# (m, n, k, log2c, scattered): decode-shaped (skinny kernel) and token-tiled
+# (matrix-core GEMM) problems with ragged m, n and k.
+LINEAR_CASES = [
+    (4, 1024, 1024, 16, False),     # the single-layer workload
+    (1, 1024, 1024, 16, False),
+    (3, 1000, 1040, 12, True),
+    (16, 64, 2048, 8, True),        # chunks smaller than a K range: table lookups
+    (17, 520, 4096, 21, True),
+    (33, 200, 1152, 10, True),
+    (64, 1024, 4096, 21, False),
+    (65, 384, 1024, 12, True),
+    (130, 260, 2048, 8, True),
+    (300, 512, 512, 16, True),
+    (256, 640, 4096, 21, True),
+]
+
+
+def _case_id(c):
+    return "m%d_n%d_k%d_c%d%s" % (c[0], c[1], c[2], c[3], "_scat" if c[4] else "")
+
+
+@pytest.fixture(scope="module", params=LINEAR_CASES, ids=_case_id)
+def linear_case(request):
+    m, n, k, log2c, scattered = request.param
+    w = workloads.weight_fp16(n, k, seed=100 + n)
+    x = workloads.activations_fp16(m, k, seed=200 + m)
+    numel = n * k
+    n_chunks = -(-numel // (1 << log2c))
+    if scattered:
+        nst = Nested(w, log2c, n_slots=2 * n_chunks + 3, slot_seed=n + k, filler_seed=m)
+    else:
+        nst = Nested(w, log2c)
+    return m, n, k, w, x, nst
+
+
+def test_linear_planes(linear_case):
+    linear_case[-1].check_planes()
+
+
+@pytest.mark.parametrize("mode", [FAST, FULL], ids=["fast", "full"])
+def test_linear_matches_oracle(linear_case, mode):
+    m, n, k, w, x, nst = linear_case
+    y = dps.linear(x.to(DEV), nst.nw, mode)
+    torch.cuda.synchronize()
+    ref = oracle.linear(_omode(mode), u16(x), nst.hi_ref,
+                        nst.res_ref if mode == FULL else None)
+    assert_close(y, ref, "mode=%d" % mode)
+
+
+def test_fast_equals_full_with_zero_residual(linear_case):
+    """Fast mode == full mode whose residual bytes are all zero, bit for bit."""
+    m, n, k, w, x, nst = linear_case
+    zero_res = dps.Residual(torch.zeros_like(nst.res.pool), nst.res.slots, nst.res.log2_chunk)
+    nw0 = dps.NestedWeight(nst.nw.hi, zero_res)
+    xd = x.to(DEV)
+    y_fast = dps.linear(xd, nst.nw, FAST)
+    y_full0 = dps.linear(xd, nw0, FULL)
+    torch.cuda.synchronize()
+    assert torch.equal(y_fast.view(torch.int16), y_full0.view(torch.int16))
+
+
+def test_fast_never_reads_residual(linear_case):
+    """Fast mode with the pool overwritten (0xFF), and with no residual at
+    all, gives the same bits as with the intact residual."""
+    m, n, k, w, x, nst = linear_case
+    xd = x.to(DEV)
+    y_clean = dps.linear(xd, nst.nw, FAST)
+    poisoned = dps.Residual(torch.full_like(nst.res.pool, 0xFF), nst.res.slots,
+                            nst.res.log2_chunk)
+    y_poison = dps.linear(xd, dps.NestedWeight(nst.nw.hi, poisoned), FAST)
+    y_none = dps.linear(xd, dps.NestedWeight(nst.nw.hi, None), FAST)
+    torch.cuda.synchronize()
+    assert torch.equal(y_clean.view(torch.int16), y_poison.view(torch.int16))
+    assert torch.equal(y_clean.view(torch.int16), y_none.view(torch.int16))
+
+
+def test_linear_is_deterministic(linear_case):
+    m, n, k, w, x, nst = linear_case
+    xd = x.to(DEV)
+    a = dps.linear(xd, nst.nw, FULL)
+    b = dps.linear(xd, nst.nw, FULL)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+@pytest.mark.parametrize("m", [16, 200])
+def test_one_hot_rows_select_weights_exactly(m):
+    """x[r] = e_{j_r}: Y[r][c] is exactly W[c][j_r] (full) or its E5M2 part
+    (fast); checks operand layout, merge and addressing end to end."""
+    n, k = 272, 1024
+    w = workloads.weight_fp16(n, k, seed=31)
+    nst = Nested(w, 9, n_slots=4000, slot_seed=32, filler_seed=33)
+    cols = torch.randperm(k, generator=torch.Generator().manual_seed(34))[:m]
+    x = torch.zeros((m, k), dtype=torch.float16)
+    x[torch.arange(m), cols] = 1.0
+    for mode in (FULL, FAST):
+        y = dps.linear(x.to(DEV), nst.nw, mode)
+        torch.cuda.synchronize()
+        if mode == FULL:
+            want = w[:, cols].t().contiguous()
+        else:
+            want = torch.from_numpy(nst.hi_ref[:, cols.numpy()].T.copy()).view(
+                torch.float8_e5m2).to(torch.float16)
+        # value equality: a -0 weight times 1 plus +0 terms sums to +0 (IEEE)
+        assert torch.equal(y.cpu().float(), want.float()), mode
+
+
+def test_special_weight_values():
+    """Subnormal, signed-zero and infinite weights through both modes."""
+    n, k = 32, 256
+    w = workloads.weight_fp16(n, k, seed=41)
+    w[0, :] = 0.0
+    w[1, :] = -0.0
+    w[2, ::2] = 6.0e-8          # FP16 subnormal, E5M2 part is zero
+    w[3, ::3] = 1.52587890625e-05   # E5M2 subnormal 2^-16
+    w[4, 7] = float("inf")
+    nst = Nested(w, 8)
+    x = workloads.activations_fp16(8, k, seed=42)
+    x[:, 7] = 0.5
+    for mode in (FULL, FAST):
+        y = dps.linear(x.to(DEV), nst.nw, mode)
+        torch.cuda.synchronize()
+        ref = oracle.linear(_omode(mode), u16(x), nst.hi_ref,
+                            nst.res_ref if mode == FULL else None)
+        got = y.cpu().double().numpy()
+        assert np.isinf(got[:, 4]).all() and (np.sign(got[:, 4]) == np.sign(ref[:, 4])).all()
+        keep = np.ones(n, bool)
+        keep[4] = False
+        assert_close(y[:, torch.from_numpy(keep).to(DEV)], ref[:, keep])
+
+
+# -----------------------------------------------------------------------------
+# FP8 activations (fast-mode prefill)
+# -----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("m,n,k", [(128, 256, 1024), (200, 300, 2048), (17, 130, 4096),
+                                   (513, 640, 1152)])
+def test_linear_fp8_matches_oracle(m, n, k):
+    w = workloads.weight_fp16(n, k, seed=51 + m)
+    x = workloads.activations_fp16(m, k, seed=52 + m, outlier_frac=0.01, outlier_scale=20.0)
+    nst = Nested(w, 21)
+    y = dps.linear(x.to(DEV), nst.nw, FAST, act="fp8")
+    torch.cuda.synchronize()
+    xq, s = oracle.act_quant(u16(x))
+    ref = oracle.linear_fp8(xq, s, nst.hi_ref)
+    assert_close(y, ref)
+
+
+# -----------------------------------------------------------------------------
+# grouped (MoE)
+# -----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("counts,n,k,log2c", [
+    ((5, 0, 17, 64, 1, 3), 192, 512, 12),           # decode-sized groups, an empty expert
+    ((100, 0, 300, 129, 7), 160, 1024, 10),          # token-tiled groups
+    ((128, 140, 120, 133, 110, 125, 131, 137), 256, 256, 21),
+])
+@pytest.mark.parametrize("mode", [FAST, FULL], ids=["fast", "full"])
+def test_grouped_matches_oracle(counts, n, k, log2c, mode):
+    e = len(counts)
+    rows = sum(counts)
+    w = workloads.weight_fp16(n, k, seed=61, experts=e)
+    x = workloads.activations_fp16(rows, k, seed=62)
+    offsets = np.zeros(e + 1, dtype=np.int64)
+    offsets[1:] = np.cumsum(counts)
+    numel = e * n * k
+    n_chunks = -(-numel // (1 << log2c))
+    nst = Nested(w, log2c, n_slots=n_chunks + 5, slot_seed=63, filler_seed=64)
+    nst.check_planes()
+    off_dev = torch.from_numpy(offsets.astype(np.int32)).to(DEV)
+    y = dps.linear_grouped(x.to(DEV), off_dev, nst.nw, mode)
+    torch.cuda.synchronize()
+    ref = oracle.linear_grouped(_omode(mode), u16(x), offsets, nst.hi_ref,
+                                nst.res_ref if mode == FULL else None)
+    assert_close(y, ref)
+
+
+def test_grouped_single_expert_equals_dense():
+    n, k, m = 300, 512, 90
+    w = workloads.weight_fp16(n, k, seed=71)
+    x = workloads.activations_fp16(m, k, seed=72).to(DEV)
+    nst = Nested(w, 12)
+    off = torch.tensor([0, m], dtype=torch.int32, device=DEV)
+    nw3 = dps.NestedWeight(nst.nw.hi.view(1, n, k), nst.res)
+    for mode in (FAST, FULL):
+        a = dps.linear(x, nst.nw, mode)
+        b = dps.linear_grouped(x, off, nw3, mode)
+        torch.cuda.synchronize()
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+# -----------------------------------------------------------------------------
+# error paths on the device-side entry points
+# -----------------------------------------------------------------------------
+
+def test_workspace_too_small_is_rejected():
+    n, k, m = 4096, 4096, 32
+    w = workloads.weight_fp16(n, k, seed=81)
+    nst = Nested(w, 21)
+    need = dps.workspace_bytes(FULL, 0, m, n, k)
+    assert need > 0
+    x = workloads.activations_fp16(m, k, seed=82).to(DEV)
+    small = torch.empty(need - 256, dtype=torch.uint8, device=DEV)
+    with pytest.raises(dps.DpsError) as ei:
+        dps.linear(x, nst.nw, FULL, workspace=small)
+    assert ei.value.status == 4
