@@ -11,8 +11,9 @@
 namespace dps {
 int skinny_rows_per_block(int variant);
 int skinny_k_per_batch(int variant);
+int skinny_pass_rows(int64_t rows, bool grouped);
 int gemm_rows_per_block();
-int gemm_tokens_per_block();
+int gemm_tokens_per_block(int variant);
 }  // namespace dps
 
 namespace {
@@ -123,7 +124,8 @@ LinearPlan plan_linear(int mode, uint32_t flags, int64_t rows, int64_t n, int64_
     const int64_t rows_per_expert = grouped ? cdiv(rows, experts) : rows;
     if (flags & DPS_ACT_FP8_ROWSCALE) {
         p.kind = KIND_GEMM_FP8;
-        const int64_t tiles = cdiv(n, gemm_rows_per_block()) * cdiv(rows, gemm_tokens_per_block());
+        const int64_t tiles =
+            cdiv(n, gemm_rows_per_block()) * cdiv(rows, gemm_tokens_per_block(GEMM_REG_128));
         int64_t s = cdiv(target, tiles);
         const int64_t smax = k / 1024 > 1 ? k / 1024 : 1;
         s = s < 1 ? 1 : (s > smax ? smax : s);
@@ -132,20 +134,32 @@ LinearPlan plan_linear(int mode, uint32_t flags, int64_t rows, int64_t n, int64_
         p.ws_quant = align256(rows * k) + align256(rows * 4);
     } else if (rows_per_expert <= 64) {
         p.kind = KIND_SKINNY;
-        p.variant = 0;
+        // measured on MI355X: 16 rows per wave for up to 16 tokens, 32 rows with
+        // half-length batches above that (lighter register footprints win)
+        p.variant = rows_per_expert <= 16 ? 1 : 2;
         const int64_t kpb = skinny_k_per_batch(p.variant);
+        // the block's X slice [pass rows][ksplit + 8] FP16 lives in 64 KiB of LDS
+        const int64_t xr = skinny_pass_rows(rows, grouped);
+        int64_t kmax = (32768 / xr - 8) / kpb * kpb;
+        kmax = kmax < kpb ? kpb : kmax;
         const int64_t blocks = cdiv(n, skinny_rows_per_block(p.variant)) * experts;
-        int64_t s = cdiv(target, blocks);
+        int64_t s = cdiv((int64_t)cu_count, blocks);
         const int64_t smax = k / kpb > 1 ? k / kpb : 1;
         s = s < 1 ? 1 : (s > smax ? smax : s);
         p.ksplit = round_up(cdiv(k, s), kpb);
+        if (p.ksplit > kmax)
+            p.ksplit = kmax;
         p.splits = (int)cdiv(k, p.ksplit);
     } else {
         p.kind = KIND_GEMM_F16;
+        // measured on MI355X: the LDS-DMA pipeline wins with one byte plane
+        // (fast mode), the register-staged kernel with two (full mode); K is
+        // split only until the tiles cover the CUs, keeping >= 1024 per range
+        p.variant = mode == MODE_FAST ? GEMM_DMA_128 : GEMM_REG_128;
         const int64_t tiles =
-            cdiv(n, gemm_rows_per_block()) * cdiv(rows, gemm_tokens_per_block());
-        int64_t s = cdiv(target, tiles);
-        const int64_t smax = k / 512 > 1 ? k / 512 : 1;
+            cdiv(n, gemm_rows_per_block()) * cdiv(rows, gemm_tokens_per_block(p.variant));
+        int64_t s = cdiv((int64_t)cu_count, tiles);
+        const int64_t smax = k / 1024 > 1 ? k / 1024 : 1;
         s = s < 1 ? 1 : (s > smax ? smax : s);
         p.ksplit = round_up(cdiv(k, s), 64);
         p.splits = (int)cdiv(k, p.ksplit);
@@ -244,8 +258,7 @@ dps_status run_linear(int mode, uint32_t flags, const uint16_t *x, const int32_t
                 "workspace is smaller than dps_workspace_bytes()");
         REQUIRE(aligned(ws, 256), DPS_ERR_ALIGNMENT, "workspace is not 256-byte aligned");
     }
-    const int64_t token_tiles = (rows + dps::gemm_tokens_per_block() - 1) /
-                                    dps::gemm_tokens_per_block() + (grouped ? w->experts : 0);
+    const int64_t token_tiles = (rows + 127) / 128 + (grouped ? w->experts : 0);
     REQUIRE(token_tiles <= 65535, DPS_ERR_UNSUPPORTED, "too many rows for one call");
     REQUIRE(plan.splits <= 65535, DPS_ERR_UNSUPPORTED, "k too large for one call");
 

@@ -36,16 +36,16 @@ struct ResidualView {
 };
 
 // Physical byte offset of logical residual byte li, or -1 when its chunk is
-// beyond the table or its slot is outside the pool.
+// beyond the table or its slot is outside the pool.  Branch-free: the table
+// read is always issued (entry 0 stands in for an out-of-range chunk;
+// n_chunks >= 1 whenever a residual is read).
 __device__ __forceinline__ int64_t residual_offset(const ResidualView &r, int64_t li)
 {
     const int64_t c = li >> r.log2c;
-    if (c < 0 || c >= r.n_chunks)
-        return -1;
-    const int64_t s = r.slots[c];
-    if (s < 0 || s >= r.n_pool_slots)
-        return -1;
-    return (s << r.log2c) | (li & ((int64_t(1) << r.log2c) - 1));
+    const bool cin = c >= 0 && c < r.n_chunks;
+    const int64_t s = r.slots[cin ? c : 0];
+    const bool sin = cin && s >= 0 && s < r.n_pool_slots;
+    return sin ? ((s << r.log2c) | (li & ((int64_t(1) << r.log2c) - 1))) : -1;
 }
 
 // Addressing for one contiguous logical range [lbegin, lend) that spans at

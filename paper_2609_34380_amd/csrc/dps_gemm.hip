@@ -41,13 +41,13 @@ struct GemmArgs {
 // Token range of this block: dense calls use grid.y as the token tile;
 // grouped calls walk the experts' tile counts.  Returns false if no work.
 __device__ __forceinline__ bool block_rows(const GemmArgs &a, int64_t &e, int64_t &m0,
-                                           int64_t &m1)
+                                           int64_t &m1, int bm = BM)
 {
     const int64_t t = blockIdx.y;
     if (!a.offsets) {
         e = 0;
-        m0 = t * BM;
-        m1 = m0 + BM < a.rows ? m0 + BM : a.rows;
+        m0 = t * bm;
+        m1 = m0 + bm < a.rows ? m0 + bm : a.rows;
         return m0 < m1;
     }
     int64_t cum = 0;
@@ -55,11 +55,11 @@ __device__ __forceinline__ bool block_rows(const GemmArgs &a, int64_t &e, int64_
     for (int64_t ex = 0; ex < a.experts; ++ex) {
         int64_t o1 = a.offsets[ex + 1];
         o1 = o1 < prev ? prev : (o1 > a.rows ? a.rows : o1);
-        const int64_t tiles = (o1 - prev + BM - 1) / BM;
+        const int64_t tiles = (o1 - prev + bm - 1) / bm;
         if (t < cum + tiles) {
             e = ex;
-            m0 = prev + (t - cum) * BM;
-            m1 = m0 + BM < o1 ? m0 + BM : o1;
+            m0 = prev + (t - cum) * bm;
+            m1 = m0 + bm < o1 ? m0 + bm : o1;
             return true;
         }
         cum += tiles;
@@ -238,6 +238,198 @@ __global__ __launch_bounds__(256) void gemm_f16_kernel(GemmArgs a)
 }
 
 // ------------------------------------------------------------------------------
+// FP16 matrix cores, LDS-DMA pipeline (gfx950 global_load_lds_dwordx4)
+// ------------------------------------------------------------------------------
+// Tiles stream global -> LDS with direct-to-LDS loads (no registers in flight)
+// through a ring of DMA_STAGES stages; each stage holds, for 64 K elements,
+// the 128-row upper-byte tile, the residual-byte tile (full mode) and the
+// BM-token X tile.  A DMA instruction writes 64 lanes x 16 bytes contiguously,
+// so each lane is pointed at the global chunk that belongs at its LDS slot;
+// the slot order is XOR-swizzled per row so that the MFMA-layout reads below
+// are free of bank conflicts.  Lanes whose chunk is past the K range, or whose
+// residual chunk has no valid slot, load from a zero vector instead (a DMA
+// cannot zero-fill).  One barrier per stage.
+constexpr int DMA_BK = 64;
+constexpr int DMA_STAGES = 3;
+constexpr int DMA_W_BYTES = BN * DMA_BK;  // one byte plane, 8 KiB
+
+__device__ __attribute__((aligned(16))) const uint8_t g_zero16[16] = {0};
+
+#define DPS_LDS(p) ((__attribute__((address_space(3))) void *)(p))
+
+__device__ __forceinline__ void dma16(const void *src, void *lds_wave_base)
+{
+    __builtin_amdgcn_global_load_lds(src, DPS_LDS(lds_wave_base), 16, 0, 0);
+}
+
+// s_waitcnt vmcnt(n) leaving the other counters alone (gfx9 encoding).
+#define DPS_WAIT_VMCNT(n) \
+    __builtin_amdgcn_s_waitcnt(((n) & 0xF) | ((((n) >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8))
+
+template <int MODE, int BM>
+struct DmaCfg {
+    static constexpr int X_BYTES = BM * DMA_BK * 2;
+    static constexpr int PLANES = MODE == MODE_FULL ? 2 : 1;
+    static constexpr int STAGE = DMA_W_BYTES * PLANES + X_BYTES;
+    static constexpr int LDS = STAGE * DMA_STAGES;
+    static constexpr int X_INSTR = X_BYTES / 1024 / 4;          // per wave per stage
+    static constexpr int W_INSTR = DMA_W_BYTES / 1024 / 4;      // per wave per plane per stage
+    static constexpr int NI = W_INSTR * PLANES + X_INSTR;       // DMA instructions per wave per stage
+    static constexpr int MT = BM / 32;                          // 16-token tiles per wave
+};
+
+template <int MODE, int BM, bool RANGE>
+__global__ __launch_bounds__(256) void gemm_f16_dma_kernel(GemmArgs a)
+{
+    using C = DmaCfg<MODE, BM>;
+    __shared__ __attribute__((aligned(16))) uint8_t smem[C::LDS];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int li = lane & 15;
+    const int lg = lane >> 4;
+
+    int64_t e, mrow0, mrow1;
+    if (!block_rows(a, e, mrow0, mrow1, BM))
+        return;
+    const int ntile = blockIdx.x / a.splits;
+    const int s = blockIdx.x % a.splits;
+    const int64_t n0 = (int64_t)ntile * BN;
+    const int64_t kb0 = (int64_t)s * a.ksplit;
+    const int64_t ke = kb0 + a.ksplit < a.k ? kb0 + a.ksplit : a.k;
+    const int64_t ntk = ke > kb0 ? (ke - kb0 + DMA_BK - 1) / DMA_BK : 0;
+    const uint16_t *x = static_cast<const uint16_t *>(a.x);
+
+    // ---- per-lane DMA sources that do not change with the K stage ---------------
+    // weight rows: instruction j (= wave * W_INSTR + jj) covers rows 16j .. 16j+15,
+    // lane l -> row 16j + l/4, LDS chunk slot l%4 holding logical chunk
+    // (l%4) ^ ((row >> 2) & 3)
+    const uint8_t *wsrc[C::W_INSTR];
+    int64_t wl[C::W_INSTR];
+    int wchunk[C::W_INSTR];
+    RangeResidual rr[C::W_INSTR];
+#pragma unroll
+    for (int jj = 0; jj < C::W_INSTR; ++jj) {
+        const int j = wave * C::W_INSTR + jj;
+        const int r = 16 * j + (lane >> 2);
+        int64_t nr = n0 + r;
+        nr = nr < a.n ? nr : a.n - 1;
+        wl[jj] = (e * a.n + nr) * a.k;
+        wsrc[jj] = a.hi + wl[jj];
+        wchunk[jj] = (lane & 3) ^ ((r >> 2) & 3);
+        rr[jj].ok0 = rr[jj].ok1 = false;
+        rr[jj].delta0 = rr[jj].delta1 = 0;
+        rr[jj].bnd = 0;
+        if (MODE == MODE_FULL && RANGE && ke > kb0)
+            rr[jj] = range_residual(a.res, wl[jj] + kb0, wl[jj] + ke);
+    }
+    // X rows: instruction j covers rows 8j .. 8j+7, lane l -> row 8j + l/8,
+    // slot l%8 holding logical chunk (l%8) ^ (row & 7) (8 halfs per chunk)
+    const uint16_t *xsrc[C::X_INSTR];
+    int xchunk[C::X_INSTR];
+#pragma unroll
+    for (int jj = 0; jj < C::X_INSTR; ++jj) {
+        const int j = wave * C::X_INSTR + jj;
+        const int r = 8 * j + (lane >> 3);
+        int64_t m = mrow0 + r;
+        m = m < mrow1 ? m : mrow1 - 1;
+        xsrc[jj] = x + m * a.k;
+        xchunk[jj] = (lane & 7) ^ (r & 7);
+    }
+
+    auto issue = [&](int64_t t) {
+        uint8_t *st = smem + (int)(t % DMA_STAGES) * C::STAGE;
+        const bool live = t < ntk;
+        const int64_t kt = kb0 + t * DMA_BK;
+#pragma unroll
+        for (int jj = 0; jj < C::W_INSTR; ++jj) {
+            const int j = wave * C::W_INSTR + jj;
+            const int64_t kk = kt + wchunk[jj] * 16;
+            const bool ok = live && kk < ke;
+            dma16(ok ? (const void *)(wsrc[jj] + kk) : (const void *)g_zero16, st + j * 1024);
+            if (MODE == MODE_FULL) {
+                const int64_t li2 = wl[jj] + (ok ? kk : kb0);
+                const void *src = g_zero16;
+                if (RANGE) {
+                    const bool second = li2 >= rr[jj].bnd;
+                    const bool cok = second ? rr[jj].ok1 : rr[jj].ok0;
+                    const int64_t d = second ? rr[jj].delta1 : rr[jj].delta0;
+                    if (ok && cok)
+                        src = a.res.pool + (d + li2);
+                } else {
+                    const int64_t off = residual_offset(a.res, li2);
+                    if (ok && off >= 0)
+                        src = a.res.pool + off;
+                }
+                dma16(src, st + DMA_W_BYTES + j * 1024);
+            }
+        }
+#pragma unroll
+        for (int jj = 0; jj < C::X_INSTR; ++jj) {
+            const int j = wave * C::X_INSTR + jj;
+            const int64_t kk = kt + xchunk[jj] * 8;
+            const bool ok = live && kk < ke;
+            dma16(ok ? (const void *)(xsrc[jj] + kk) : (const void *)g_zero16,
+                  st + DMA_W_BYTES * C::PLANES + j * 1024);
+        }
+    };
+
+    const int wn = wave & 1;
+    const int wm = wave >> 1;
+    f32x4 acc[4][C::MT];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < C::MT; ++j)
+            acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+#pragma unroll
+    for (int t = 0; t < DMA_STAGES - 1; ++t)
+        issue(t);
+    for (int64_t t = 0; t < ntk; ++t) {
+        DPS_WAIT_VMCNT(C::NI * (DMA_STAGES - 2));
+        __syncthreads();
+        issue(t + DMA_STAGES - 1);
+        const uint8_t *st = smem + (int)(t % DMA_STAGES) * C::STAGE;
+        const uint8_t *xs = st + DMA_W_BYTES * C::PLANES;
+        half8 a0[4], a1[4];
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+            const int r = wn * 64 + nt * 16 + li;
+            const int off = r * DMA_BK + ((lg ^ ((r >> 2) & 3)) << 4);
+            const u32x4 h = *reinterpret_cast<const u32x4 *>(st + off);
+            u32x4 l = {0u, 0u, 0u, 0u};
+            if (MODE == MODE_FULL)
+                l = *reinterpret_cast<const u32x4 *>(st + DMA_W_BYTES + off);
+            a0[nt] = merge8(h.x, h.y, l.x, l.y);
+            a1[nt] = merge8(h.z, h.w, l.z, l.w);
+        }
+#pragma unroll
+        for (int mt = 0; mt < C::MT; ++mt) {
+            const int r = wm * (BM / 2) + mt * 16 + li;
+            const uint8_t *row = xs + r * (DMA_BK * 2);
+            const half8 b0 = as_half8(*reinterpret_cast<const u32x4 *>(row + (((2 * lg) ^ (r & 7)) << 4)));
+            const half8 b1 =
+                as_half8(*reinterpret_cast<const u32x4 *>(row + (((2 * lg + 1) ^ (r & 7)) << 4)));
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt) {
+                acc[nt][mt] = mfma16x16x32(a0[nt], b0, acc[nt][mt]);
+                acc[nt][mt] = mfma16x16x32(a1[nt], b1, acc[nt][mt]);
+            }
+        }
+    }
+    DPS_WAIT_VMCNT(0);  // no DMA may still target this block's LDS when it exits
+
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+        for (int mt = 0; mt < C::MT; ++mt)
+            store_tile_out(a, s, mrow0 + wm * (BM / 2) + mt * 16 + li,
+                           n0 + wn * 64 + nt * 16 + lg * 4, acc[nt][mt], mrow1);
+}
+
+// ------------------------------------------------------------------------------
 // FP8 matrix cores: E5M2 weights x E4M3 activations
 // ------------------------------------------------------------------------------
 constexpr int BK8 = 128;        // K elements (= bytes) per tile
@@ -345,15 +537,24 @@ __global__ __launch_bounds__(256) void gemm_fp8_kernel(GemmArgs a)
     }
 }
 
-int64_t token_tiles(int64_t rows, int64_t experts, bool grouped)
+int64_t token_tiles(int64_t rows, int64_t experts, bool grouped, int bm = BM)
 {
-    return grouped ? (rows + BM - 1) / BM + experts : (rows + BM - 1) / BM;
+    return grouped ? (rows + bm - 1) / bm + experts : (rows + bm - 1) / bm;
+}
+
+template <int MODE, int BMT>
+void launch_dma(const GemmArgs &a, const LinearPlan &plan, dim3 grid, hipStream_t stream)
+{
+    if (MODE == MODE_FULL && plan.range_addr)
+        hipLaunchKernelGGL((gemm_f16_dma_kernel<MODE, BMT, true>), grid, dim3(256), 0, stream, a);
+    else
+        hipLaunchKernelGGL((gemm_f16_dma_kernel<MODE, BMT, false>), grid, dim3(256), 0, stream, a);
 }
 
 }  // namespace
 
 int gemm_rows_per_block() { return BN; }
-int gemm_tokens_per_block() { return BM; }
+int gemm_tokens_per_block(int variant) { return variant == GEMM_DMA_256 ? 256 : BM; }
 
 hipError_t launch_gemm_f16(const LinearProblem &p, const LinearPlan &plan, float *partial,
                            hipStream_t stream)
@@ -373,6 +574,23 @@ hipError_t launch_gemm_f16(const LinearProblem &p, const LinearPlan &plan, float
     a.partial = partial;
     a.scale = nullptr;
     const int64_t nt = (p.n + BN - 1) / BN;
+    if (plan.variant == GEMM_DMA_128 || plan.variant == GEMM_DMA_256) {
+        const int bm = plan.variant == GEMM_DMA_256 ? 256 : 128;
+        dim3 grid((unsigned)(nt * plan.splits),
+                  (unsigned)token_tiles(p.rows, p.experts, p.offsets != nullptr, bm), 1);
+        if (p.mode == MODE_FULL) {
+            if (bm == 256)
+                launch_dma<MODE_FULL, 256>(a, plan, grid, stream);
+            else
+                launch_dma<MODE_FULL, 128>(a, plan, grid, stream);
+        } else {
+            if (bm == 256)
+                launch_dma<MODE_FAST, 256>(a, plan, grid, stream);
+            else
+                launch_dma<MODE_FAST, 128>(a, plan, grid, stream);
+        }
+        return hipGetLastError();
+    }
     dim3 grid((unsigned)(nt * plan.splits),
               (unsigned)token_tiles(p.rows, p.experts, p.offsets != nullptr), 1);
     if (p.mode == MODE_FULL) {

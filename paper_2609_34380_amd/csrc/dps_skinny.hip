@@ -1,19 +1,25 @@
-// dps_skinny.hip -- decode-shaped nested linear (few activation rows), gfx950.
+// dps_skinny.hip -- decode-shaped nested linear (up to 64 activation rows per
+// pass), gfx950.
 //
-// Y = X . W^T with W read straight from HBM into registers, merged there
-// (full mode) or zero-extended (fast mode) into FP16 operands, and fed to
-// v_mfma_f32_16x16x32_f16 with the weights as the A operand (16 weight rows
-// per tile) and the activations as the B operand (16 tokens per tile, rows
-// past the end read as zero).  The op is bound by the weight stream, so:
-//   - every weight byte is loaded exactly once, in 16-byte vectors, by one
-//     lane; a wave covers 16 rows x 64 bytes per load instruction;
-//   - the K dimension is cut into `splits` ranges (grid.y) so that enough
-//     waves stream concurrently; each range writes fp32 partials that a
-//     second kernel sums in a fixed order (deterministic, no atomics);
-//   - each lane's residual bytes for one row and one K range fall into at
-//     most two chunks, resolved once before the loop (RANGE), or the chunk
-//     table is read per vector when a range is longer than a chunk.
-// Within one 64-element K block the lane group g = lane/16 holds elements
+// Y = X . W^T with W streamed from HBM straight into registers with
+// nontemporal 16-byte loads, merged there (full mode) or zero-extended (fast
+// mode) into FP16 operands and fed to v_mfma_f32_16x16x32_f16 with the weights
+// as the A operand (16 weight rows per tile) and the activations as the B
+// operand (16 tokens per tile).  The op is bound by the weight stream:
+//   - every weight byte is loaded once, by one lane, in a 16-byte vector; a
+//     wave covers 16 rows x 64 bytes per load instruction;
+//   - weight batches are ping-ponged: the loads of batch b+1 are in flight
+//     while batch b is multiplied;
+//   - the block's slice of X ([rows][K range], FP16) is staged once in LDS
+//     and read back as B operands, so activations cost no global traffic in
+//     the loop and no registers across it;
+//   - K is cut into `splits` ranges (grid.y) so that enough waves stream at
+//     once; each range writes fp32 partials that a second kernel sums in a
+//     fixed order (deterministic, no atomics);
+//   - a lane's residual bytes for one row and one K range fall into at most
+//     two chunks, resolved once before the loop (RANGE), or the chunk table
+//     is read per vector when a range is longer than a chunk.
+// Within one 64-element K block, lane group g = lane/16 holds elements
 // 16g .. 16g+15 of its row; the first MFMA takes the low 8, the second the
 // high 8.  A and B use the same assignment, so the contraction is complete.
 #include "dps_internal.h"
@@ -21,6 +27,8 @@
 namespace dps {
 
 namespace {
+
+constexpr int kWaves = 4;  // waves per block; each owns 16 * RT weight rows
 
 struct SkinnyArgs {
     const uint16_t *x;
@@ -32,13 +40,116 @@ struct SkinnyArgs {
     uint16_t *y;
     float *partial;
     int splits;
+    int x_rows;    // X rows staged in LDS per pass (<= 16 * MT)
 };
 
-template <int MODE, int RT, int MT, int U, int WPG, bool RANGE>
-__global__ __launch_bounds__(WPG * 64) void skinny_kernel(SkinnyArgs a)
+__device__ __forceinline__ u32x4 load_nt(const void *p)
 {
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+}
+
+// v if keep, else zero -- as a bitwise mask, so the compiler keeps the load
+// unconditional instead of turning a select of a load into a branch.
+__device__ __forceinline__ u32x4 select16(bool keep, u32x4 v)
+{
+    const uint32_t m = 0u - (uint32_t)keep;
+    return v & u32x4{m, m, m, m};
+}
+
+// Per-lane row state for the weight stream.  Every load below is issued
+// unconditionally: lanes whose row, K position or residual chunk is out of
+// range read an always-valid address instead (safe_*) and zero the value
+// with a select.  Branch-free loads let the compiler wait only for the batch
+// it is about to multiply while the next batch stays in flight.
+template <int RT>
+struct RowState {
+    const uint8_t *hrow[RT];   // upper-byte row base (clamped to row 0 if beyond n)
+    int64_t lrow[RT];          // logical residual offset of the row
+    bool rok[RT];
+    RangeResidual rr[RT];
+};
+
+template <int MODE, int RT, int U, bool RANGE>
+struct WBatch {
+    u32x4 h[U][RT];
+    u32x4 l[MODE == MODE_FULL ? U : 1][RT];
+
+    // Loads the batch starting at K position kb; `live` false loads a dummy
+    // (cached) vector per lane and yields zeros.
+    __device__ __forceinline__ void load(const RowState<RT> &st, const ResidualView &res,
+                                         int64_t kb, int64_t ke, int64_t klast, bool live, int lg)
+    {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t kk = kb + u * 64 + lg * 16;
+            const bool kin = live && kk < ke;
+            const int64_t ks = kin ? kk : klast;
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) {
+                const bool ok = kin && st.rok[rt];
+                h[u][rt] = select16(ok, load_nt(st.hrow[rt] + ks));
+                if (MODE == MODE_FULL) {
+                    const int64_t li = st.lrow[rt] + ks;
+                    if (RANGE) {
+                        const RangeResidual &r = st.rr[rt];
+                        const bool second = li >= r.bnd;
+                        const bool cok = second ? r.ok1 : r.ok0;
+                        const int64_t d = second ? r.delta1 : r.delta0;
+                        const int64_t off = cok ? d + li : 0;
+                        l[u][rt] = select16(ok && cok, load_nt(res.pool + off));
+                    } else {
+                        const int64_t off = residual_offset(res, li);
+                        l[u][rt] = select16(ok && off >= 0, load_nt(res.pool + (off >= 0 ? off : 0)));
+                    }
+                }
+            }
+        }
+    }
+};
+
+template <int MODE, int RT, int MT, int U, bool RANGE>
+__device__ __forceinline__ void compute_batch(const WBatch<MODE, RT, U, RANGE> &w,
+                                              const uint16_t *xs, int xpitch, int xrow_last,
+                                              int64_t kb, int64_t kb0, int64_t ke,
+                                              const bool *xok, int li, int lg,
+                                              f32x4 (&acc)[RT][MT])
+{
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int64_t kk = kb + u * 64 + lg * 16;
+        const bool kin = kk < ke;
+        const int64_t kc = (kin ? kk : kb0) - kb0;
+        half8 b0[MT], b1[MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            const bool ok = xok[mt] && kin;
+            const int r = ok ? mt * 16 + li : xrow_last;
+            const uint16_t *src = xs + r * xpitch + kc;
+            b0[mt] = as_half8(select16(ok, *reinterpret_cast<const u32x4 *>(src)));
+            b1[mt] = as_half8(select16(ok, *reinterpret_cast<const u32x4 *>(src + 8)));
+        }
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+            const u32x4 h = w.h[u][rt];
+            const u32x4 l = MODE == MODE_FULL ? w.l[u][rt] : u32x4{0u, 0u, 0u, 0u};
+            const half8 a0 = merge8(h.x, h.y, l.x, l.y);
+            const half8 a1 = merge8(h.z, h.w, l.z, l.w);
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                acc[rt][mt] = mfma16x16x32(a0, b0[mt], acc[rt][mt]);
+                acc[rt][mt] = mfma16x16x32(a1, b1[mt], acc[rt][mt]);
+            }
+        }
+    }
+}
+
+template <int MODE, int RT, int MT, int U, bool RANGE>
+__global__ __launch_bounds__(kWaves * 64) void skinny_kernel(SkinnyArgs a)
+{
+    extern __shared__ __attribute__((aligned(16))) uint16_t xs[];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
     const int li = lane & 15;
     const int lg = lane >> 4;
     const int e = blockIdx.z;
@@ -50,94 +161,73 @@ __global__ __launch_bounds__(WPG * 64) void skinny_kernel(SkinnyArgs a)
         row1 = o1 < row0 ? row0 : (o1 > a.rows ? a.rows : o1);
     }
     if (row0 >= row1)
-        return;
-    const int64_t nb = ((int64_t)blockIdx.x * WPG + wave) * (16 * RT);
-    if (nb >= a.n)
-        return;
+        return;  // uniform across the block
+    const int64_t nb = ((int64_t)blockIdx.x * kWaves + wave) * (16 * RT);
+    const bool active = nb < a.n;  // whole wave has rows (no early return: barriers below)
     const int s = blockIdx.y;
     const int64_t kb0 = (int64_t)s * a.ksplit;
     const int64_t ke = kb0 + a.ksplit < a.k ? kb0 + a.ksplit : a.k;
+    const int64_t klen = ke > kb0 ? ke - kb0 : 0;
+    const int xpitch = (int)a.ksplit + 8;
 
-    const uint8_t *hrow[RT];
-    int64_t lrow[RT];
-    bool rok[RT];
-    RangeResidual rr[RT];
+    RowState<RT> st;
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
         const int64_t nr = nb + rt * 16 + li;
-        rok[rt] = nr < a.n;
-        lrow[rt] = ((int64_t)e * a.n + nr) * a.k;
-        hrow[rt] = a.hi + lrow[rt];
-        if (MODE == MODE_FULL && RANGE) {
-            rr[rt].ok0 = rr[rt].ok1 = false;
-            rr[rt].delta0 = rr[rt].delta1 = 0;
-            rr[rt].bnd = 0;
-            if (rok[rt] && ke > kb0)
-                rr[rt] = range_residual(a.res, lrow[rt] + kb0, lrow[rt] + ke);
-        }
+        st.rok[rt] = nr < a.n;
+        st.lrow[rt] = ((int64_t)e * a.n + (st.rok[rt] ? nr : 0)) * a.k;
+        st.hrow[rt] = a.hi + st.lrow[rt];
+        st.rr[rt].ok0 = st.rr[rt].ok1 = false;
+        st.rr[rt].delta0 = st.rr[rt].delta1 = 0;
+        st.rr[rt].bnd = 0;
+        if (MODE == MODE_FULL && RANGE && klen > 0)
+            st.rr[rt] = range_residual(a.res, st.lrow[rt] + kb0, st.lrow[rt] + ke);
     }
+    const int64_t klast = klen > 0 ? ke - 16 : 0;  // an in-range K position for dummy loads
 
-    for (int64_t mg = row0; mg < row1; mg += 16 * MT) {
+    for (int64_t mg = row0; mg < row1; mg += a.x_rows) {
+        const int64_t mrows = row1 - mg < a.x_rows ? row1 - mg : a.x_rows;
+        // ---- stage X[mg .. mg+mrows)[kb0 .. ke) into LDS --------------------------
+        __syncthreads();
+        {
+            const int64_t vpr = klen >> 3;  // 16-byte vectors per row
+            const int64_t total = mrows * vpr;
+            for (int64_t v = tid; v < total; v += kWaves * 64) {
+                const int64_t r = v / vpr;
+                const int64_t c = v - r * vpr;
+                *reinterpret_cast<u32x4 *>(xs + r * xpitch + c * 8) =
+                    load16(a.x + (mg + r) * a.k + kb0 + c * 8);
+            }
+        }
+        __syncthreads();
+        if (!active)
+            continue;
+
         f32x4 acc[RT][MT];
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
                 acc[rt][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-        const uint16_t *xrow[MT];
         bool xok[MT];
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            const int64_t m = mg + mt * 16 + li;
-            xok[mt] = m < row1;
-            xrow[mt] = a.x + m * a.k;
-        }
+        for (int mt = 0; mt < MT; ++mt)
+            xok[mt] = mt * 16 + li < mrows;
 
-        for (int64_t kb = kb0; kb < ke; kb += 64 * U) {
-            u32x4 wh[U][RT], wl[U][RT], xv[U][MT][2];
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int64_t kk = kb + u * 64 + lg * 16;
-                const bool kin = kk < ke;
-#pragma unroll
-                for (int rt = 0; rt < RT; ++rt) {
-                    const u32x4 z = {0u, 0u, 0u, 0u};
-                    wh[u][rt] = z;
-                    wl[u][rt] = z;
-                    if (rok[rt] && kin) {
-                        wh[u][rt] = load16(hrow[rt] + kk);
-                        if (MODE == MODE_FULL)
-                            wl[u][rt] = RANGE ? load_lo_range(a.res, rr[rt], lrow[rt] + kk)
-                                              : load_lo_lookup(a.res, lrow[rt] + kk);
-                    }
-                }
-#pragma unroll
-                for (int mt = 0; mt < MT; ++mt) {
-                    const u32x4 z = {0u, 0u, 0u, 0u};
-                    xv[u][mt][0] = z;
-                    xv[u][mt][1] = z;
-                    if (xok[mt] && kin) {
-                        xv[u][mt][0] = load16(xrow[mt] + kk);
-                        xv[u][mt][1] = load16(xrow[mt] + kk + 8);
-                    }
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-#pragma unroll
-                for (int rt = 0; rt < RT; ++rt) {
-                    const u32x4 h = wh[u][rt];
-                    const u32x4 l = MODE == MODE_FULL ? wl[u][rt] : u32x4{0u, 0u, 0u, 0u};
-                    const half8 a0 = merge8(h.x, h.y, l.x, l.y);
-                    const half8 a1 = merge8(h.z, h.w, l.z, l.w);
-#pragma unroll
-                    for (int mt = 0; mt < MT; ++mt) {
-                        acc[rt][mt] = mfma16x16x32(a0, as_half8(xv[u][mt][0]), acc[rt][mt]);
-                        acc[rt][mt] = mfma16x16x32(a1, as_half8(xv[u][mt][1]), acc[rt][mt]);
-                    }
-                }
-            }
+        constexpr int KB = 64 * U;
+        const int64_t nbatch = (klen + KB - 1) / KB;
+        const int xrow_last = (int)mrows - 1;
+        WBatch<MODE, RT, U, RANGE> wa, wb;
+        wa.load(st, a.res, kb0, ke, klast, nbatch > 0, lg);
+        for (int64_t b = 0; b < nbatch; b += 2) {
+            wb.load(st, a.res, kb0 + (b + 1) * KB, ke, klast, b + 1 < nbatch, lg);
+            compute_batch<MODE, RT, MT, U, RANGE>(wa, xs, xpitch, xrow_last, kb0 + b * KB, kb0,
+                                                  ke, xok, li, lg, acc);
+            wa.load(st, a.res, kb0 + (b + 2) * KB, ke, klast, b + 2 < nbatch, lg);
+            if (b + 1 < nbatch)
+                compute_batch<MODE, RT, MT, U, RANGE>(wb, xs, xpitch, xrow_last,
+                                                      kb0 + (b + 1) * KB, kb0, ke, xok, li, lg,
+                                                      acc);
         }
 
         // lane holds D[4*lg + r][li]: weight rows n0..n0+3 of token m
@@ -147,7 +237,7 @@ __global__ __launch_bounds__(WPG * 64) void skinny_kernel(SkinnyArgs a)
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
                 const int64_t m = mg + mt * 16 + li;
-                if (m >= row1 || n0 >= a.n)
+                if (mt * 16 + li >= mrows || n0 >= a.n)
                     continue;
                 const f32x4 v = acc[rt][mt];
                 if (a.splits == 1) {
@@ -176,25 +266,26 @@ __global__ __launch_bounds__(WPG * 64) void skinny_kernel(SkinnyArgs a)
     }
 }
 
-// Tile variants: rows per wave = 16 * RT, K elements per batch = 64 * U.
+// Tile variants (rows per wave = 16 * RT, K elements per batch = 64 * U).
 struct SkinnyVariant {
-    int rt, u, wpg;
+    int rt, u;
 };
-constexpr SkinnyVariant kVariants[] = {{2, 4, 4}, {1, 4, 4}, {2, 2, 4}, {1, 8, 4}};
+constexpr SkinnyVariant kVariants[] = {{2, 4}, {1, 4}, {2, 2}, {1, 8}};
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 
-template <int MODE, int RT, int MT, int U, int WPG>
+template <int MODE, int RT, int MT, int U>
 hipError_t launch_t(const SkinnyArgs &args, const LinearPlan &plan, int64_t experts,
                     hipStream_t stream)
 {
-    const int64_t rows_per_block = (int64_t)WPG * RT * 16;
+    const int64_t rows_per_block = (int64_t)kWaves * RT * 16;
     dim3 grid((unsigned)((args.n + rows_per_block - 1) / rows_per_block), (unsigned)plan.splits,
               (unsigned)experts);
+    const size_t lds = (size_t)args.x_rows * (size_t)(args.ksplit + 8) * 2;
     if (plan.range_addr)
-        hipLaunchKernelGGL((skinny_kernel<MODE, RT, MT, U, WPG, true>), grid, dim3(WPG * 64), 0,
+        hipLaunchKernelGGL((skinny_kernel<MODE, RT, MT, U, true>), grid, dim3(kWaves * 64), lds,
                            stream, args);
     else
-        hipLaunchKernelGGL((skinny_kernel<MODE, RT, MT, U, WPG, false>), grid, dim3(WPG * 64), 0,
+        hipLaunchKernelGGL((skinny_kernel<MODE, RT, MT, U, false>), grid, dim3(kWaves * 64), lds,
                            stream, args);
     return hipGetLastError();
 }
@@ -204,10 +295,10 @@ hipError_t launch_mt(const SkinnyArgs &args, const LinearPlan &plan, int64_t exp
                      hipStream_t stream)
 {
     switch (plan.variant) {
-    case 0: return launch_t<MODE, 2, MT, 4, 4>(args, plan, experts, stream);
-    case 1: return launch_t<MODE, 1, MT, 4, 4>(args, plan, experts, stream);
-    case 2: return launch_t<MODE, 2, MT, 2, 4>(args, plan, experts, stream);
-    case 3: return launch_t<MODE, 1, MT, 8, 4>(args, plan, experts, stream);
+    case 0: return launch_t<MODE, 2, MT, 4>(args, plan, experts, stream);
+    case 1: return launch_t<MODE, 1, MT, 4>(args, plan, experts, stream);
+    case 2: return launch_t<MODE, 2, MT, 2>(args, plan, experts, stream);
+    case 3: return launch_t<MODE, 1, MT, 8>(args, plan, experts, stream);
     default: return hipErrorInvalidValue;
     }
 }
@@ -226,11 +317,16 @@ hipError_t launch_mode(const SkinnyArgs &args, const LinearPlan &plan, int mt, i
 }  // namespace
 
 int skinny_variant_count() { return kNumVariants; }
-int skinny_rows_per_block(int variant)
-{
-    return kVariants[variant].wpg * kVariants[variant].rt * 16;
-}
+int skinny_rows_per_block(int variant) { return kWaves * kVariants[variant].rt * 16; }
 int skinny_k_per_batch(int variant) { return kVariants[variant].u * 64; }
+
+// Tokens per pass for a call with `rows` rows in total (dense) or grouped.
+int skinny_pass_rows(int64_t rows, bool grouped)
+{
+    if (grouped)
+        return 64;
+    return rows <= 16 ? (int)rows : (rows <= 32 ? (int)rows : (int)(rows < 64 ? rows : 64));
+}
 
 hipError_t launch_skinny(const LinearProblem &p, const LinearPlan &plan, float *partial,
                          hipStream_t stream)
@@ -247,10 +343,8 @@ hipError_t launch_skinny(const LinearProblem &p, const LinearPlan &plan, float *
     args.y = p.y;
     args.partial = partial;
     args.splits = plan.splits;
-    // tokens per pass: 16 * mt; grouped calls loop over passes per expert
-    int mt = 4;
-    if (!p.offsets)
-        mt = p.rows <= 16 ? 1 : (p.rows <= 32 ? 2 : 4);
+    args.x_rows = skinny_pass_rows(p.rows, p.offsets != nullptr);
+    const int mt = (args.x_rows + 15) / 16;
     return p.mode == MODE_FULL ? launch_mode<MODE_FULL>(args, plan, mt, p.experts, stream)
                                : launch_mode<MODE_FAST>(args, plan, mt, p.experts, stream);
 }
