@@ -45,6 +45,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--roofline-reps", type=int, default=40)
+    ap.add_argument("--probe-call", default=None,
+                    help="LAYER:M:MODE -- run only that call (for rocprofv3) and a copy "
+                         "kernel of known size, then exit")
+    ap.add_argument("--probe-reps", type=int, default=20)
     return ap.parse_args()
 
 
@@ -70,6 +74,9 @@ def main():
     stream = torch.cuda.Stream()
 
     layers = workloads.H4096_SET
+    if args.probe_call:
+        probe(args, torch, dps, workloads, layers, dev, stream)
+        return
     ms = workloads.DECODE_M
     modes = (("fast", dps.MODE_FAST), ("full", dps.MODE_FULL))
 
@@ -167,7 +174,13 @@ def main():
                               "roofline_frac": round(bound_t / t, 3)})
 
     # ---- dominant call: back-to-back launches between events ----------------------
-    dom = max(breakdown, key=lambda b: b["us"])
+    # the slowest call that is a single kernel (no split-K reduction launch), so
+    # its event time is one kernel's duration and matches rocprofv3's
+    single = [b for b in breakdown
+              if dps.workspace_bytes(dps.MODE_FAST if b["mode"] == "fast" else dps.MODE_FULL, 0,
+                                     b["M"], *[(n, k) for nm, n, k in layers
+                                               if nm == b["layer"]][0]) == 0]
+    dom = max(single or breakdown, key=lambda b: b["us"])
     dm, dmode = dom["M"], dps.MODE_FAST if dom["mode"] == "fast" else dps.MODE_FULL
     dli = [l[0] for l in layers].index(dom["layer"])
     _, dn, dk = layers[dli]
@@ -196,8 +209,9 @@ def main():
         roof = {"bound": "mfma", "achieved": round(flops / t_launch / 1e12, 1),
                 "peak": MFMA_F16_TFLOPS, "unit": "TFLOP/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = None
+    roof["traffic"] = measured_traffic("%s:%d:%s" % (dom["layer"], dm, dom["mode"]))
     roof["kernel"] = ("%s layer %dx%d, M=%d, %s mode" % (dom["layer"], dn, dk, dm, dom["mode"]))
+    roof["probe_call"] = "%s:%d:%s" % (dom["layer"], dm, dom["mode"])
     roof["us_per_launch"] = round(t_launch * 1e6, 2)
     roof["algorithmic_bytes_per_launch"] = alg_bytes
 
@@ -237,6 +251,70 @@ def main():
         "secondary": secondary,
     }
     print(json.dumps(out), flush=True)
+
+
+def measured_traffic(probe_call):
+    """HBM bytes per launch of the dominant kernel from the committed rocprofv3
+    counter record (profiles/*_traffic.md), or None when no record matches this
+    call or the kernel sources changed since the counters were taken."""
+    import glob
+    import hashlib
+
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_34380_amd", "csrc")
+    for f in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.h"))):
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    digest = h.hexdigest()
+    for path in glob.glob(os.path.join(ROOT, "profiles", "*_traffic.md")):
+        with open(path) as fh:
+            for line in fh:
+                line = line.strip()
+                if line.startswith("{") and "csrc_sha256" in line:
+                    rec = json.loads(line)
+                    if rec.get("probe_call") == probe_call and rec.get("csrc_sha256") == digest:
+                        return rec["traffic_bytes_per_launch"]
+    return None
+
+
+def probe(args, torch, dps, workloads, layers, dev, stream):
+    """One call of the decode set, launched back to back on rotating weight
+    copies, then a device-to-device copy of 256 MiB (a kernel of known HBM
+    traffic, to calibrate rocprofv3's FETCH_SIZE / WRITE_SIZE)."""
+    name, m, mode_name = args.probe_call.split(":")
+    m = int(m)
+    mode = dps.MODE_FAST if mode_name == "fast" else dps.MODE_FULL
+    li = [l[0] for l in layers].index(name)
+    _, n, k = layers[li]
+    with torch.cuda.stream(stream):
+        nws = []
+        for c in range(COPIES):
+            w = workloads.weight_fp16(n, k, seed=1000 * c + li, device=dev)
+            nws.append(dps.split(w, dps.make_residual(n * k, LOG2_CHUNK, dev)))
+            del w
+        x = workloads.activations_fp16(m, k, seed=m * 7 + k, device=dev)
+        y = torch.empty((m, n), dtype=torch.float16, device=dev)
+        need = dps.workspace_bytes(mode, 0, m, n, k)
+        ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+        for r in range(COPIES):
+            dps.linear(x, nws[r], mode, out=y, workspace=ws)
+        stream.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for r in range(args.probe_reps):
+            dps.linear(x, nws[r % COPIES], mode, out=y, workspace=ws)
+        e1.record(stream)
+        stream.synchronize()
+        src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        stream.synchronize()
+    t = e0.elapsed_time(e1) * 1e-3 / args.probe_reps
+    print(json.dumps({"probe_call": args.probe_call, "us_per_call": round(t * 1e6, 2),
+                      "kernels_per_call": 1 if need == 0 else 2,
+                      "copy_bytes_each_way": 256 << 20}), flush=True)
 
 
 def prefill_secondary(torch, dps, workloads, nws, layers, stream):

@@ -12,6 +12,7 @@ namespace dps {
 int skinny_rows_per_block(int variant);
 int skinny_k_per_batch(int variant);
 int skinny_pass_rows(int64_t rows, bool grouped);
+int64_t skinny_max_ksplit(int variant, int mode, int64_t pass_rows);
 int gemm_rows_per_block();
 int gemm_tokens_per_block(int variant);
 }  // namespace dps
@@ -134,14 +135,16 @@ LinearPlan plan_linear(int mode, uint32_t flags, int64_t rows, int64_t n, int64_
         p.ws_quant = align256(rows * k) + align256(rows * 4);
     } else if (rows_per_expert <= 64) {
         p.kind = KIND_SKINNY;
-        // measured on MI355X: 16 rows per wave for up to 16 tokens, 32 rows with
-        // half-length batches above that (lighter register footprints win)
-        p.variant = rows_per_expert <= 16 ? 1 : 2;
-        const int64_t kpb = skinny_k_per_batch(p.variant);
-        // the block's X slice [pass rows][ksplit + 8] FP16 lives in 64 KiB of LDS
+        // measured on MI355X: up to 8 tokens, the weight stream through shallow
+        // per-wave LDS rings (two blocks per CU); above that, registers with
+        // 16 rows per wave up to 16 tokens and 32 rows (half batches) beyond
         const int64_t xr = skinny_pass_rows(rows, grouped);
-        int64_t kmax = (32768 / xr - 8) / kpb * kpb;
-        kmax = kmax < kpb ? kpb : kmax;
+        p.variant = xr <= 16 ? 1 : 2;
+        if (xr <= 8 && skinny_max_ksplit(SKINNY_RING_HALF, mode, xr) > 0)
+            p.variant = SKINNY_RING_HALF;
+        const int64_t kpb = skinny_k_per_batch(p.variant);
+        // the block's X slice [pass rows][ksplit + 8] FP16 must fit its LDS share
+        const int64_t kmax = skinny_max_ksplit(p.variant, mode, xr);
         const int64_t blocks = cdiv(n, skinny_rows_per_block(p.variant)) * experts;
         int64_t s = cdiv((int64_t)cu_count, blocks);
         const int64_t smax = k / kpb > 1 ? k / kpb : 1;
@@ -155,7 +158,10 @@ LinearPlan plan_linear(int mode, uint32_t flags, int64_t rows, int64_t n, int64_
         // measured on MI355X: the LDS-DMA pipeline wins with one byte plane
         // (fast mode), the register-staged kernel with two (full mode); K is
         // split only until the tiles cover the CUs, keeping >= 1024 per range
-        p.variant = mode == MODE_FAST ? GEMM_DMA_128 : GEMM_REG_128;
+        // above 128 tokens per expert, full mode takes 256-token tiles so that
+        // each weight tile is fetched once (128-token tiles fetch it twice)
+        p.variant = mode == MODE_FAST ? GEMM_DMA_128
+                                      : (rows_per_expert > 128 ? GEMM_DMA_256 : GEMM_REG_128);
         const int64_t tiles =
             cdiv(n, gemm_rows_per_block()) * cdiv(rows, gemm_tokens_per_block(p.variant));
         int64_t s = cdiv((int64_t)cu_count, tiles);

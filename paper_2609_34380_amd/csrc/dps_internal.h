@@ -39,6 +39,9 @@ enum KernelKind { KIND_SKINNY = 0, KIND_GEMM_F16 = 1, KIND_GEMM_FP8 = 2 };
 // FP16 GEMM variants: register-staged 128-token tiles, or the LDS-DMA pipeline
 // with 128- or 256-token tiles (128 weight rows each).
 enum GemmVariant { GEMM_REG_128 = 0, GEMM_DMA_128 = 1, GEMM_DMA_256 = 2 };
+// Decode-kernel variants 0..3 keep the weight stream in registers (tile
+// shapes differ); SKINNY_RING streams it through per-wave LDS rings.
+enum { SKINNY_RING = 4, SKINNY_RING_HALF = 5 };
 
 // Kernel choice and work split for one call.  plan_linear is the single
 // place that decides; dps_workspace_bytes and the launch both call it.

@@ -266,6 +266,209 @@ __global__ __launch_bounds__(kWaves * 64) void skinny_kernel(SkinnyArgs a)
     }
 }
 
+// ------------------------------------------------------------------------------
+// Ring variant: the weight stream goes global -> LDS with direct-to-LDS loads
+// (gfx950 global_load_lds_dwordx4) through a private ring of RING stages per
+// wave, so many stages are in flight without holding registers.  A stage is
+// 16 weight rows x 256 K bytes per plane; each of its DMA instructions reads 4
+// rows x 256 contiguous bytes.  Within a row the 16-byte chunk for K offset
+// 16c sits at slot c ^ (row % 16), which makes the MFMA-layout reads (16 rows
+// at one K offset) hit distinct banks.  X is the only other global traffic and
+// is staged before the stream starts, so the wait for stage t is a plain
+// vmcnt on this wave's own DMA queue -- no barriers inside the loop.
+// ------------------------------------------------------------------------------
+constexpr int RING_SK = 256;                    // K bytes per stage and plane
+constexpr int RING_STAGE_PLANE = 16 * RING_SK;  // 4 KiB
+
+__device__ __attribute__((aligned(16))) const uint8_t g_zero16_s[16] = {0};
+
+#define DPS_LDS_PTR(p) ((__attribute__((address_space(3))) void *)(p))
+#define DPS_WAIT_VM(n) \
+    __builtin_amdgcn_s_waitcnt(((n) & 0xF) | ((((n) >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8))
+
+template <int MODE, int MT, int RING, bool RANGE>
+__global__ __launch_bounds__(kWaves * 64) void ring_kernel(SkinnyArgs a)
+{
+    constexpr int PLANES = MODE == MODE_FULL ? 2 : 1;
+    constexpr int STAGE = RING_STAGE_PLANE * PLANES;
+    constexpr int NI = 4 * PLANES;  // DMA instructions per stage and wave
+    extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int li = lane & 15;
+    const int lg = lane >> 4;
+    const int e = blockIdx.z;
+
+    int64_t row0 = 0, row1 = a.rows;
+    if (a.offsets) {
+        const int64_t o0 = a.offsets[e], o1 = a.offsets[e + 1];
+        row0 = o0 < 0 ? 0 : (o0 > a.rows ? a.rows : o0);
+        row1 = o1 < row0 ? row0 : (o1 > a.rows ? a.rows : o1);
+    }
+    if (row0 >= row1)
+        return;  // uniform across the block
+    const int64_t nb = ((int64_t)blockIdx.x * kWaves + wave) * 16;
+    const bool active = nb < a.n;
+    const int s = blockIdx.y;
+    const int64_t kb0 = (int64_t)s * a.ksplit;
+    const int64_t ke = kb0 + a.ksplit < a.k ? kb0 + a.ksplit : a.k;
+    const int64_t klen = ke > kb0 ? ke - kb0 : 0;
+    const int xpitch = (int)a.ksplit + 8;  // halfs
+    uint16_t *xs = reinterpret_cast<uint16_t *>(lds);
+    uint8_t *ring = lds + (((size_t)a.x_rows * xpitch * 2 + 255) & ~(size_t)255) +
+                    (size_t)wave * RING * STAGE;
+
+    // DMA sources: instruction j of a stage covers rows 4j .. 4j+3; lane l ->
+    // row 4j + l/16, slot l%16, logical 16-byte chunk (l%16) ^ row
+    const uint8_t *wsrc[4];
+    int64_t wl[4];
+    int wchunk[4];
+    RangeResidual rr[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int r = 4 * j + (lane >> 4);
+        int64_t nr = nb + r;
+        nr = nr < a.n ? nr : a.n - 1;
+        wl[j] = ((int64_t)e * a.n + nr) * a.k;
+        wsrc[j] = a.hi + wl[j];
+        wchunk[j] = (lane & 15) ^ r;
+        rr[j].ok0 = rr[j].ok1 = false;
+        rr[j].delta0 = rr[j].delta1 = 0;
+        rr[j].bnd = 0;
+        if (MODE == MODE_FULL && RANGE && klen > 0)
+            rr[j] = range_residual(a.res, wl[j] + kb0, wl[j] + ke);
+    }
+    const int64_t nstage = (klen + RING_SK - 1) / RING_SK;
+
+    auto issue = [&](int64_t t) {
+        uint8_t *st = ring + (int)(t % RING) * STAGE;
+        const bool live = t < nstage;
+        const int64_t kt = kb0 + t * RING_SK;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t kk = kt + wchunk[j] * 16;
+            const bool ok = live && kk < ke;
+            __builtin_amdgcn_global_load_lds(ok ? (const void *)(wsrc[j] + kk)
+                                                : (const void *)g_zero16_s,
+                                             DPS_LDS_PTR(st + j * 1024), 16, 0, 0);
+            if (MODE == MODE_FULL) {
+                const int64_t lo = wl[j] + (ok ? kk : kb0);
+                const void *src = g_zero16_s;
+                if (RANGE) {
+                    const bool second = lo >= rr[j].bnd;
+                    const bool cok = second ? rr[j].ok1 : rr[j].ok0;
+                    const int64_t d = second ? rr[j].delta1 : rr[j].delta0;
+                    if (ok && cok)
+                        src = a.res.pool + (d + lo);
+                } else {
+                    const int64_t off = residual_offset(a.res, lo);
+                    if (ok && off >= 0)
+                        src = a.res.pool + off;
+                }
+                __builtin_amdgcn_global_load_lds(src, DPS_LDS_PTR(st + RING_STAGE_PLANE + j * 1024),
+                                                 16, 0, 0);
+            }
+        }
+    };
+
+    for (int64_t mg = row0; mg < row1; mg += a.x_rows) {
+        const int64_t mrows = row1 - mg < a.x_rows ? row1 - mg : a.x_rows;
+        // ---- stage X[mg .. mg+mrows)[kb0 .. ke) into LDS (plain loads) -------------
+        __syncthreads();
+        {
+            const int64_t vpr = klen >> 3;
+            const int64_t total = mrows * vpr;
+            for (int64_t v = tid; v < total; v += kWaves * 64) {
+                const int64_t r = v / vpr;
+                const int64_t c = v - r * vpr;
+                *reinterpret_cast<u32x4 *>(xs + r * xpitch + c * 8) =
+                    load16(a.x + (mg + r) * a.k + kb0 + c * 8);
+            }
+        }
+        __syncthreads();
+        if (!active)
+            continue;
+
+        f32x4 acc[MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+            acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        bool xok[MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+            xok[mt] = mt * 16 + li < mrows;
+        const int xrow_last = (int)mrows - 1;
+
+#pragma unroll
+        for (int t = 0; t < RING - 1; ++t)
+            issue(t);
+        for (int64_t t = 0; t < nstage; ++t) {
+            DPS_WAIT_VM(NI * (RING - 2));
+            const uint8_t *st = ring + (int)(t % RING) * STAGE;
+            const int64_t kt = kb0 + t * RING_SK;
+#pragma unroll
+            for (int q = 0; q < RING_SK / 64; ++q) {
+                // lane (li, lg): row li, K chunk 4q + lg of this stage
+                const int slot = ((4 * q + lg) ^ li) << 4;
+                const u32x4 h = *reinterpret_cast<const u32x4 *>(st + li * RING_SK + slot);
+                u32x4 l = {0u, 0u, 0u, 0u};
+                if (MODE == MODE_FULL)
+                    l = *reinterpret_cast<const u32x4 *>(st + RING_STAGE_PLANE + li * RING_SK + slot);
+                const half8 a0 = merge8(h.x, h.y, l.x, l.y);
+                const half8 a1 = merge8(h.z, h.w, l.z, l.w);
+                const int64_t kk = kt + q * 64 + lg * 16;
+                const bool kin = kk < ke;
+                const int64_t kc = (kin ? kk : kb0) - kb0;
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) {
+                    const bool ok = xok[mt] && kin;
+                    const int r = ok ? mt * 16 + li : xrow_last;
+                    const uint16_t *src = xs + r * xpitch + kc;
+                    const half8 b0 = as_half8(select16(ok, *reinterpret_cast<const u32x4 *>(src)));
+                    const half8 b1 =
+                        as_half8(select16(ok, *reinterpret_cast<const u32x4 *>(src + 8)));
+                    acc[mt] = mfma16x16x32(a0, b0, acc[mt]);
+                    acc[mt] = mfma16x16x32(a1, b1, acc[mt]);
+                }
+            }
+            issue(t + RING - 1);
+        }
+        DPS_WAIT_VM(0);
+
+        // lane holds D[4*lg + r][li]: weight rows n0..n0+3 of token m
+        const int64_t n0 = nb + lg * 4;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            const int64_t m = mg + mt * 16 + li;
+            if (mt * 16 + li >= mrows || n0 >= a.n)
+                continue;
+            const f32x4 v = acc[mt];
+            if (a.splits == 1) {
+                uint16_t *yp = a.y + m * a.n + n0;
+                if (n0 + 3 < a.n && (a.n & 3) == 0) {
+                    typedef _Float16 half4 __attribute__((ext_vector_type(4)));
+                    half4 hv = {(_Float16)v.x, (_Float16)v.y, (_Float16)v.z, (_Float16)v.w};
+                    *reinterpret_cast<half4 *>(yp) = hv;
+                } else {
+                    const float vv[4] = {v.x, v.y, v.z, v.w};
+                    for (int r = 0; r < 4 && n0 + r < a.n; ++r)
+                        yp[r] = __builtin_bit_cast(uint16_t, (_Float16)vv[r]);
+                }
+            } else {
+                float *pp = a.partial + ((int64_t)s * a.rows + m) * a.n + n0;
+                if (n0 + 3 < a.n && (a.n & 3) == 0) {
+                    *reinterpret_cast<f32x4 *>(pp) = v;
+                } else {
+                    const float vv[4] = {v.x, v.y, v.z, v.w};
+                    for (int r = 0; r < 4 && n0 + r < a.n; ++r)
+                        pp[r] = vv[r];
+                }
+            }
+        }
+    }
+}
+
 // Tile variants (rows per wave = 16 * RT, K elements per batch = 64 * U).
 struct SkinnyVariant {
     int rt, u;
@@ -290,11 +493,61 @@ hipError_t launch_t(const SkinnyArgs &args, const LinearPlan &plan, int64_t expe
     return hipGetLastError();
 }
 
+// LDS per block: the deep rings take the whole 160 KiB of a gfx950 CU (one
+// block per CU); the shallow rings take half, so two blocks share a CU.
+template <bool DEEP>
+constexpr int ring_lds() { return DEEP ? 160 * 1024 : 80 * 1024; }
+
+template <int MODE, bool DEEP>
+constexpr int ring_depth() { return MODE == MODE_FULL ? (DEEP ? 3 : 2) : (DEEP ? 6 : 3); }
+
+template <int MODE, bool DEEP>
+constexpr int ring_bytes()
+{
+    return kWaves * ring_depth<MODE, DEEP>() * RING_STAGE_PLANE * (MODE == MODE_FULL ? 2 : 1);
+}
+
+template <int MODE, int MT, bool DEEP>
+hipError_t launch_ring(const SkinnyArgs &args, const LinearPlan &plan, int64_t experts,
+                       hipStream_t stream)
+{
+    constexpr int RING = ring_depth<MODE, DEEP>();
+    constexpr int kRingLds = ring_lds<DEEP>();
+    const size_t xbytes = ((size_t)args.x_rows * (size_t)(args.ksplit + 8) * 2 + 255) & ~(size_t)255;
+    const size_t lds = xbytes + ring_bytes<MODE, DEEP>();
+    if (lds > (size_t)kRingLds)
+        return hipErrorInvalidValue;
+    dim3 grid((unsigned)((args.n + kWaves * 16 - 1) / (kWaves * 16)), (unsigned)plan.splits,
+              (unsigned)experts);
+    if (plan.range_addr) {
+        static bool attr = false;
+        if (!attr) {
+            hipFuncSetAttribute((const void *)ring_kernel<MODE, MT, RING, true>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize, kRingLds);
+            attr = true;
+        }
+        hipLaunchKernelGGL((ring_kernel<MODE, MT, RING, true>), grid, dim3(kWaves * 64), lds,
+                           stream, args);
+    } else {
+        static bool attr = false;
+        if (!attr) {
+            hipFuncSetAttribute((const void *)ring_kernel<MODE, MT, RING, false>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize, kRingLds);
+            attr = true;
+        }
+        hipLaunchKernelGGL((ring_kernel<MODE, MT, RING, false>), grid, dim3(kWaves * 64), lds,
+                           stream, args);
+    }
+    return hipGetLastError();
+}
+
 template <int MODE, int MT>
 hipError_t launch_mt(const SkinnyArgs &args, const LinearPlan &plan, int64_t experts,
                      hipStream_t stream)
 {
     switch (plan.variant) {
+    case SKINNY_RING: return launch_ring<MODE, MT, true>(args, plan, experts, stream);
+    case SKINNY_RING_HALF: return launch_ring<MODE, MT, false>(args, plan, experts, stream);
     case 0: return launch_t<MODE, 2, MT, 4>(args, plan, experts, stream);
     case 1: return launch_t<MODE, 1, MT, 4>(args, plan, experts, stream);
     case 2: return launch_t<MODE, 2, MT, 2>(args, plan, experts, stream);
@@ -317,8 +570,28 @@ hipError_t launch_mode(const SkinnyArgs &args, const LinearPlan &plan, int mt, i
 }  // namespace
 
 int skinny_variant_count() { return kNumVariants; }
-int skinny_rows_per_block(int variant) { return kWaves * kVariants[variant].rt * 16; }
-int skinny_k_per_batch(int variant) { return kVariants[variant].u * 64; }
+int skinny_rows_per_block(int variant)
+{
+    return variant >= SKINNY_RING ? kWaves * 16 : kWaves * kVariants[variant].rt * 16;
+}
+int skinny_k_per_batch(int variant)
+{
+    return variant >= SKINNY_RING ? RING_SK : kVariants[variant].u * 64;
+}
+// Largest K range (multiple of the batch) whose X slice fits the block's LDS.
+int64_t skinny_max_ksplit(int variant, int mode, int64_t pass_rows)
+{
+    const int64_t kpb = skinny_k_per_batch(variant);
+    int64_t budget = 65536;
+    if (variant == SKINNY_RING)
+        budget = ring_lds<true>() - 256 -
+                 (mode == MODE_FULL ? ring_bytes<MODE_FULL, true>() : ring_bytes<MODE_FAST, true>());
+    if (variant == SKINNY_RING_HALF)
+        budget = ring_lds<false>() - 256 -
+                 (mode == MODE_FULL ? ring_bytes<MODE_FULL, false>() : ring_bytes<MODE_FAST, false>());
+    const int64_t kmax = (budget / 2 / pass_rows - 8) / kpb * kpb;
+    return kmax < kpb ? 0 : kmax;  // 0: this variant cannot hold the X slice
+}
 
 // Tokens per pass for a call with `rows` rows in total (dense) or grouped.
 int skinny_pass_rows(int64_t rows, bool grouped)
