@@ -13,7 +13,7 @@ int skinny_rows_per_block(int variant);
 int skinny_k_per_batch(int variant);
 int skinny_pass_rows(int64_t rows, bool grouped);
 int64_t skinny_max_ksplit(int variant, int mode, int64_t pass_rows);
-int gemm_rows_per_block();
+int gemm_rows_per_block(int variant);
 int gemm_tokens_per_block(int variant);
 }  // namespace dps
 
@@ -125,8 +125,9 @@ LinearPlan plan_linear(int mode, uint32_t flags, int64_t rows, int64_t n, int64_
     const int64_t rows_per_expert = grouped ? cdiv(rows, experts) : rows;
     if (flags & DPS_ACT_FP8_ROWSCALE) {
         p.kind = KIND_GEMM_FP8;
+        p.variant = rows > 128 ? GEMM_G3_256x256 : GEMM_G3_256x128;
         const int64_t tiles =
-            cdiv(n, gemm_rows_per_block()) * cdiv(rows, gemm_tokens_per_block(GEMM_REG_128));
+            cdiv(n, gemm_rows_per_block(p.variant)) * cdiv(rows, gemm_tokens_per_block(p.variant));
         int64_t s = cdiv(target, tiles);
         const int64_t smax = k / 1024 > 1 ? k / 1024 : 1;
         s = s < 1 ? 1 : (s > smax ? smax : s);
@@ -160,10 +161,9 @@ LinearPlan plan_linear(int mode, uint32_t flags, int64_t rows, int64_t n, int64_
         // split only until the tiles cover the CUs, keeping >= 1024 per range
         // above 128 tokens per expert, full mode takes 256-token tiles so that
         // each weight tile is fetched once (128-token tiles fetch it twice)
-        p.variant = mode == MODE_FAST ? GEMM_DMA_128
-                                      : (rows_per_expert > 128 ? GEMM_DMA_256 : GEMM_REG_128);
+        p.variant = rows_per_expert > 128 ? GEMM_G3_256x256 : GEMM_G3_256x128;
         const int64_t tiles =
-            cdiv(n, gemm_rows_per_block()) * cdiv(rows, gemm_tokens_per_block(p.variant));
+            cdiv(n, gemm_rows_per_block(p.variant)) * cdiv(rows, gemm_tokens_per_block(p.variant));
         int64_t s = cdiv((int64_t)cu_count, tiles);
         const int64_t smax = k / 1024 > 1 ? k / 1024 : 1;
         s = s < 1 ? 1 : (s > smax ? smax : s);

@@ -430,6 +430,256 @@ __global__ __launch_bounds__(256) void gemm_f16_dma_kernel(GemmArgs a)
 }
 
 // ------------------------------------------------------------------------------
+// Eight-wave LDS-DMA GEMM (two waves per SIMD), FP16 full/fast and FP8 fast
+// ------------------------------------------------------------------------------
+// Block tile BN weight rows x BM tokens, waves in a WN x WM grid, each wave
+// (BN/WN) x (BM/WM).  A stage covers BK K elements: 64 for FP16 (processed as
+// two 32-wide MFMA steps), 128 for FP8 (one 16x16x128 step).  Stages stream
+// global -> LDS by direct-to-LDS loads through a ring of NSTAGE slots, one
+// barrier per stage.  LDS rows hold 16-byte chunks at slot chunk ^ swz(row),
+// swz(row) = (row / rows-per-256-bytes) % chunks-per-row, so the 16 rows a
+// fragment read touches land in 16 distinct 16-byte bank groups.
+//   FP16 step h, lane (i, g): A = weight row i, K 32h+8g .. +7 (8 bytes per
+//   plane, merged into FP16 in registers); B = token row i, same K.
+//   FP8, lane (i, g): A and B = bytes 32g .. 32g+31 of the stage.
+enum { G3_FULL = 0, G3_FAST = 1, G3_FP8 = 2 };
+
+template <int KIND, int BN_, int BM_, int WN, int WM, int NSTAGE>
+struct G3 {
+    static constexpr bool FP8 = KIND == G3_FP8;
+    static constexpr int PLANES = KIND == G3_FULL ? 2 : 1;
+    static constexpr int BK = FP8 ? 128 : 64;
+    static constexpr int WROW = BK;                  // bytes per weight row per plane
+    static constexpr int XROW = FP8 ? BK : 2 * BK;   // bytes per token row
+    static constexpr int W_BYTES = BN_ * WROW;
+    static constexpr int X_BYTES = BM_ * XROW;
+    static constexpr int STAGE = W_BYTES * PLANES + X_BYTES;
+    static constexpr int LDS = STAGE * NSTAGE;
+    static constexpr int NWAVES = WN * WM;
+    static constexpr int W_INSTR = W_BYTES / 1024 / NWAVES;
+    static constexpr int X_INSTR = X_BYTES / 1024 / NWAVES;
+    static constexpr int NI = W_INSTR * PLANES + X_INSTR;
+    static constexpr int TN = BN_ / WN, TM = BM_ / WM;
+    static constexpr int NT = TN / 16, MT = TM / 16;
+    static_assert(W_BYTES % (1024 * NWAVES) == 0 && X_BYTES % (1024 * NWAVES) == 0, "tiling");
+    static_assert(LDS <= 160 * 1024, "LDS");
+};
+
+// slot swizzle for rows of `rowbytes` bytes (64 or 128)
+template <int ROWBYTES>
+__device__ __forceinline__ int g3_swz(int r)
+{
+    return (r / (256 / ROWBYTES)) % (ROWBYTES / 16);
+}
+
+template <int KIND, int BN_, int BM_, int WN, int WM, int NSTAGE, bool RANGE>
+__global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
+{
+    using C = G3<KIND, BN_, BM_, WN, WM, NSTAGE>;
+    __shared__ __attribute__((aligned(16))) uint8_t smem[C::LDS];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int li = lane & 15;
+    const int lg = lane >> 4;
+
+    int64_t e, mrow0, mrow1;
+    int ntile, s;
+    if (a.offsets) {
+        if (!block_rows(a, e, mrow0, mrow1, BM_))
+            return;
+        ntile = blockIdx.x / a.splits;
+        s = blockIdx.x % a.splits;
+    } else {
+        // Dense calls use a 1-D grid remapped for the 8 XCDs: block L runs on
+        // XCD L % 8, so XCD x is given the contiguous tile range
+        // [x * per_xcd, (x+1) * per_xcd), walked with the token tile fastest.
+        // Blocks sharing a weight tile then run together on one XCD and fetch
+        // it into that XCD's L2 once.
+        const int64_t mtiles = (a.rows + BM_ - 1) / BM_;
+        const int64_t ntiles = (a.n + BN_ - 1) / BN_;
+        const int64_t total = mtiles * ntiles * a.splits;
+        const int64_t per_xcd = (total + 7) / 8;
+        const int64_t lin = blockIdx.x;
+        const int64_t t = (lin % 8) * per_xcd + lin / 8;
+        if (t >= total)
+            return;
+        const int64_t mt = t % mtiles;
+        ntile = (int)((t / mtiles) % ntiles);
+        s = (int)(t / (mtiles * ntiles));
+        e = 0;
+        mrow0 = mt * BM_;
+        mrow1 = mrow0 + BM_ < a.rows ? mrow0 + BM_ : a.rows;
+    }
+    const int64_t n0 = (int64_t)ntile * BN_;
+    const int64_t kb0 = (int64_t)s * a.ksplit;
+    const int64_t ke = kb0 + a.ksplit < a.k ? kb0 + a.ksplit : a.k;
+    const int64_t ntk = ke > kb0 ? (ke - kb0 + C::BK - 1) / C::BK : 0;
+
+    // ---- per-lane DMA descriptors (fixed across stages) ---------------------------
+    // weight instruction j: LDS bytes j*1024 .. +1023 of the plane tile
+    const uint8_t *wsrc[C::W_INSTR];
+    int64_t wl[C::W_INSTR];
+    int wel[C::W_INSTR];  // element offset of this lane's chunk within the stage
+    RangeResidual rr[C::W_INSTR];
+#pragma unroll
+    for (int jj = 0; jj < C::W_INSTR; ++jj) {
+        const int j = wave * C::W_INSTR + jj;
+        const int pos = j * 1024 + lane * 16;
+        const int r = pos / C::WROW;
+        const int slot = (pos % C::WROW) / 16;
+        const int chunk = slot ^ g3_swz<C::WROW>(r);
+        int64_t nr = n0 + r;
+        nr = nr < a.n ? nr : a.n - 1;
+        wl[jj] = (e * a.n + nr) * a.k;
+        wsrc[jj] = a.hi + wl[jj];
+        wel[jj] = chunk * 16;
+        rr[jj].ok0 = rr[jj].ok1 = false;
+        rr[jj].delta0 = rr[jj].delta1 = 0;
+        rr[jj].bnd = 0;
+        if (KIND == G3_FULL && RANGE && ke > kb0)
+            rr[jj] = range_residual(a.res, wl[jj] + kb0, wl[jj] + ke);
+    }
+    const uint8_t *xsrc[C::X_INSTR];
+    int xel[C::X_INSTR];
+    constexpr int XELEM = C::FP8 ? 1 : 2;  // bytes per X element
+#pragma unroll
+    for (int jj = 0; jj < C::X_INSTR; ++jj) {
+        const int j = wave * C::X_INSTR + jj;
+        const int pos = j * 1024 + lane * 16;
+        const int r = pos / C::XROW;
+        const int slot = (pos % C::XROW) / 16;
+        const int chunk = slot ^ g3_swz<C::XROW>(r);
+        int64_t m = mrow0 + r;
+        m = m < mrow1 ? m : mrow1 - 1;
+        xsrc[jj] = static_cast<const uint8_t *>(a.x) + m * a.k * XELEM;
+        xel[jj] = chunk * (16 / XELEM);
+    }
+
+    auto issue = [&](int64_t t) {
+        uint8_t *st = smem + (int)(t % NSTAGE) * C::STAGE;
+        const bool live = t < ntk;
+        const int64_t kt = kb0 + t * C::BK;
+#pragma unroll
+        for (int jj = 0; jj < C::W_INSTR; ++jj) {
+            const int j = wave * C::W_INSTR + jj;
+            const int64_t kk = kt + wel[jj];
+            const bool ok = live && kk < ke;
+            dma16(ok ? (const void *)(wsrc[jj] + kk) : (const void *)g_zero16, st + j * 1024);
+            if (KIND == G3_FULL) {
+                const int64_t lo = wl[jj] + (ok ? kk : kb0);
+                const void *src = g_zero16;
+                if (RANGE) {
+                    const bool second = lo >= rr[jj].bnd;
+                    const bool cok = second ? rr[jj].ok1 : rr[jj].ok0;
+                    const int64_t d = second ? rr[jj].delta1 : rr[jj].delta0;
+                    if (ok && cok)
+                        src = a.res.pool + (d + lo);
+                } else {
+                    const int64_t off = residual_offset(a.res, lo);
+                    if (ok && off >= 0)
+                        src = a.res.pool + off;
+                }
+                dma16(src, st + C::W_BYTES + j * 1024);
+            }
+        }
+#pragma unroll
+        for (int jj = 0; jj < C::X_INSTR; ++jj) {
+            const int j = wave * C::X_INSTR + jj;
+            const int64_t kk = kt + xel[jj];
+            const bool ok = live && kk < ke;
+            dma16(ok ? (const void *)(xsrc[jj] + kk * XELEM) : (const void *)g_zero16,
+                  st + C::W_BYTES * C::PLANES + j * 1024);
+        }
+    };
+
+    const int wn = wave % WN;
+    const int wm = wave / WN;
+    f32x4 acc[C::NT][C::MT];
+#pragma unroll
+    for (int i = 0; i < C::NT; ++i)
+#pragma unroll
+        for (int j = 0; j < C::MT; ++j)
+            acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+#pragma unroll
+    for (int t = 0; t < NSTAGE - 1; ++t)
+        issue(t);
+    for (int64_t t = 0; t < ntk; ++t) {
+        DPS_WAIT_VMCNT(C::NI * (NSTAGE - 2));
+        __syncthreads();
+        issue(t + NSTAGE - 1);
+        const uint8_t *st = smem + (int)(t % NSTAGE) * C::STAGE;
+        const uint8_t *xs = st + C::W_BYTES * C::PLANES;
+        if (C::FP8) {
+            i32x8 av[C::NT];
+#pragma unroll
+            for (int nt = 0; nt < C::NT; ++nt) {
+                const int r = wn * C::TN + nt * 16 + li;
+                const uint8_t *row = st + r * C::WROW;
+                const int sw = g3_swz<C::WROW>(r);
+                const u32x4 p = *reinterpret_cast<const u32x4 *>(row + (((2 * lg) ^ sw) << 4));
+                const u32x4 q = *reinterpret_cast<const u32x4 *>(row + (((2 * lg + 1) ^ sw) << 4));
+                av[nt] = i32x8{(int)p.x, (int)p.y, (int)p.z, (int)p.w,
+                               (int)q.x, (int)q.y, (int)q.z, (int)q.w};
+            }
+#pragma unroll
+            for (int mt = 0; mt < C::MT; ++mt) {
+                const int r = wm * C::TM + mt * 16 + li;
+                const uint8_t *row = xs + r * C::XROW;
+                const int sw = g3_swz<C::XROW>(r);
+                const u32x4 p = *reinterpret_cast<const u32x4 *>(row + (((2 * lg) ^ sw) << 4));
+                const u32x4 q = *reinterpret_cast<const u32x4 *>(row + (((2 * lg + 1) ^ sw) << 4));
+                const i32x8 bv = {(int)p.x, (int)p.y, (int)p.z, (int)p.w,
+                                  (int)q.x, (int)q.y, (int)q.z, (int)q.w};
+#pragma unroll
+                for (int nt = 0; nt < C::NT; ++nt)
+                    acc[nt][mt] = mfma16x16x128_bf8_fp8(av[nt], bv, acc[nt][mt]);
+            }
+        } else {
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                half8 av[C::NT];
+#pragma unroll
+                for (int nt = 0; nt < C::NT; ++nt) {
+                    const int r = wn * C::TN + nt * 16 + li;
+                    const int off = r * C::WROW +
+                                    (((2 * h + (lg >> 1)) ^ g3_swz<C::WROW>(r)) << 4) + ((lg & 1) << 3);
+                    const u32x2 hv = *reinterpret_cast<const u32x2 *>(st + off);
+                    u32x2 lv = {0u, 0u};
+                    if (KIND == G3_FULL)
+                        lv = *reinterpret_cast<const u32x2 *>(st + C::W_BYTES + off);
+                    av[nt] = merge8(hv.x, hv.y, lv.x, lv.y);
+                }
+#pragma unroll
+                for (int mt = 0; mt < C::MT; ++mt) {
+                    const int r = wm * C::TM + mt * 16 + li;
+                    const half8 bv = as_half8(*reinterpret_cast<const u32x4 *>(
+                        xs + r * C::XROW + (((4 * h + lg) ^ g3_swz<C::XROW>(r)) << 4)));
+#pragma unroll
+                    for (int nt = 0; nt < C::NT; ++nt)
+                        acc[nt][mt] = mfma16x16x32(av[nt], bv, acc[nt][mt]);
+                }
+            }
+        }
+    }
+    DPS_WAIT_VMCNT(0);  // no DMA may still target this block's LDS when it exits
+
+#pragma unroll
+    for (int mt = 0; mt < C::MT; ++mt) {
+        const int64_t m = mrow0 + wm * C::TM + mt * 16 + li;
+        float sc = 1.f;
+        if (C::FP8)
+            sc = m < mrow1 ? a.scale[m] : 0.f;
+#pragma unroll
+        for (int nt = 0; nt < C::NT; ++nt)
+            store_tile_out(a, s, m, n0 + wn * C::TN + nt * 16 + lg * 4,
+                           C::FP8 ? acc[nt][mt] * sc : acc[nt][mt], mrow1);
+    }
+}
+
+// ------------------------------------------------------------------------------
 // FP8 matrix cores: E5M2 weights x E4M3 activations
 // ------------------------------------------------------------------------------
 constexpr int BK8 = 128;        // K elements (= bytes) per tile
@@ -553,8 +803,58 @@ void launch_dma(const GemmArgs &a, const LinearPlan &plan, dim3 grid, hipStream_
 
 }  // namespace
 
-int gemm_rows_per_block() { return BN; }
-int gemm_tokens_per_block(int variant) { return variant == GEMM_DMA_256 ? 256 : BM; }
+int gemm_rows_per_block(int variant)
+{
+    return (variant == GEMM_G3_256x256 || variant == GEMM_G3_256x128 ||
+            variant == GEMM_G3_256x256_W16)
+               ? 256
+               : BN;
+}
+int gemm_tokens_per_block(int variant)
+{
+    return (variant == GEMM_DMA_256 || variant == GEMM_G3_256x256 || variant == GEMM_G3_128x256 ||
+            variant == GEMM_G3_256x256_W16)
+               ? 256
+               : BM;
+}
+
+namespace {
+
+template <int KIND, int BN_, int BM_, int WN, int WM, int NS>
+hipError_t launch_g3(const GemmArgs &a, const LinearPlan &plan, bool grouped, hipStream_t stream)
+{
+    const int64_t nt = (a.n + BN_ - 1) / BN_;
+    dim3 grid((unsigned)(nt * plan.splits),
+              (unsigned)token_tiles(a.rows, a.experts, grouped, BM_), 1);
+    if (!grouped) {
+        const int64_t total = nt * plan.splits * ((a.rows + BM_ - 1) / BM_);
+        grid = dim3((unsigned)((total + 7) / 8 * 8), 1, 1);
+    }
+    if (KIND == G3_FULL && plan.range_addr)
+        hipLaunchKernelGGL((gemm3_kernel<KIND, BN_, BM_, WN, WM, NS, true>), grid,
+                           dim3(WN * WM * 64), 0, stream, a);
+    else
+        hipLaunchKernelGGL((gemm3_kernel<KIND, BN_, BM_, WN, WM, NS, false>), grid,
+                           dim3(WN * WM * 64), 0, stream, a);
+    return hipGetLastError();
+}
+
+template <int KIND>
+hipError_t launch_g3_variant(const GemmArgs &a, const LinearPlan &plan, bool grouped,
+                             hipStream_t stream)
+{
+    constexpr bool TWO = KIND == G3_FULL;  // two byte planes: shallower rings
+    switch (plan.variant) {
+    case GEMM_G3_256x256: return launch_g3<KIND, 256, 256, 2, 4, TWO ? 2 : (KIND == G3_FP8 ? 2 : 3)>(a, plan, grouped, stream);
+    case GEMM_G3_128x256: return launch_g3<KIND, 128, 256, 2, 4, 3>(a, plan, grouped, stream);
+    case GEMM_G3_256x128: return launch_g3<KIND, 256, 128, 4, 2, 3>(a, plan, grouped, stream);
+    case GEMM_G3_128x128: return launch_g3<KIND, 128, 128, 2, 4, 3>(a, plan, grouped, stream);
+    case GEMM_G3_256x256_W16: return launch_g3<KIND, 256, 256, 4, 4, TWO ? 2 : (KIND == G3_FP8 ? 2 : 3)>(a, plan, grouped, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
 
 hipError_t launch_gemm_f16(const LinearProblem &p, const LinearPlan &plan, float *partial,
                            hipStream_t stream)
@@ -574,6 +874,9 @@ hipError_t launch_gemm_f16(const LinearProblem &p, const LinearPlan &plan, float
     a.partial = partial;
     a.scale = nullptr;
     const int64_t nt = (p.n + BN - 1) / BN;
+    if (plan.variant >= GEMM_G3_256x256)
+        return p.mode == MODE_FULL ? launch_g3_variant<G3_FULL>(a, plan, p.offsets != nullptr, stream)
+                                   : launch_g3_variant<G3_FAST>(a, plan, p.offsets != nullptr, stream);
     if (plan.variant == GEMM_DMA_128 || plan.variant == GEMM_DMA_256) {
         const int bm = plan.variant == GEMM_DMA_256 ? 256 : 128;
         dim3 grid((unsigned)(nt * plan.splits),
@@ -622,6 +925,8 @@ hipError_t launch_gemm_fp8(const uint8_t *xq, const float *scale, int64_t m, int
     a.y = y;
     a.partial = partial;
     a.scale = scale;
+    if (plan.variant >= GEMM_G3_256x256)
+        return launch_g3_variant<G3_FP8>(a, plan, false, stream);
     const int64_t nt = (n + BN - 1) / BN;
     dim3 grid((unsigned)(nt * plan.splits), (unsigned)token_tiles(m, 1, false), 1);
     hipLaunchKernelGGL(gemm_fp8_kernel, grid, dim3(256), 0, stream, a);

@@ -38,7 +38,17 @@ struct LinearProblem {
 enum KernelKind { KIND_SKINNY = 0, KIND_GEMM_F16 = 1, KIND_GEMM_FP8 = 2 };
 // FP16 GEMM variants: register-staged 128-token tiles, or the LDS-DMA pipeline
 // with 128- or 256-token tiles (128 weight rows each).
-enum GemmVariant { GEMM_REG_128 = 0, GEMM_DMA_128 = 1, GEMM_DMA_256 = 2 };
+enum GemmVariant {
+    GEMM_REG_128 = 0,
+    GEMM_DMA_128 = 1,
+    GEMM_DMA_256 = 2,
+    // eight-wave LDS-DMA kernels: weight rows x tokens per block
+    GEMM_G3_256x256 = 3,
+    GEMM_G3_128x256 = 4,
+    GEMM_G3_256x128 = 5,
+    GEMM_G3_128x128 = 6,
+    GEMM_G3_256x256_W16 = 7  // 256 x 256 with sixteen waves (four per SIMD)
+};
 // Decode-kernel variants 0..3 keep the weight stream in registers (tile
 // shapes differ); SKINNY_RING streams it through per-wave LDS rings.
 enum { SKINNY_RING = 4, SKINNY_RING_HALF = 5 };
