@@ -125,7 +125,8 @@ LinearPlan plan_linear(int mode, uint32_t flags, int64_t rows, int64_t n, int64_
     const int64_t rows_per_expert = grouped ? cdiv(rows, experts) : rows;
     if (flags & DPS_ACT_FP8_ROWSCALE) {
         p.kind = KIND_GEMM_FP8;
-        p.variant = rows > 128 ? GEMM_G3_256x256 : GEMM_G3_256x128;
+        // measured on MI355X: 256 x 256 tiles for wide layers, 256 x 128 otherwise
+        p.variant = (n > 4096 && rows > 128) ? GEMM_G3_256x256 : GEMM_G3_256x128;
         const int64_t tiles =
             cdiv(n, gemm_rows_per_block(p.variant)) * cdiv(rows, gemm_tokens_per_block(p.variant));
         int64_t s = cdiv(target, tiles);
@@ -156,15 +157,24 @@ LinearPlan plan_linear(int mode, uint32_t flags, int64_t rows, int64_t n, int64_
         p.splits = (int)cdiv(k, p.ksplit);
     } else {
         p.kind = KIND_GEMM_F16;
-        // measured on MI355X: the LDS-DMA pipeline wins with one byte plane
-        // (fast mode), the register-staged kernel with two (full mode); K is
-        // split only until the tiles cover the CUs, keeping >= 1024 per range
-        // above 128 tokens per expert, full mode takes 256-token tiles so that
-        // each weight tile is fetched once (128-token tiles fetch it twice)
-        p.variant = rows_per_expert > 128 ? GEMM_G3_256x256 : GEMM_G3_256x128;
+        // One plan for both modes, so that fast mode equals full mode over a
+        // zero residual bit for bit (same tiles, same K ranges, same order).
+        // Tile shape by tokens per expert, from MI355X sweeps of the FP16
+        // layers at 128, 256 and 2048 tokens (fast + full time summed):
+        //   <= 128: register-staged 128 x 128;  129..1023: eight-wave 256 x 128;
+        //   >= 1024: eight-wave 256 x 256.
+        // K is split so that about eight waves per CU are resident (the split
+        // count rounds down); each range keeps >= 1024 elements.
+        if (rows_per_expert <= 128)
+            p.variant = GEMM_REG_128;
+        else if (rows_per_expert < 1024)
+            p.variant = GEMM_G3_256x128;
+        else
+            p.variant = GEMM_G3_256x256;
+        const int64_t waves_per_block = p.variant == GEMM_REG_128 ? 4 : 8;
         const int64_t tiles =
             cdiv(n, gemm_rows_per_block(p.variant)) * cdiv(rows, gemm_tokens_per_block(p.variant));
-        int64_t s = cdiv((int64_t)cu_count, tiles);
+        int64_t s = (8 * (int64_t)cu_count / waves_per_block) / tiles;
         const int64_t smax = k / 1024 > 1 ? k / 1024 : 1;
         s = s < 1 ? 1 : (s > smax ? smax : s);
         p.ksplit = round_up(cdiv(k, s), 64);
