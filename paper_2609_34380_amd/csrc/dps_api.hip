@@ -165,19 +165,14 @@ LinearPlan plan_linear(int mode, uint32_t flags, int64_t rows, int64_t n, int64_
         //   >= 1024: eight-wave 256 x 256.
         // K is split so that about eight waves per CU are resident (the split
         // count rounds down); each range keeps >= 1024 elements.
-        if (rows_per_expert <= 128)
-            p.variant = GEMM_REG_128;
-        else if (rows_per_expert < 1024)
-            p.variant = GEMM_G3_256x128;
-        else
-            p.variant = GEMM_G3_256x256;
-        const int64_t waves_per_block = p.variant == GEMM_REG_128 ? 4 : 8;
+        p.variant = GEMM_G4_128x128;
+        const int64_t waves_per_block = 8;
         const int64_t tiles =
             cdiv(n, gemm_rows_per_block(p.variant)) * cdiv(rows, gemm_tokens_per_block(p.variant));
         int64_t s = (8 * (int64_t)cu_count / waves_per_block) / tiles;
         const int64_t smax = k / 1024 > 1 ? k / 1024 : 1;
         s = s < 1 ? 1 : (s > smax ? smax : s);
-        p.ksplit = round_up(cdiv(k, s), 64);
+        p.ksplit = round_up(cdiv(k, s), 128);
         p.splits = (int)cdiv(k, p.ksplit);
     }
     p.range_addr = mode == MODE_FULL && p.ksplit <= (int64_t(1) << log2c);

@@ -433,15 +433,24 @@ __global__ __launch_bounds__(256) void gemm_f16_dma_kernel(GemmArgs a)
 // Eight-wave LDS-DMA GEMM (two waves per SIMD), FP16 full/fast and FP8 fast
 // ------------------------------------------------------------------------------
 // Block tile BN weight rows x BM tokens, waves in a WN x WM grid, each wave
-// (BN/WN) x (BM/WM).  A stage covers BK K elements: 64 for FP16 (processed as
-// two 32-wide MFMA steps), 128 for FP8 (one 16x16x128 step).  Stages stream
-// global -> LDS by direct-to-LDS loads through a ring of NSTAGE slots, one
-// barrier per stage.  LDS rows hold 16-byte chunks at slot chunk ^ swz(row),
-// swz(row) = (row / rows-per-256-bytes) % chunks-per-row, so the 16 rows a
-// fragment read touches land in 16 distinct 16-byte bank groups.
-//   FP16 step h, lane (i, g): A = weight row i, K 32h+8g .. +7 (8 bytes per
-//   plane, merged into FP16 in registers); B = token row i, same K.
-//   FP8, lane (i, g): A and B = bytes 32g .. 32g+31 of the stage.
+// (BN/WN) x (BM/WM).  A stage covers BK K elements: 64 for FP16 (two 32-wide
+// MFMA steps), 128 for FP8 (one 16x16x128 step).  Stages stream global -> LDS
+// by direct-to-LDS loads through a ring of NSTAGE slots, one barrier per stage.
+//
+// LDS holds operands in fragment order: every 1 KiB block is the set of
+// 16-byte pieces that lanes 0..63 of a fragment read take, lane l at byte 16l.
+// Each fragment read is then one linear ds_read_b128 (measured conflict-free
+// on gfx950; row-major tiles read with 8-byte or strided 16-byte pieces ran at
+// half speed or less), and each DMA instruction fills one block, the per-lane
+// global address doing the gather.  Lane (i, g) = (lane % 16, lane / 16):
+//   FP16 weight plane, block q: row 16q+i, K 16g .. 16g+15 (one piece per
+//     plane feeds both MFMA steps: step h takes bytes 8h .. 8h+7, merged
+//     into FP16 in registers);
+//   FP16 tokens, block 2p+h: token 16p+i, K 16g+8h .. 16g+8h+7;
+//   FP8 weights and tokens, block 2q+c: row 16q+i, K 64c+16g .. +15 (the two
+//     pieces of a lane form its 32-byte MFMA operand).
+// A and B pair the same K elements in every lane, so each MFMA sums over
+// exactly the stage's K range.
 enum { G3_FULL = 0, G3_FAST = 1, G3_FP8 = 2 };
 
 template <int KIND, int BN_, int BM_, int WN, int WM, int NSTAGE>
@@ -464,13 +473,6 @@ struct G3 {
     static_assert(W_BYTES % (1024 * NWAVES) == 0 && X_BYTES % (1024 * NWAVES) == 0, "tiling");
     static_assert(LDS <= 160 * 1024, "LDS");
 };
-
-// slot swizzle for rows of `rowbytes` bytes (64 or 128)
-template <int ROWBYTES>
-__device__ __forceinline__ int g3_swz(int r)
-{
-    return (r / (256 / ROWBYTES)) % (ROWBYTES / 16);
-}
 
 template <int KIND, int BN_, int BM_, int WN, int WM, int NSTAGE, bool RANGE>
 __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
@@ -518,23 +520,21 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
     const int64_t ntk = ke > kb0 ? (ke - kb0 + C::BK - 1) / C::BK : 0;
 
     // ---- per-lane DMA descriptors (fixed across stages) ---------------------------
-    // weight instruction j: LDS bytes j*1024 .. +1023 of the plane tile
+    // weight instruction j fills block j of the plane tile (see the layout above)
     const uint8_t *wsrc[C::W_INSTR];
     int64_t wl[C::W_INSTR];
-    int wel[C::W_INSTR];  // element offset of this lane's chunk within the stage
+    int wel[C::W_INSTR];  // K offset of this lane's piece within the stage
     RangeResidual rr[C::W_INSTR];
 #pragma unroll
     for (int jj = 0; jj < C::W_INSTR; ++jj) {
         const int j = wave * C::W_INSTR + jj;
-        const int pos = j * 1024 + lane * 16;
-        const int r = pos / C::WROW;
-        const int slot = (pos % C::WROW) / 16;
-        const int chunk = slot ^ g3_swz<C::WROW>(r);
+        constexpr int BPG = C::WROW / 64;  // blocks per 16-row group
+        const int r = (j / BPG) * 16 + li;
         int64_t nr = n0 + r;
         nr = nr < a.n ? nr : a.n - 1;
         wl[jj] = (e * a.n + nr) * a.k;
         wsrc[jj] = a.hi + wl[jj];
-        wel[jj] = chunk * 16;
+        wel[jj] = (j % BPG) * 64 + lg * 16;
         rr[jj].ok0 = rr[jj].ok1 = false;
         rr[jj].delta0 = rr[jj].delta1 = 0;
         rr[jj].bnd = 0;
@@ -546,15 +546,12 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
     constexpr int XELEM = C::FP8 ? 1 : 2;  // bytes per X element
 #pragma unroll
     for (int jj = 0; jj < C::X_INSTR; ++jj) {
-        const int j = wave * C::X_INSTR + jj;
-        const int pos = j * 1024 + lane * 16;
-        const int r = pos / C::XROW;
-        const int slot = (pos % C::XROW) / 16;
-        const int chunk = slot ^ g3_swz<C::XROW>(r);
+        const int j = wave * C::X_INSTR + jj;  // block 2p + h (FP16) or 2p + c (FP8)
+        const int r = (j / 2) * 16 + li;
         int64_t m = mrow0 + r;
         m = m < mrow1 ? m : mrow1 - 1;
         xsrc[jj] = static_cast<const uint8_t *>(a.x) + m * a.k * XELEM;
-        xel[jj] = chunk * (16 / XELEM);
+        xel[jj] = C::FP8 ? (j % 2) * 64 + lg * 16 : lg * 16 + (j % 2) * 8;
     }
 
     auto issue = [&](int64_t t) {
@@ -612,25 +609,22 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
         issue(t + NSTAGE - 1);
         const uint8_t *st = smem + (int)(t % NSTAGE) * C::STAGE;
         const uint8_t *xs = st + C::W_BYTES * C::PLANES;
+        const int lo16 = lane * 16;
         if (C::FP8) {
             i32x8 av[C::NT];
 #pragma unroll
             for (int nt = 0; nt < C::NT; ++nt) {
-                const int r = wn * C::TN + nt * 16 + li;
-                const uint8_t *row = st + r * C::WROW;
-                const int sw = g3_swz<C::WROW>(r);
-                const u32x4 p = *reinterpret_cast<const u32x4 *>(row + (((2 * lg) ^ sw) << 4));
-                const u32x4 q = *reinterpret_cast<const u32x4 *>(row + (((2 * lg + 1) ^ sw) << 4));
+                const uint8_t *blk = st + (wn * C::NT + nt) * 2048 + lo16;
+                const u32x4 p = *reinterpret_cast<const u32x4 *>(blk);
+                const u32x4 q = *reinterpret_cast<const u32x4 *>(blk + 1024);
                 av[nt] = i32x8{(int)p.x, (int)p.y, (int)p.z, (int)p.w,
                                (int)q.x, (int)q.y, (int)q.z, (int)q.w};
             }
 #pragma unroll
             for (int mt = 0; mt < C::MT; ++mt) {
-                const int r = wm * C::TM + mt * 16 + li;
-                const uint8_t *row = xs + r * C::XROW;
-                const int sw = g3_swz<C::XROW>(r);
-                const u32x4 p = *reinterpret_cast<const u32x4 *>(row + (((2 * lg) ^ sw) << 4));
-                const u32x4 q = *reinterpret_cast<const u32x4 *>(row + (((2 * lg + 1) ^ sw) << 4));
+                const uint8_t *blk = xs + (wm * C::MT + mt) * 2048 + lo16;
+                const u32x4 p = *reinterpret_cast<const u32x4 *>(blk);
+                const u32x4 q = *reinterpret_cast<const u32x4 *>(blk + 1024);
                 const i32x8 bv = {(int)p.x, (int)p.y, (int)p.z, (int)p.w,
                                   (int)q.x, (int)q.y, (int)q.z, (int)q.w};
 #pragma unroll
@@ -638,28 +632,26 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
                     acc[nt][mt] = mfma16x16x128_bf8_fp8(av[nt], bv, acc[nt][mt]);
             }
         } else {
+            half8 a0[C::NT], a1[C::NT];
+#pragma unroll
+            for (int nt = 0; nt < C::NT; ++nt) {
+                const int off = (wn * C::NT + nt) * 1024 + lo16;
+                const u32x4 hv = *reinterpret_cast<const u32x4 *>(st + off);
+                u32x4 lv = {0u, 0u, 0u, 0u};
+                if (KIND == G3_FULL)
+                    lv = *reinterpret_cast<const u32x4 *>(st + C::W_BYTES + off);
+                a0[nt] = merge8(hv.x, hv.y, lv.x, lv.y);
+                a1[nt] = merge8(hv.z, hv.w, lv.z, lv.w);
+            }
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
-                half8 av[C::NT];
-#pragma unroll
-                for (int nt = 0; nt < C::NT; ++nt) {
-                    const int r = wn * C::TN + nt * 16 + li;
-                    const int off = r * C::WROW +
-                                    (((2 * h + (lg >> 1)) ^ g3_swz<C::WROW>(r)) << 4) + ((lg & 1) << 3);
-                    const u32x2 hv = *reinterpret_cast<const u32x2 *>(st + off);
-                    u32x2 lv = {0u, 0u};
-                    if (KIND == G3_FULL)
-                        lv = *reinterpret_cast<const u32x2 *>(st + C::W_BYTES + off);
-                    av[nt] = merge8(hv.x, hv.y, lv.x, lv.y);
-                }
 #pragma unroll
                 for (int mt = 0; mt < C::MT; ++mt) {
-                    const int r = wm * C::TM + mt * 16 + li;
                     const half8 bv = as_half8(*reinterpret_cast<const u32x4 *>(
-                        xs + r * C::XROW + (((4 * h + lg) ^ g3_swz<C::XROW>(r)) << 4)));
+                        xs + (2 * (wm * C::MT + mt) + h) * 1024 + lo16));
 #pragma unroll
                     for (int nt = 0; nt < C::NT; ++nt)
-                        acc[nt][mt] = mfma16x16x32(av[nt], bv, acc[nt][mt]);
+                        acc[nt][mt] = mfma16x16x32(h ? a1[nt] : a0[nt], bv, acc[nt][mt]);
                 }
             }
         }
@@ -676,6 +668,262 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
         for (int nt = 0; nt < C::NT; ++nt)
             store_tile_out(a, s, m, n0 + wn * C::TN + nt * 16 + lg * 4,
                            C::FP8 ? acc[nt][mt] * sc : acc[nt][mt], mrow1);
+    }
+}
+
+// ------------------------------------------------------------------------------
+// Wide-row LDS-DMA GEMM, FP16 full/fast: 128 x 128 tiles, 128-element stages
+// ------------------------------------------------------------------------------
+// On gfx950 an LDS-DMA (or plain) load instruction runs at about half speed
+// when each row it touches gets 64 contiguous bytes instead of >= 128 (MI355X,
+// L2-resident data: 26 vs 50 B/clk per CU; from HBM 4.4 vs 5.2-7.2 TB/s), so
+// a stage here spans 128 K elements: weight planes arrive as 8 rows x 128 B
+// per instruction and tokens as 4 rows x 256 B.  LDS keeps the rows, 16-byte
+// chunks placed at slot chunk ^ swz(row), and fragment reads are single
+// ds_read_b128 in patterns measured conflict-free:
+//   weight plane, 128-byte rows, swz8(r) = (r >> 1) & 7: lane (i, g) of
+//     K-half q reads chunk 4q + g of row i, K 64q+16g .. +15, which feeds two
+//     MFMA steps s (bytes 8s .. 8s+7, merged into FP16 in registers);
+//   tokens, 256-byte rows, swz16(r) = r & 15: step (q, s) of lane (i, g)
+//     reads chunk 8q + 2g + s of token i, K 64q+16g+8s .. +7.
+// Both operands of every MFMA pair the same K elements.  Eight waves: waves
+// 0-3 take K-half 0 of every stage and waves 4-7 K-half 1, each over a 64 x 64
+// quarter of the tile (two waves per SIMD); the halves are summed through LDS
+// at the end, in a fixed order.
+//
+// Weights and tokens stream through separate LDS rings: WS weight slots (the
+// weight stream comes from HBM and wants several stages in flight) and two
+// token slots (tokens are L2-resident).  Iteration t issues tokens of stage
+// t+1, then weights of stage t+WS-1; since the vector-memory counter retires
+// in issue order, waiting until only the last weight group is outstanding
+// retires exactly tokens t and weights t, and the later weight stages stay in
+// flight across the barrier.
+template <int MODE, int WS>
+struct G4 {
+    static constexpr int PLANES = MODE == MODE_FULL ? 2 : 1;
+    static constexpr int BK = 128;
+    static constexpr int W_BYTES = 128 * BK;        // one plane, 128 rows
+    static constexpr int W_SLOT = W_BYTES * PLANES;
+    static constexpr int X_SLOT = 128 * BK * 2;     // 128 tokens, FP16
+    static constexpr int X_BASE = W_SLOT * WS;
+    static constexpr int LDS = X_BASE + 2 * X_SLOT;
+    static constexpr int W_INSTR = W_BYTES / 1024 / 8;  // per wave per plane
+    static constexpr int X_INSTR = X_SLOT / 1024 / 8;
+    static constexpr int NW = W_INSTR * PLANES;         // weight instructions per wave per stage
+    static_assert(WS >= 3, "the counter scheme needs three weight slots");
+    static_assert(LDS <= 160 * 1024 && LDS >= 4 * 16384, "LDS (the K-half reduction needs 64 KiB)");
+};
+
+__device__ __forceinline__ int swz8(int r) { return (r >> 1) & 7; }
+__device__ __forceinline__ int swz16(int r) { return r & 15; }
+
+template <int MODE, int WS, bool RANGE>
+__global__ __launch_bounds__(512) void gemm4_kernel(GemmArgs a)
+{
+    using C = G4<MODE, WS>;
+    __shared__ __attribute__((aligned(16))) uint8_t smem[C::LDS];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int li = lane & 15;
+    const int lg = lane >> 4;
+    const int kh = wave >> 2;        // K-half of every stage
+    const int wn = (wave >> 1) & 1;  // 64-row quarter
+    const int wm = wave & 1;         // 64-token quarter
+
+    int64_t e, mrow0, mrow1;
+    int ntile, s;
+    if (a.offsets) {
+        if (!block_rows(a, e, mrow0, mrow1, 128))
+            return;
+        ntile = blockIdx.x / a.splits;
+        s = blockIdx.x % a.splits;
+    } else {
+        // 1-D grid remapped for the 8 XCDs (block L runs on XCD L % 8): XCD x
+        // takes the tile range [x * per_xcd, (x+1) * per_xcd).  Tiles are
+        // walked in groups of four weight tiles: token tile, then weight tile
+        // within the group, so the ~32 blocks resident on an XCD cover about
+        // 4 weight tiles x 8 token tiles and both operands are re-read from
+        // that XCD's L2 rather than from HBM.
+        const int64_t mtiles = (a.rows + 127) / 128;
+        const int64_t ntiles = (a.n + 127) / 128;
+        const int64_t total = mtiles * ntiles * a.splits;
+        const int64_t per_xcd = (total + 7) / 8;
+        const int64_t lin = blockIdx.x;
+        const int64_t t = (lin % 8) * per_xcd + lin / 8;
+        if (t >= total)
+            return;
+        constexpr int64_t G = 4;
+        s = (int)(t / (mtiles * ntiles));
+        const int64_t r = t % (mtiles * ntiles);
+        const int64_t chunk = r / (G * mtiles);
+        const int64_t within = r % (G * mtiles);
+        const int64_t gc = ntiles - chunk * G < G ? ntiles - chunk * G : G;
+        const int64_t mt = within / gc;
+        ntile = (int)(chunk * G + within % gc);
+        e = 0;
+        mrow0 = mt * 128;
+        mrow1 = mrow0 + 128 < a.rows ? mrow0 + 128 : a.rows;
+    }
+    const int64_t n0 = (int64_t)ntile * 128;
+    const int64_t kb0 = (int64_t)s * a.ksplit;
+    const int64_t ke = kb0 + a.ksplit < a.k ? kb0 + a.ksplit : a.k;
+    const int64_t ntk = ke > kb0 ? (ke - kb0 + C::BK - 1) / C::BK : 0;
+
+    // ---- per-lane DMA descriptors (fixed across stages) ---------------------------
+    // weight instruction j: rows 8j .. 8j+7, lane -> row 8j + lane/8, slot lane%8
+    const uint8_t *wsrc[C::W_INSTR];
+    int64_t wl[C::W_INSTR];
+    int wel[C::W_INSTR];  // K offset of this lane's chunk within the stage
+    RangeResidual rr[C::W_INSTR];
+#pragma unroll
+    for (int jj = 0; jj < C::W_INSTR; ++jj) {
+        const int j = wave * C::W_INSTR + jj;
+        const int r = 8 * j + (lane >> 3);
+        int64_t nr = n0 + r;
+        nr = nr < a.n ? nr : a.n - 1;
+        wl[jj] = (e * a.n + nr) * a.k;
+        wsrc[jj] = a.hi + wl[jj];
+        wel[jj] = ((lane & 7) ^ swz8(r)) * 16;
+        rr[jj].ok0 = rr[jj].ok1 = false;
+        rr[jj].delta0 = rr[jj].delta1 = 0;
+        rr[jj].bnd = 0;
+        if (MODE == MODE_FULL && RANGE && ke > kb0)
+            rr[jj] = range_residual(a.res, wl[jj] + kb0, wl[jj] + ke);
+    }
+    // token instruction j: rows 4j .. 4j+3, lane -> row 4j + lane/16, slot lane%16
+    const uint16_t *xsrc[C::X_INSTR];
+    int xel[C::X_INSTR];
+#pragma unroll
+    for (int jj = 0; jj < C::X_INSTR; ++jj) {
+        const int j = wave * C::X_INSTR + jj;
+        const int r = 4 * j + (lane >> 4);
+        int64_t m = mrow0 + r;
+        m = m < mrow1 ? m : mrow1 - 1;
+        xsrc[jj] = static_cast<const uint16_t *>(a.x) + m * a.k;
+        xel[jj] = ((lane & 15) ^ swz16(r)) * 8;
+    }
+
+    auto issue_w = [&](int64_t t) {
+        uint8_t *st = smem + (int)(t % WS) * C::W_SLOT;
+        const bool live = t < ntk;
+        const int64_t kt = kb0 + t * C::BK;
+#pragma unroll
+        for (int jj = 0; jj < C::W_INSTR; ++jj) {
+            const int j = wave * C::W_INSTR + jj;
+            const int64_t kk = kt + wel[jj];
+            const bool ok = live && kk < ke;
+            dma16(ok ? (const void *)(wsrc[jj] + kk) : (const void *)g_zero16, st + j * 1024);
+            if (MODE == MODE_FULL) {
+                const int64_t lo = wl[jj] + (ok ? kk : kb0);
+                const void *src = g_zero16;
+                if (RANGE) {
+                    const bool second = lo >= rr[jj].bnd;
+                    const bool cok = second ? rr[jj].ok1 : rr[jj].ok0;
+                    const int64_t d = second ? rr[jj].delta1 : rr[jj].delta0;
+                    if (ok && cok)
+                        src = a.res.pool + (d + lo);
+                } else {
+                    const int64_t off = residual_offset(a.res, lo);
+                    if (ok && off >= 0)
+                        src = a.res.pool + off;
+                }
+                dma16(src, st + C::W_BYTES + j * 1024);
+            }
+        }
+    };
+    auto issue_x = [&](int64_t t) {
+        uint8_t *st = smem + C::X_BASE + (int)(t & 1) * C::X_SLOT;
+        const bool live = t < ntk;
+        const int64_t kt = kb0 + t * C::BK;
+#pragma unroll
+        for (int jj = 0; jj < C::X_INSTR; ++jj) {
+            const int j = wave * C::X_INSTR + jj;
+            const int64_t kk = kt + xel[jj];
+            const bool ok = live && kk < ke;
+            dma16(ok ? (const void *)(xsrc[jj] + kk) : (const void *)g_zero16, st + j * 1024);
+        }
+    };
+
+    f32x4 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // fragment read offsets (fixed across stages)
+    int aoff[4], boff[4][2];
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) {
+        const int r = wn * 64 + nt * 16 + li;
+        aoff[nt] = r * 128 + (((4 * kh + lg) ^ swz8(r)) << 4);
+    }
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+        const int r = wm * 64 + mt * 16 + li;
+#pragma unroll
+        for (int sidx = 0; sidx < 2; ++sidx)
+            boff[mt][sidx] = r * 256 + (((8 * kh + 2 * lg + sidx) ^ swz16(r)) << 4);
+    }
+
+    // prologue in the steady-state order: weights 0 .. WS-3, tokens 0, weights WS-2
+#pragma unroll
+    for (int t = 0; t < WS - 2; ++t)
+        issue_w(t);
+    issue_x(0);
+    issue_w(WS - 2);
+    for (int64_t t = 0; t < ntk; ++t) {
+        DPS_WAIT_VMCNT(C::NW);  // all but the newest weight group: tokens t, weights t
+        __syncthreads();
+        issue_x(t + 1);
+        issue_w(t + WS - 1);
+        const uint8_t *st = smem + (int)(t % WS) * C::W_SLOT;
+        const uint8_t *xs = smem + C::X_BASE + (int)(t & 1) * C::X_SLOT;
+        half8 a0[4], a1[4];
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+            const u32x4 hv = *reinterpret_cast<const u32x4 *>(st + aoff[nt]);
+            u32x4 lv = {0u, 0u, 0u, 0u};
+            if (MODE == MODE_FULL)
+                lv = *reinterpret_cast<const u32x4 *>(st + C::W_BYTES + aoff[nt]);
+            a0[nt] = merge8(hv.x, hv.y, lv.x, lv.y);
+            a1[nt] = merge8(hv.z, hv.w, lv.z, lv.w);
+        }
+#pragma unroll
+        for (int sidx = 0; sidx < 2; ++sidx) {
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt) {
+                const half8 bv = as_half8(*reinterpret_cast<const u32x4 *>(xs + boff[mt][sidx]));
+#pragma unroll
+                for (int nt = 0; nt < 4; ++nt)
+                    acc[nt][mt] = mfma16x16x32(sidx ? a1[nt] : a0[nt], bv, acc[nt][mt]);
+            }
+        }
+    }
+    DPS_WAIT_VMCNT(0);  // no DMA may still target this block's LDS
+    __syncthreads();    // every wave is done reading the stages
+
+    // K-half 1 hands its partial sums to K-half 0 through LDS (16 KB per wave)
+    f32x4 *red = reinterpret_cast<f32x4 *>(smem) + (wave & 3) * (16 * 64);
+    if (kh == 1) {
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt)
+                red[(nt * 4 + mt) * 64 + lane] = acc[nt][mt];
+    }
+    __syncthreads();
+    if (kh == 1)
+        return;
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+        const int64_t m = mrow0 + wm * 64 + mt * 16 + li;
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt)
+            store_tile_out(a, s, m, n0 + wn * 64 + nt * 16 + lg * 4,
+                           acc[nt][mt] + red[(nt * 4 + mt) * 64 + lane], mrow1);
     }
 }
 
@@ -808,7 +1056,7 @@ int gemm_rows_per_block(int variant)
     return (variant == GEMM_G3_256x256 || variant == GEMM_G3_256x128 ||
             variant == GEMM_G3_256x256_W16)
                ? 256
-               : BN;
+               : BN;  // GEMM_G4_128x128 included
 }
 int gemm_tokens_per_block(int variant)
 {
@@ -836,6 +1084,23 @@ hipError_t launch_g3(const GemmArgs &a, const LinearPlan &plan, bool grouped, hi
     else
         hipLaunchKernelGGL((gemm3_kernel<KIND, BN_, BM_, WN, WM, NS, false>), grid,
                            dim3(WN * WM * 64), 0, stream, a);
+    return hipGetLastError();
+}
+
+template <int MODE, int WS>
+hipError_t launch_g4(const GemmArgs &a, const LinearPlan &plan, bool grouped, hipStream_t stream)
+{
+    const int64_t nt = (a.n + 127) / 128;
+    dim3 grid((unsigned)(nt * plan.splits), (unsigned)token_tiles(a.rows, a.experts, grouped, 128),
+              1);
+    if (!grouped) {
+        const int64_t total = nt * plan.splits * ((a.rows + 127) / 128);
+        grid = dim3((unsigned)((total + 7) / 8 * 8), 1, 1);
+    }
+    if (MODE == MODE_FULL && plan.range_addr)
+        hipLaunchKernelGGL((gemm4_kernel<MODE, WS, true>), grid, dim3(512), 0, stream, a);
+    else
+        hipLaunchKernelGGL((gemm4_kernel<MODE, WS, false>), grid, dim3(512), 0, stream, a);
     return hipGetLastError();
 }
 
@@ -874,6 +1139,9 @@ hipError_t launch_gemm_f16(const LinearProblem &p, const LinearPlan &plan, float
     a.partial = partial;
     a.scale = nullptr;
     const int64_t nt = (p.n + BN - 1) / BN;
+    if (plan.variant == GEMM_G4_128x128)
+        return p.mode == MODE_FULL ? launch_g4<MODE_FULL, 3>(a, plan, p.offsets != nullptr, stream)
+                                   : launch_g4<MODE_FAST, 6>(a, plan, p.offsets != nullptr, stream);
     if (plan.variant >= GEMM_G3_256x256)
         return p.mode == MODE_FULL ? launch_g3_variant<G3_FULL>(a, plan, p.offsets != nullptr, stream)
                                    : launch_g3_variant<G3_FAST>(a, plan, p.offsets != nullptr, stream);

@@ -47,7 +47,9 @@ enum GemmVariant {
     GEMM_G3_128x256 = 4,
     GEMM_G3_256x128 = 5,
     GEMM_G3_128x128 = 6,
-    GEMM_G3_256x256_W16 = 7  // 256 x 256 with sixteen waves (four per SIMD)
+    GEMM_G3_256x256_W16 = 7,  // 256 x 256 with sixteen waves (four per SIMD)
+    // 128 x 128, 128-element stages with wide-row loads, K split over waves
+    GEMM_G4_128x128 = 8
 };
 // Decode-kernel variants 0..3 keep the weight stream in registers (tile
 // shapes differ); SKINNY_RING streams it through per-wave LDS rings.
