@@ -135,7 +135,11 @@ LinearPlan plan_linear(int mode, uint32_t flags, int64_t rows, int64_t n, int64_
         p.ksplit = round_up(cdiv(k, s), 128);
         p.splits = (int)cdiv(k, p.ksplit);
         p.ws_quant = align256(rows * k) + align256(rows * 4);
-    } else if (rows_per_expert <= 64) {
+    } else if (rows_per_expert <= 16) {
+        // Up to 16 tokens per expert the decode kernel streams the weights
+        // (LDS rings of 256-byte rows); from 17 tokens on, the wide-row GEMM
+        // below is as fast or faster on MI355X (at 32 tokens, full mode, the
+        // 28672 x 4096 layer takes 59 us against 95 us).
         p.kind = KIND_SKINNY;
         // measured on MI355X: up to 8 tokens, the weight stream through shallow
         // per-wave LDS rings (two blocks per CU); above that, registers with
@@ -159,11 +163,10 @@ LinearPlan plan_linear(int mode, uint32_t flags, int64_t rows, int64_t n, int64_
         p.kind = KIND_GEMM_F16;
         // One plan for both modes, so that fast mode equals full mode over a
         // zero residual bit for bit (same tiles, same K ranges, same order).
-        // Tile shape by tokens per expert, from MI355X sweeps of the FP16
-        // layers at 128, 256 and 2048 tokens (fast + full time summed):
-        //   <= 128: register-staged 128 x 128;  129..1023: eight-wave 256 x 128;
-        //   >= 1024: eight-wave 256 x 256.
-        // K is split so that about eight waves per CU are resident (the split
+        // Every FP16 shape above 16 tokens per expert takes the wide-row
+        // 128 x 128 GEMM (on MI355X it beat the register-staged and eight-wave
+        // kernels at 128 and 256 tokens and matched them at 2048).  K is split
+        // so that about one block of eight waves per CU is resident (the split
         // count rounds down); each range keeps >= 1024 elements.
         p.variant = GEMM_G4_128x128;
         const int64_t waves_per_block = 8;

@@ -433,24 +433,15 @@ __global__ __launch_bounds__(256) void gemm_f16_dma_kernel(GemmArgs a)
 // Eight-wave LDS-DMA GEMM (two waves per SIMD), FP16 full/fast and FP8 fast
 // ------------------------------------------------------------------------------
 // Block tile BN weight rows x BM tokens, waves in a WN x WM grid, each wave
-// (BN/WN) x (BM/WM).  A stage covers BK K elements: 64 for FP16 (two 32-wide
-// MFMA steps), 128 for FP8 (one 16x16x128 step).  Stages stream global -> LDS
-// by direct-to-LDS loads through a ring of NSTAGE slots, one barrier per stage.
-//
-// LDS holds operands in fragment order: every 1 KiB block is the set of
-// 16-byte pieces that lanes 0..63 of a fragment read take, lane l at byte 16l.
-// Each fragment read is then one linear ds_read_b128 (measured conflict-free
-// on gfx950; row-major tiles read with 8-byte or strided 16-byte pieces ran at
-// half speed or less), and each DMA instruction fills one block, the per-lane
-// global address doing the gather.  Lane (i, g) = (lane % 16, lane / 16):
-//   FP16 weight plane, block q: row 16q+i, K 16g .. 16g+15 (one piece per
-//     plane feeds both MFMA steps: step h takes bytes 8h .. 8h+7, merged
-//     into FP16 in registers);
-//   FP16 tokens, block 2p+h: token 16p+i, K 16g+8h .. 16g+8h+7;
-//   FP8 weights and tokens, block 2q+c: row 16q+i, K 64c+16g .. +15 (the two
-//     pieces of a lane form its 32-byte MFMA operand).
-// A and B pair the same K elements in every lane, so each MFMA sums over
-// exactly the stage's K range.
+// (BN/WN) x (BM/WM).  A stage covers BK K elements: 64 for FP16 (processed as
+// two 32-wide MFMA steps), 128 for FP8 (one 16x16x128 step).  Stages stream
+// global -> LDS by direct-to-LDS loads through a ring of NSTAGE slots, one
+// barrier per stage.  LDS rows hold 16-byte chunks at slot chunk ^ swz(row),
+// swz(row) = (row / rows-per-256-bytes) % chunks-per-row, so the 16 rows a
+// fragment read touches land in 16 distinct 16-byte bank groups.
+//   FP16 step h, lane (i, g): A = weight row i, K 32h+8g .. +7 (8 bytes per
+//   plane, merged into FP16 in registers); B = token row i, same K.
+//   FP8, lane (i, g): A and B = bytes 32g .. 32g+31 of the stage.
 enum { G3_FULL = 0, G3_FAST = 1, G3_FP8 = 2 };
 
 template <int KIND, int BN_, int BM_, int WN, int WM, int NSTAGE>
@@ -473,6 +464,13 @@ struct G3 {
     static_assert(W_BYTES % (1024 * NWAVES) == 0 && X_BYTES % (1024 * NWAVES) == 0, "tiling");
     static_assert(LDS <= 160 * 1024, "LDS");
 };
+
+// slot swizzle for rows of `rowbytes` bytes (64 or 128)
+template <int ROWBYTES>
+__device__ __forceinline__ int g3_swz(int r)
+{
+    return (r / (256 / ROWBYTES)) % (ROWBYTES / 16);
+}
 
 template <int KIND, int BN_, int BM_, int WN, int WM, int NSTAGE, bool RANGE>
 __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
@@ -520,21 +518,23 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
     const int64_t ntk = ke > kb0 ? (ke - kb0 + C::BK - 1) / C::BK : 0;
 
     // ---- per-lane DMA descriptors (fixed across stages) ---------------------------
-    // weight instruction j fills block j of the plane tile (see the layout above)
+    // weight instruction j: LDS bytes j*1024 .. +1023 of the plane tile
     const uint8_t *wsrc[C::W_INSTR];
     int64_t wl[C::W_INSTR];
-    int wel[C::W_INSTR];  // K offset of this lane's piece within the stage
+    int wel[C::W_INSTR];  // element offset of this lane's chunk within the stage
     RangeResidual rr[C::W_INSTR];
 #pragma unroll
     for (int jj = 0; jj < C::W_INSTR; ++jj) {
         const int j = wave * C::W_INSTR + jj;
-        constexpr int BPG = C::WROW / 64;  // blocks per 16-row group
-        const int r = (j / BPG) * 16 + li;
+        const int pos = j * 1024 + lane * 16;
+        const int r = pos / C::WROW;
+        const int slot = (pos % C::WROW) / 16;
+        const int chunk = slot ^ g3_swz<C::WROW>(r);
         int64_t nr = n0 + r;
         nr = nr < a.n ? nr : a.n - 1;
         wl[jj] = (e * a.n + nr) * a.k;
         wsrc[jj] = a.hi + wl[jj];
-        wel[jj] = (j % BPG) * 64 + lg * 16;
+        wel[jj] = chunk * 16;
         rr[jj].ok0 = rr[jj].ok1 = false;
         rr[jj].delta0 = rr[jj].delta1 = 0;
         rr[jj].bnd = 0;
@@ -546,12 +546,15 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
     constexpr int XELEM = C::FP8 ? 1 : 2;  // bytes per X element
 #pragma unroll
     for (int jj = 0; jj < C::X_INSTR; ++jj) {
-        const int j = wave * C::X_INSTR + jj;  // block 2p + h (FP16) or 2p + c (FP8)
-        const int r = (j / 2) * 16 + li;
+        const int j = wave * C::X_INSTR + jj;
+        const int pos = j * 1024 + lane * 16;
+        const int r = pos / C::XROW;
+        const int slot = (pos % C::XROW) / 16;
+        const int chunk = slot ^ g3_swz<C::XROW>(r);
         int64_t m = mrow0 + r;
         m = m < mrow1 ? m : mrow1 - 1;
         xsrc[jj] = static_cast<const uint8_t *>(a.x) + m * a.k * XELEM;
-        xel[jj] = C::FP8 ? (j % 2) * 64 + lg * 16 : lg * 16 + (j % 2) * 8;
+        xel[jj] = chunk * (16 / XELEM);
     }
 
     auto issue = [&](int64_t t) {
@@ -609,22 +612,25 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
         issue(t + NSTAGE - 1);
         const uint8_t *st = smem + (int)(t % NSTAGE) * C::STAGE;
         const uint8_t *xs = st + C::W_BYTES * C::PLANES;
-        const int lo16 = lane * 16;
         if (C::FP8) {
             i32x8 av[C::NT];
 #pragma unroll
             for (int nt = 0; nt < C::NT; ++nt) {
-                const uint8_t *blk = st + (wn * C::NT + nt) * 2048 + lo16;
-                const u32x4 p = *reinterpret_cast<const u32x4 *>(blk);
-                const u32x4 q = *reinterpret_cast<const u32x4 *>(blk + 1024);
+                const int r = wn * C::TN + nt * 16 + li;
+                const uint8_t *row = st + r * C::WROW;
+                const int sw = g3_swz<C::WROW>(r);
+                const u32x4 p = *reinterpret_cast<const u32x4 *>(row + (((2 * lg) ^ sw) << 4));
+                const u32x4 q = *reinterpret_cast<const u32x4 *>(row + (((2 * lg + 1) ^ sw) << 4));
                 av[nt] = i32x8{(int)p.x, (int)p.y, (int)p.z, (int)p.w,
                                (int)q.x, (int)q.y, (int)q.z, (int)q.w};
             }
 #pragma unroll
             for (int mt = 0; mt < C::MT; ++mt) {
-                const uint8_t *blk = xs + (wm * C::MT + mt) * 2048 + lo16;
-                const u32x4 p = *reinterpret_cast<const u32x4 *>(blk);
-                const u32x4 q = *reinterpret_cast<const u32x4 *>(blk + 1024);
+                const int r = wm * C::TM + mt * 16 + li;
+                const uint8_t *row = xs + r * C::XROW;
+                const int sw = g3_swz<C::XROW>(r);
+                const u32x4 p = *reinterpret_cast<const u32x4 *>(row + (((2 * lg) ^ sw) << 4));
+                const u32x4 q = *reinterpret_cast<const u32x4 *>(row + (((2 * lg + 1) ^ sw) << 4));
                 const i32x8 bv = {(int)p.x, (int)p.y, (int)p.z, (int)p.w,
                                   (int)q.x, (int)q.y, (int)q.z, (int)q.w};
 #pragma unroll
@@ -632,26 +638,28 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
                     acc[nt][mt] = mfma16x16x128_bf8_fp8(av[nt], bv, acc[nt][mt]);
             }
         } else {
-            half8 a0[C::NT], a1[C::NT];
-#pragma unroll
-            for (int nt = 0; nt < C::NT; ++nt) {
-                const int off = (wn * C::NT + nt) * 1024 + lo16;
-                const u32x4 hv = *reinterpret_cast<const u32x4 *>(st + off);
-                u32x4 lv = {0u, 0u, 0u, 0u};
-                if (KIND == G3_FULL)
-                    lv = *reinterpret_cast<const u32x4 *>(st + C::W_BYTES + off);
-                a0[nt] = merge8(hv.x, hv.y, lv.x, lv.y);
-                a1[nt] = merge8(hv.z, hv.w, lv.z, lv.w);
-            }
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
+                half8 av[C::NT];
+#pragma unroll
+                for (int nt = 0; nt < C::NT; ++nt) {
+                    const int r = wn * C::TN + nt * 16 + li;
+                    const int off = r * C::WROW +
+                                    (((2 * h + (lg >> 1)) ^ g3_swz<C::WROW>(r)) << 4) + ((lg & 1) << 3);
+                    const u32x2 hv = *reinterpret_cast<const u32x2 *>(st + off);
+                    u32x2 lv = {0u, 0u};
+                    if (KIND == G3_FULL)
+                        lv = *reinterpret_cast<const u32x2 *>(st + C::W_BYTES + off);
+                    av[nt] = merge8(hv.x, hv.y, lv.x, lv.y);
+                }
 #pragma unroll
                 for (int mt = 0; mt < C::MT; ++mt) {
+                    const int r = wm * C::TM + mt * 16 + li;
                     const half8 bv = as_half8(*reinterpret_cast<const u32x4 *>(
-                        xs + (2 * (wm * C::MT + mt) + h) * 1024 + lo16));
+                        xs + r * C::XROW + (((4 * h + lg) ^ g3_swz<C::XROW>(r)) << 4)));
 #pragma unroll
                     for (int nt = 0; nt < C::NT; ++nt)
-                        acc[nt][mt] = mfma16x16x32(h ? a1[nt] : a0[nt], bv, acc[nt][mt]);
+                        acc[nt][mt] = mfma16x16x32(av[nt], bv, acc[nt][mt]);
                 }
             }
         }
