@@ -164,11 +164,13 @@ LinearPlan plan_linear(int mode, uint32_t flags, int64_t rows, int64_t n, int64_
         // One plan for both modes, so that fast mode equals full mode over a
         // zero residual bit for bit (same tiles, same K ranges, same order).
         // Every FP16 shape above 16 tokens per expert takes the wide-row
-        // 128 x 128 GEMM (on MI355X it beat the register-staged and eight-wave
-        // kernels at 128 and 256 tokens and matched them at 2048).  K is split
+        // GEMM (on MI355X it beat the register-staged and eight-wave kernels
+        // at 128 and 256 tokens and matched them at 2048), with a 32-, 64- or
+        // 128-token tile so that short calls stage no padding rows.  K is split
         // so that about one block of eight waves per CU is resident (the split
         // count rounds down); each range keeps >= 1024 elements.
-        p.variant = GEMM_G4_128x128;
+        p.variant = rows_per_expert <= 32 ? GEMM_G4_128x32
+                    : (rows_per_expert <= 64 ? GEMM_G4_128x64 : GEMM_G4_128x128);
         const int64_t waves_per_block = 8;
         const int64_t tiles =
             cdiv(n, gemm_rows_per_block(p.variant)) * cdiv(rows, gemm_tokens_per_block(p.variant));

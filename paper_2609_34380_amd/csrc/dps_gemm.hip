@@ -695,9 +695,10 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
 //   tokens, 256-byte rows, swz16(r) = r & 15: step (q, s) of lane (i, g)
 //     reads chunk 8q + 2g + s of token i, K 64q+16g+8s .. +7.
 // Both operands of every MFMA pair the same K elements.  Eight waves: waves
-// 0-3 take K-half 0 of every stage and waves 4-7 K-half 1, each over a 64 x 64
-// quarter of the tile (two waves per SIMD); the halves are summed through LDS
-// at the end, in a fixed order.
+// 0-3 take K-half 0 of every stage and waves 4-7 K-half 1, each over a
+// 64 x BM/2 quarter of the tile (two waves per SIMD); the halves are summed
+// through LDS at the end, in a fixed order.  The token tile BM (32, 64 or
+// 128) follows the call's token count, so short calls stage no padding rows.
 //
 // Weights and tokens stream through separate LDS rings: WS weight slots (the
 // weight stream comes from HBM and wants several stages in flight) and two
@@ -706,29 +707,31 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
 // in issue order, waiting until only the last weight group is outstanding
 // retires exactly tokens t and weights t, and the later weight stages stay in
 // flight across the barrier.
-template <int MODE, int WS>
+template <int MODE, int BM, int WS>
 struct G4 {
     static constexpr int PLANES = MODE == MODE_FULL ? 2 : 1;
     static constexpr int BK = 128;
+    static constexpr int MT = BM / 32;              // 16-token tiles per wave
     static constexpr int W_BYTES = 128 * BK;        // one plane, 128 rows
     static constexpr int W_SLOT = W_BYTES * PLANES;
-    static constexpr int X_SLOT = 128 * BK * 2;     // 128 tokens, FP16
+    static constexpr int X_SLOT = BM * BK * 2;      // BM tokens, FP16
     static constexpr int X_BASE = W_SLOT * WS;
     static constexpr int LDS = X_BASE + 2 * X_SLOT;
     static constexpr int W_INSTR = W_BYTES / 1024 / 8;  // per wave per plane
     static constexpr int X_INSTR = X_SLOT / 1024 / 8;
     static constexpr int NW = W_INSTR * PLANES;         // weight instructions per wave per stage
     static_assert(WS >= 3, "the counter scheme needs three weight slots");
+    static_assert(BM == 32 || BM == 64 || BM == 128, "token tile");
     static_assert(LDS <= 160 * 1024 && LDS >= 4 * 16384, "LDS (the K-half reduction needs 64 KiB)");
 };
 
 __device__ __forceinline__ int swz8(int r) { return (r >> 1) & 7; }
 __device__ __forceinline__ int swz16(int r) { return r & 15; }
 
-template <int MODE, int WS, bool RANGE>
+template <int MODE, int BM, int WS, bool RANGE>
 __global__ __launch_bounds__(512) void gemm4_kernel(GemmArgs a)
 {
-    using C = G4<MODE, WS>;
+    using C = G4<MODE, BM, WS>;
     __shared__ __attribute__((aligned(16))) uint8_t smem[C::LDS];
 
     const int tid = threadIdx.x;
@@ -738,12 +741,12 @@ __global__ __launch_bounds__(512) void gemm4_kernel(GemmArgs a)
     const int lg = lane >> 4;
     const int kh = wave >> 2;        // K-half of every stage
     const int wn = (wave >> 1) & 1;  // 64-row quarter
-    const int wm = wave & 1;         // 64-token quarter
+    const int wm = wave & 1;         // BM/2-token half
 
     int64_t e, mrow0, mrow1;
     int ntile, s;
     if (a.offsets) {
-        if (!block_rows(a, e, mrow0, mrow1, 128))
+        if (!block_rows(a, e, mrow0, mrow1, BM))
             return;
         ntile = blockIdx.x / a.splits;
         s = blockIdx.x % a.splits;
@@ -754,7 +757,7 @@ __global__ __launch_bounds__(512) void gemm4_kernel(GemmArgs a)
         // within the group, so the ~32 blocks resident on an XCD cover about
         // 4 weight tiles x 8 token tiles and both operands are re-read from
         // that XCD's L2 rather than from HBM.
-        const int64_t mtiles = (a.rows + 127) / 128;
+        const int64_t mtiles = (a.rows + BM - 1) / BM;
         const int64_t ntiles = (a.n + 127) / 128;
         const int64_t total = mtiles * ntiles * a.splits;
         const int64_t per_xcd = (total + 7) / 8;
@@ -771,8 +774,8 @@ __global__ __launch_bounds__(512) void gemm4_kernel(GemmArgs a)
         const int64_t mt = within / gc;
         ntile = (int)(chunk * G + within % gc);
         e = 0;
-        mrow0 = mt * 128;
-        mrow1 = mrow0 + 128 < a.rows ? mrow0 + 128 : a.rows;
+        mrow0 = mt * BM;
+        mrow1 = mrow0 + BM < a.rows ? mrow0 + BM : a.rows;
     }
     const int64_t n0 = (int64_t)ntile * 128;
     const int64_t kb0 = (int64_t)s * a.ksplit;
@@ -854,23 +857,23 @@ __global__ __launch_bounds__(512) void gemm4_kernel(GemmArgs a)
         }
     };
 
-    f32x4 acc[4][4];
+    f32x4 acc[4][C::MT];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < C::MT; ++j)
             acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     // fragment read offsets (fixed across stages)
-    int aoff[4], boff[4][2];
+    int aoff[4], boff[C::MT][2];
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt) {
         const int r = wn * 64 + nt * 16 + li;
         aoff[nt] = r * 128 + (((4 * kh + lg) ^ swz8(r)) << 4);
     }
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
-        const int r = wm * 64 + mt * 16 + li;
+    for (int mt = 0; mt < C::MT; ++mt) {
+        const int r = wm * (BM / 2) + mt * 16 + li;
 #pragma unroll
         for (int sidx = 0; sidx < 2; ++sidx)
             boff[mt][sidx] = r * 256 + (((8 * kh + 2 * lg + sidx) ^ swz16(r)) << 4);
@@ -902,7 +905,7 @@ __global__ __launch_bounds__(512) void gemm4_kernel(GemmArgs a)
 #pragma unroll
         for (int sidx = 0; sidx < 2; ++sidx) {
 #pragma unroll
-            for (int mt = 0; mt < 4; ++mt) {
+            for (int mt = 0; mt < C::MT; ++mt) {
                 const half8 bv = as_half8(*reinterpret_cast<const u32x4 *>(xs + boff[mt][sidx]));
 #pragma unroll
                 for (int nt = 0; nt < 4; ++nt)
@@ -913,25 +916,25 @@ __global__ __launch_bounds__(512) void gemm4_kernel(GemmArgs a)
     DPS_WAIT_VMCNT(0);  // no DMA may still target this block's LDS
     __syncthreads();    // every wave is done reading the stages
 
-    // K-half 1 hands its partial sums to K-half 0 through LDS (16 KB per wave)
-    f32x4 *red = reinterpret_cast<f32x4 *>(smem) + (wave & 3) * (16 * 64);
+    // K-half 1 hands its partial sums to K-half 0 through LDS (4 KB per tile)
+    f32x4 *red = reinterpret_cast<f32x4 *>(smem) + (wave & 3) * (4 * C::MT * 64);
     if (kh == 1) {
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
-            for (int mt = 0; mt < 4; ++mt)
-                red[(nt * 4 + mt) * 64 + lane] = acc[nt][mt];
+            for (int mt = 0; mt < C::MT; ++mt)
+                red[(nt * C::MT + mt) * 64 + lane] = acc[nt][mt];
     }
     __syncthreads();
     if (kh == 1)
         return;
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
-        const int64_t m = mrow0 + wm * 64 + mt * 16 + li;
+    for (int mt = 0; mt < C::MT; ++mt) {
+        const int64_t m = mrow0 + wm * (BM / 2) + mt * 16 + li;
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt)
             store_tile_out(a, s, m, n0 + wn * 64 + nt * 16 + lg * 4,
-                           acc[nt][mt] + red[(nt * 4 + mt) * 64 + lane], mrow1);
+                           acc[nt][mt] + red[(nt * C::MT + mt) * 64 + lane], mrow1);
     }
 }
 
@@ -1068,6 +1071,10 @@ int gemm_rows_per_block(int variant)
 }
 int gemm_tokens_per_block(int variant)
 {
+    if (variant == GEMM_G4_128x64)
+        return 64;
+    if (variant == GEMM_G4_128x32)
+        return 32;
     return (variant == GEMM_DMA_256 || variant == GEMM_G3_256x256 || variant == GEMM_G3_128x256 ||
             variant == GEMM_G3_256x256_W16)
                ? 256
@@ -1095,21 +1102,35 @@ hipError_t launch_g3(const GemmArgs &a, const LinearPlan &plan, bool grouped, hi
     return hipGetLastError();
 }
 
-template <int MODE, int WS>
+template <int MODE, int BM, int WS>
 hipError_t launch_g4(const GemmArgs &a, const LinearPlan &plan, bool grouped, hipStream_t stream)
 {
     const int64_t nt = (a.n + 127) / 128;
-    dim3 grid((unsigned)(nt * plan.splits), (unsigned)token_tiles(a.rows, a.experts, grouped, 128),
+    dim3 grid((unsigned)(nt * plan.splits), (unsigned)token_tiles(a.rows, a.experts, grouped, BM),
               1);
     if (!grouped) {
-        const int64_t total = nt * plan.splits * ((a.rows + 127) / 128);
+        const int64_t total = nt * plan.splits * ((a.rows + BM - 1) / BM);
         grid = dim3((unsigned)((total + 7) / 8 * 8), 1, 1);
     }
     if (MODE == MODE_FULL && plan.range_addr)
-        hipLaunchKernelGGL((gemm4_kernel<MODE, WS, true>), grid, dim3(512), 0, stream, a);
+        hipLaunchKernelGGL((gemm4_kernel<MODE, BM, WS, true>), grid, dim3(512), 0, stream, a);
     else
-        hipLaunchKernelGGL((gemm4_kernel<MODE, WS, false>), grid, dim3(512), 0, stream, a);
+        hipLaunchKernelGGL((gemm4_kernel<MODE, BM, WS, false>), grid, dim3(512), 0, stream, a);
     return hipGetLastError();
+}
+
+// weight-ring depth per (mode, token tile): the deepest ring that fits 160 KiB
+template <int MODE>
+hipError_t launch_g4_variant(const GemmArgs &a, const LinearPlan &plan, bool grouped,
+                             hipStream_t stream)
+{
+    constexpr bool FULL = MODE == MODE_FULL;
+    switch (plan.variant) {
+    case GEMM_G4_128x128: return launch_g4<MODE, 128, FULL ? 3 : 6>(a, plan, grouped, stream);
+    case GEMM_G4_128x64: return launch_g4<MODE, 64, FULL ? 4 : 8>(a, plan, grouped, stream);
+    case GEMM_G4_128x32: return launch_g4<MODE, 32, FULL ? 4 : 9>(a, plan, grouped, stream);
+    default: return hipErrorInvalidValue;
+    }
 }
 
 template <int KIND>
@@ -1147,9 +1168,9 @@ hipError_t launch_gemm_f16(const LinearProblem &p, const LinearPlan &plan, float
     a.partial = partial;
     a.scale = nullptr;
     const int64_t nt = (p.n + BN - 1) / BN;
-    if (plan.variant == GEMM_G4_128x128)
-        return p.mode == MODE_FULL ? launch_g4<MODE_FULL, 3>(a, plan, p.offsets != nullptr, stream)
-                                   : launch_g4<MODE_FAST, 6>(a, plan, p.offsets != nullptr, stream);
+    if (plan.variant >= GEMM_G4_128x128)
+        return p.mode == MODE_FULL ? launch_g4_variant<MODE_FULL>(a, plan, p.offsets != nullptr, stream)
+                                   : launch_g4_variant<MODE_FAST>(a, plan, p.offsets != nullptr, stream);
     if (plan.variant >= GEMM_G3_256x256)
         return p.mode == MODE_FULL ? launch_g3_variant<G3_FULL>(a, plan, p.offsets != nullptr, stream)
                                    : launch_g3_variant<G3_FAST>(a, plan, p.offsets != nullptr, stream);

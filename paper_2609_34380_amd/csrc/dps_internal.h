@@ -48,8 +48,11 @@ enum GemmVariant {
     GEMM_G3_256x128 = 5,
     GEMM_G3_128x128 = 6,
     GEMM_G3_256x256_W16 = 7,  // 256 x 256 with sixteen waves (four per SIMD)
-    // 128 x 128, 128-element stages with wide-row loads, K split over waves
-    GEMM_G4_128x128 = 8
+    // 128 weight rows x 128/64/32 tokens, 128-element stages with wide-row
+    // loads, K split over waves
+    GEMM_G4_128x128 = 8,
+    GEMM_G4_128x64 = 9,
+    GEMM_G4_128x32 = 10
 };
 // Decode-kernel variants 0..3 keep the weight stream in registers (tile
 // shapes differ); SKINNY_RING streams it through per-wave LDS rings.

@@ -135,6 +135,7 @@ LINEAR_CASES = [
     (3, 1000, 1040, 12, True),
     (16, 64, 2048, 8, True),        # chunks smaller than a K range: table lookups
     (17, 520, 4096, 21, True),
+    (32, 768, 2048, 14, True),      # one full 32-token tile
     (33, 200, 1152, 10, True),
     (64, 1024, 4096, 21, False),
     (65, 384, 1024, 12, True),
@@ -282,6 +283,8 @@ def test_linear_fp8_matches_oracle(m, n, k):
 @pytest.mark.parametrize("counts,n,k,log2c", [
     ((5, 0, 17, 64, 1, 3), 192, 512, 12),           # decode-sized groups, an empty expert
     ((100, 0, 300, 129, 7), 160, 1024, 10),          # token-tiled groups
+    ((40, 0, 70, 3, 33), 256, 1024, 12),             # 32-token tiles, several per expert
+    ((90, 20, 0, 100), 320, 768, 11),                # 64-token tiles
     ((128, 140, 120, 133, 110, 125, 131, 137), 256, 256, 21),
 ])
 @pytest.mark.parametrize("mode", [FAST, FULL], ids=["fast", "full"])
