@@ -266,6 +266,22 @@ __device__ __forceinline__ void dma16(const void *src, void *lds_wave_base)
 #define DPS_WAIT_VMCNT(n) \
     __builtin_amdgcn_s_waitcnt(((n) & 0xF) | ((((n) >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8))
 
+// Block barrier between pipeline stages.  __syncthreads() carries a
+// workgroup-scope fence, which the compiler satisfies by waiting for every
+// outstanding vector-memory operation (direct-to-LDS loads count as LDS
+// writes): the whole DMA ring would drain at every stage.  The loops instead
+// wait for exactly what they need -- their own DMA of the stage about to be
+// read (vmcnt, before this call) and their own LDS reads of the slot about to
+// be refilled (lgkmcnt(0), here) -- and then meet at a bare s_barrier.  The
+// empty asm statements keep the compiler from moving memory accesses across.
+__device__ __forceinline__ void stage_barrier()
+{
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt at their maxima
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
 template <int MODE, int BM>
 struct DmaCfg {
     static constexpr int X_BYTES = BM * DMA_BK * 2;
@@ -389,7 +405,7 @@ __global__ __launch_bounds__(256) void gemm_f16_dma_kernel(GemmArgs a)
         issue(t);
     for (int64_t t = 0; t < ntk; ++t) {
         DPS_WAIT_VMCNT(C::NI * (DMA_STAGES - 2));
-        __syncthreads();
+        stage_barrier();
         issue(t + DMA_STAGES - 1);
         const uint8_t *st = smem + (int)(t % DMA_STAGES) * C::STAGE;
         const uint8_t *xs = st + DMA_W_BYTES * C::PLANES;
@@ -608,7 +624,7 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
         issue(t);
     for (int64_t t = 0; t < ntk; ++t) {
         DPS_WAIT_VMCNT(C::NI * (NSTAGE - 2));
-        __syncthreads();
+        stage_barrier();
         issue(t + NSTAGE - 1);
         const uint8_t *st = smem + (int)(t % NSTAGE) * C::STAGE;
         const uint8_t *xs = st + C::W_BYTES * C::PLANES;
@@ -782,81 +798,101 @@ __global__ __launch_bounds__(512) void gemm4_kernel(GemmArgs a)
     const int64_t ke = kb0 + a.ksplit < a.k ? kb0 + a.ksplit : a.k;
     const int64_t ntk = ke > kb0 ? (ke - kb0 + C::BK - 1) / C::BK : 0;
 
-    // ---- per-lane DMA descriptors (fixed across stages) ---------------------------
+    // ---- per-lane DMA state (fixed across stages) ------------------------------
+    // Stage t of a lane's weight piece starts at wp + 128 t (upper bytes) and,
+    // in full mode, at rp0/rp1 + 128 t (residual bytes in the first / second
+    // chunk the row's K range touches; the second serves stages >= tsw).  A
+    // piece lies inside [kb0, ke) while 128 t < wlim.  Token pieces likewise:
+    // xp + 128 t elements, inside while 128 t < xlim.
     // weight instruction j: rows 8j .. 8j+7, lane -> row 8j + lane/8, slot lane%8
-    const uint8_t *wsrc[C::W_INSTR];
-    int64_t wl[C::W_INSTR];
-    int wel[C::W_INSTR];  // K offset of this lane's chunk within the stage
-    RangeResidual rr[C::W_INSTR];
+    const uint8_t *wp[C::W_INSTR];
+    const uint8_t *rp0[C::W_INSTR], *rp1[C::W_INSTR];
+    int64_t wlog[C::W_INSTR];  // logical residual index of the piece at stage 0
+    int wlim[C::W_INSTR], tsw[C::W_INSTR];
+    bool rok0[C::W_INSTR], rok1[C::W_INSTR];
 #pragma unroll
     for (int jj = 0; jj < C::W_INSTR; ++jj) {
         const int j = wave * C::W_INSTR + jj;
         const int r = 8 * j + (lane >> 3);
         int64_t nr = n0 + r;
         nr = nr < a.n ? nr : a.n - 1;
-        wl[jj] = (e * a.n + nr) * a.k;
-        wsrc[jj] = a.hi + wl[jj];
-        wel[jj] = ((lane & 7) ^ swz8(r)) * 16;
-        rr[jj].ok0 = rr[jj].ok1 = false;
-        rr[jj].delta0 = rr[jj].delta1 = 0;
-        rr[jj].bnd = 0;
-        if (MODE == MODE_FULL && RANGE && ke > kb0)
-            rr[jj] = range_residual(a.res, wl[jj] + kb0, wl[jj] + ke);
+        const int wel = ((lane & 7) ^ swz8(r)) * 16;
+        const int64_t wl = (e * a.n + nr) * a.k;
+        wp[jj] = a.hi + wl + kb0 + wel;
+        wlim[jj] = (int)(ke - kb0 - wel);
+        wlog[jj] = wl + kb0 + wel;
+        rp0[jj] = rp1[jj] = a.res.pool;
+        tsw[jj] = 0;
+        rok0[jj] = rok1[jj] = false;
+        if (MODE == MODE_FULL && RANGE && ke > kb0) {
+            const RangeResidual rr = range_residual(a.res, wl + kb0, wl + ke);
+            rp0[jj] = a.res.pool + rr.delta0 + wlog[jj];
+            rp1[jj] = a.res.pool + rr.delta1 + wlog[jj];
+            rok0[jj] = rr.ok0;
+            rok1[jj] = rr.ok1;
+            const int64_t d = rr.bnd - wlog[jj];  // first stage at or past the chunk boundary
+            tsw[jj] = d <= 0 ? 0 : (int)((d + C::BK - 1) / C::BK);
+        }
     }
     // token instruction j: rows 4j .. 4j+3, lane -> row 4j + lane/16, slot lane%16
-    const uint16_t *xsrc[C::X_INSTR];
-    int xel[C::X_INSTR];
+    const uint16_t *xp[C::X_INSTR];
+    int xlim[C::X_INSTR];
 #pragma unroll
     for (int jj = 0; jj < C::X_INSTR; ++jj) {
         const int j = wave * C::X_INSTR + jj;
         const int r = 4 * j + (lane >> 4);
         int64_t m = mrow0 + r;
         m = m < mrow1 ? m : mrow1 - 1;
-        xsrc[jj] = static_cast<const uint16_t *>(a.x) + m * a.k;
-        xel[jj] = ((lane & 15) ^ swz16(r)) * 8;
+        const int xel = ((lane & 15) ^ swz16(r)) * 8;
+        xp[jj] = static_cast<const uint16_t *>(a.x) + m * a.k + kb0 + xel;
+        xlim[jj] = (int)(ke - kb0 - xel);
     }
+    // stages entirely inside the K range need no masks
+    const int64_t t_full = (ke - kb0) / C::BK;
 
-    auto issue_w = [&](int64_t t) {
+    // One DMA "unit": token instruction jj of stage t, or weight instruction jj
+    // of stage t (upper bytes and, in full mode, residual bytes).
+    auto issue_w1 = [&](int jj, int64_t t) {
         uint8_t *st = smem + (int)(t % WS) * C::W_SLOT;
-        const bool live = t < ntk;
-        const int64_t kt = kb0 + t * C::BK;
-#pragma unroll
-        for (int jj = 0; jj < C::W_INSTR; ++jj) {
-            const int j = wave * C::W_INSTR + jj;
-            const int64_t kk = kt + wel[jj];
-            const bool ok = live && kk < ke;
-            dma16(ok ? (const void *)(wsrc[jj] + kk) : (const void *)g_zero16, st + j * 1024);
-            if (MODE == MODE_FULL) {
-                const int64_t lo = wl[jj] + (ok ? kk : kb0);
-                const void *src = g_zero16;
-                if (RANGE) {
-                    const bool second = lo >= rr[jj].bnd;
-                    const bool cok = second ? rr[jj].ok1 : rr[jj].ok0;
-                    const int64_t d = second ? rr[jj].delta1 : rr[jj].delta0;
-                    if (ok && cok)
-                        src = a.res.pool + (d + lo);
-                } else {
-                    const int64_t off = residual_offset(a.res, lo);
-                    if (ok && off >= 0)
-                        src = a.res.pool + off;
-                }
-                dma16(src, st + C::W_BYTES + j * 1024);
+        const bool masked = t >= t_full;
+        const int64_t off = t * C::BK;
+        const int j = wave * C::W_INSTR + jj;
+        const bool ok = !masked || off < wlim[jj];
+        dma16(ok ? (const void *)(wp[jj] + off) : (const void *)g_zero16, st + j * 1024);
+        if (MODE == MODE_FULL) {
+            const void *src = g_zero16;
+            if (RANGE) {
+                const bool second = t >= tsw[jj];
+                const bool cok = second ? rok1[jj] : rok0[jj];
+                const uint8_t *base = second ? rp1[jj] : rp0[jj];
+                if (ok && cok)
+                    src = base + off;
+            } else {
+                const int64_t o = residual_offset(a.res, wlog[jj] + (ok ? off : 0));
+                if (ok && o >= 0)
+                    src = a.res.pool + o;
             }
+            dma16(src, st + C::W_BYTES + j * 1024);
         }
+    };
+    auto issue_x1 = [&](int jj, int64_t t) {
+        uint8_t *st = smem + C::X_BASE + (int)(t & 1) * C::X_SLOT;
+        const bool masked = t >= t_full;
+        const int64_t off = t * C::BK;
+        const int j = wave * C::X_INSTR + jj;
+        const bool ok = !masked || off < xlim[jj];
+        dma16(ok ? (const void *)(xp[jj] + off) : (const void *)g_zero16, st + j * 1024);
+    };
+    auto issue_w = [&](int64_t t) {
+#pragma unroll
+        for (int jj = 0; jj < C::W_INSTR; ++jj)
+            issue_w1(jj, t);
     };
     auto issue_x = [&](int64_t t) {
-        uint8_t *st = smem + C::X_BASE + (int)(t & 1) * C::X_SLOT;
-        const bool live = t < ntk;
-        const int64_t kt = kb0 + t * C::BK;
 #pragma unroll
-        for (int jj = 0; jj < C::X_INSTR; ++jj) {
-            const int j = wave * C::X_INSTR + jj;
-            const int64_t kk = kt + xel[jj];
-            const bool ok = live && kk < ke;
-            dma16(ok ? (const void *)(xsrc[jj] + kk) : (const void *)g_zero16, st + j * 1024);
-        }
+        for (int jj = 0; jj < C::X_INSTR; ++jj)
+            issue_x1(jj, t);
     };
-
     f32x4 acc[4][C::MT];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -887,20 +923,25 @@ __global__ __launch_bounds__(512) void gemm4_kernel(GemmArgs a)
     issue_w(WS - 2);
     for (int64_t t = 0; t < ntk; ++t) {
         DPS_WAIT_VMCNT(C::NW);  // all but the newest weight group: tokens t, weights t
-        __syncthreads();
-        issue_x(t + 1);
-        issue_w(t + WS - 1);
+        stage_barrier();
         const uint8_t *st = smem + (int)(t % WS) * C::W_SLOT;
         const uint8_t *xs = smem + C::X_BASE + (int)(t & 1) * C::X_SLOT;
+        // fragment reads first, so their latency overlaps the DMA issue below
+        u32x4 hv[4], lv[4];
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+            hv[nt] = *reinterpret_cast<const u32x4 *>(st + aoff[nt]);
+            lv[nt] = u32x4{0u, 0u, 0u, 0u};
+            if (MODE == MODE_FULL)
+                lv[nt] = *reinterpret_cast<const u32x4 *>(st + C::W_BYTES + aoff[nt]);
+        }
+        issue_x(t + 1);
+        issue_w(t + WS - 1);
         half8 a0[4], a1[4];
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt) {
-            const u32x4 hv = *reinterpret_cast<const u32x4 *>(st + aoff[nt]);
-            u32x4 lv = {0u, 0u, 0u, 0u};
-            if (MODE == MODE_FULL)
-                lv = *reinterpret_cast<const u32x4 *>(st + C::W_BYTES + aoff[nt]);
-            a0[nt] = merge8(hv.x, hv.y, lv.x, lv.y);
-            a1[nt] = merge8(hv.z, hv.w, lv.z, lv.w);
+            a0[nt] = merge8(hv[nt].x, hv[nt].y, lv[nt].x, lv[nt].y);
+            a1[nt] = merge8(hv[nt].z, hv[nt].w, lv[nt].z, lv[nt].w);
         }
 #pragma unroll
         for (int sidx = 0; sidx < 2; ++sidx) {
