@@ -716,6 +716,12 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
 // through LDS at the end, in a fixed order.  The token tile BM (32, 64 or
 // 128) follows the call's token count, so short calls stage no padding rows.
 //
+// SPEC adds four DMA waves (one per SIMD) that do nothing but issue the
+// direct-to-LDS loads and wait for them; the eight compute waves then never
+// stall on address-unit slots and keep the matrix cores fed, and a stage costs
+// about max(DMA, MFMA) instead of their sum.  Both kinds of wave meet at the
+// one barrier per stage.
+//
 // Weights and tokens stream through separate LDS rings: WS weight slots (the
 // weight stream comes from HBM and wants several stages in flight) and two
 // token slots (tokens are L2-resident).  Iteration t issues tokens of stage
@@ -723,7 +729,7 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
 // in issue order, waiting until only the last weight group is outstanding
 // retires exactly tokens t and weights t, and the later weight stages stay in
 // flight across the barrier.
-template <int MODE, int BM, int WS>
+template <int MODE, int BM, int WS, int NISS>
 struct G4 {
     static constexpr int PLANES = MODE == MODE_FULL ? 2 : 1;
     static constexpr int BK = 128;
@@ -733,21 +739,22 @@ struct G4 {
     static constexpr int X_SLOT = BM * BK * 2;      // BM tokens, FP16
     static constexpr int X_BASE = W_SLOT * WS;
     static constexpr int LDS = X_BASE + 2 * X_SLOT;
-    static constexpr int W_INSTR = W_BYTES / 1024 / 8;  // per wave per plane
-    static constexpr int X_INSTR = X_SLOT / 1024 / 8;
-    static constexpr int NW = W_INSTR * PLANES;         // weight instructions per wave per stage
+    static constexpr int W_INSTR = W_BYTES / 1024 / NISS;  // per issuing wave per plane
+    static constexpr int X_INSTR = X_SLOT / 1024 / NISS;
+    static constexpr int NW = W_INSTR * PLANES;  // weight instructions per issuing wave per stage
     static_assert(WS >= 3, "the counter scheme needs three weight slots");
     static_assert(BM == 32 || BM == 64 || BM == 128, "token tile");
+    static_assert(X_INSTR >= 1 && W_INSTR >= 1, "DMA split over the issuing waves");
     static_assert(LDS <= 160 * 1024 && LDS >= 4 * 16384, "LDS (the K-half reduction needs 64 KiB)");
 };
 
 __device__ __forceinline__ int swz8(int r) { return (r >> 1) & 7; }
 __device__ __forceinline__ int swz16(int r) { return r & 15; }
 
-template <int MODE, int BM, int WS, bool RANGE>
-__global__ __launch_bounds__(512) void gemm4_kernel(GemmArgs a)
+template <int MODE, int BM, int WS, bool RANGE, bool SPEC>
+__global__ __launch_bounds__(SPEC ? 768 : 512) void gemm4_kernel(GemmArgs a)
 {
-    using C = G4<MODE, BM, WS>;
+    using C = G4<MODE, BM, WS, SPEC ? 4 : 8>;
     __shared__ __attribute__((aligned(16))) uint8_t smem[C::LDS];
 
     const int tid = threadIdx.x;
@@ -755,7 +762,9 @@ __global__ __launch_bounds__(512) void gemm4_kernel(GemmArgs a)
     const int wave = tid >> 6;
     const int li = lane & 15;
     const int lg = lane >> 4;
-    const int kh = wave >> 2;        // K-half of every stage
+    const bool dma_wave = SPEC && wave >= 8;
+    const int issuer = SPEC ? wave - 8 : wave;  // index among the waves that issue DMA
+    const int kh = (wave >> 2) & 1;  // K-half of every stage (compute waves)
     const int wn = (wave >> 1) & 1;  // 64-row quarter
     const int wm = wave & 1;         // BM/2-token half
 
@@ -810,9 +819,10 @@ __global__ __launch_bounds__(512) void gemm4_kernel(GemmArgs a)
     int64_t wlog[C::W_INSTR];  // logical residual index of the piece at stage 0
     int wlim[C::W_INSTR], tsw[C::W_INSTR];
     bool rok0[C::W_INSTR], rok1[C::W_INSTR];
+    const bool issues = !SPEC || dma_wave;  // compute waves of a SPEC block keep no DMA state
 #pragma unroll
-    for (int jj = 0; jj < C::W_INSTR; ++jj) {
-        const int j = wave * C::W_INSTR + jj;
+    for (int jj = 0; jj < C::W_INSTR && issues; ++jj) {
+        const int j = issuer * C::W_INSTR + jj;
         const int r = 8 * j + (lane >> 3);
         int64_t nr = n0 + r;
         nr = nr < a.n ? nr : a.n - 1;
@@ -838,8 +848,8 @@ __global__ __launch_bounds__(512) void gemm4_kernel(GemmArgs a)
     const uint16_t *xp[C::X_INSTR];
     int xlim[C::X_INSTR];
 #pragma unroll
-    for (int jj = 0; jj < C::X_INSTR; ++jj) {
-        const int j = wave * C::X_INSTR + jj;
+    for (int jj = 0; jj < C::X_INSTR && issues; ++jj) {
+        const int j = issuer * C::X_INSTR + jj;
         const int r = 4 * j + (lane >> 4);
         int64_t m = mrow0 + r;
         m = m < mrow1 ? m : mrow1 - 1;
@@ -856,7 +866,7 @@ __global__ __launch_bounds__(512) void gemm4_kernel(GemmArgs a)
         uint8_t *st = smem + (int)(t % WS) * C::W_SLOT;
         const bool masked = t >= t_full;
         const int64_t off = t * C::BK;
-        const int j = wave * C::W_INSTR + jj;
+        const int j = issuer * C::W_INSTR + jj;
         const bool ok = !masked || off < wlim[jj];
         dma16(ok ? (const void *)(wp[jj] + off) : (const void *)g_zero16, st + j * 1024);
         if (MODE == MODE_FULL) {
@@ -879,7 +889,7 @@ __global__ __launch_bounds__(512) void gemm4_kernel(GemmArgs a)
         uint8_t *st = smem + C::X_BASE + (int)(t & 1) * C::X_SLOT;
         const bool masked = t >= t_full;
         const int64_t off = t * C::BK;
-        const int j = wave * C::X_INSTR + jj;
+        const int j = issuer * C::X_INSTR + jj;
         const bool ok = !masked || off < xlim[jj];
         dma16(ok ? (const void *)(xp[jj] + off) : (const void *)g_zero16, st + j * 1024);
     };
@@ -915,18 +925,10 @@ __global__ __launch_bounds__(512) void gemm4_kernel(GemmArgs a)
             boff[mt][sidx] = r * 256 + (((8 * kh + 2 * lg + sidx) ^ swz16(r)) << 4);
     }
 
-    // prologue in the steady-state order: weights 0 .. WS-3, tokens 0, weights WS-2
-#pragma unroll
-    for (int t = 0; t < WS - 2; ++t)
-        issue_w(t);
-    issue_x(0);
-    issue_w(WS - 2);
-    for (int64_t t = 0; t < ntk; ++t) {
-        DPS_WAIT_VMCNT(C::NW);  // all but the newest weight group: tokens t, weights t
-        stage_barrier();
+    // one stage of matrix work on the slots of stage t
+    auto compute = [&](int64_t t) {
         const uint8_t *st = smem + (int)(t % WS) * C::W_SLOT;
         const uint8_t *xs = smem + C::X_BASE + (int)(t & 1) * C::X_SLOT;
-        // fragment reads first, so their latency overlaps the DMA issue below
         u32x4 hv[4], lv[4];
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt) {
@@ -935,8 +937,12 @@ __global__ __launch_bounds__(512) void gemm4_kernel(GemmArgs a)
             if (MODE == MODE_FULL)
                 lv[nt] = *reinterpret_cast<const u32x4 *>(st + C::W_BYTES + aoff[nt]);
         }
-        issue_x(t + 1);
-        issue_w(t + WS - 1);
+        // without DMA waves, this wave issues its share of the next stages'
+        // DMA here, after its fragment reads (their latency overlaps the issue)
+        if (!SPEC) {
+            issue_x(t + 1);
+            issue_w(t + WS - 1);
+        }
         half8 a0[4], a1[4];
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt) {
@@ -952,6 +958,40 @@ __global__ __launch_bounds__(512) void gemm4_kernel(GemmArgs a)
                 for (int nt = 0; nt < 4; ++nt)
                     acc[nt][mt] = mfma16x16x32(sidx ? a1[nt] : a0[nt], bv, acc[nt][mt]);
             }
+        }
+    };
+
+    if (!SPEC || dma_wave) {
+        // prologue in the steady-state order: weights 0 .. WS-3, tokens 0, weights WS-2
+#pragma unroll
+        for (int t = 0; t < WS - 2; ++t)
+            issue_w(t);
+        issue_x(0);
+        issue_w(WS - 2);
+    }
+    if (!SPEC) {
+        for (int64_t t = 0; t < ntk; ++t) {
+            DPS_WAIT_VMCNT(C::NW);  // all but the newest weight group: tokens t, weights t
+            stage_barrier();
+            compute(t);
+        }
+    } else if (dma_wave) {
+        // separate loops per role keep the DMA state out of the compute waves'
+        // registers and the accumulators out of the DMA waves'
+        for (int64_t t = 0; t < ntk; ++t) {
+            DPS_WAIT_VMCNT(C::NW);
+            stage_barrier();
+            issue_x(t + 1);
+            issue_w(t + WS - 1);
+        }
+        DPS_WAIT_VMCNT(0);  // no DMA may still target this block's LDS
+        __syncthreads();    // matches the compute waves' two barriers below
+        __syncthreads();
+        return;
+    } else {
+        for (int64_t t = 0; t < ntk; ++t) {
+            stage_barrier();
+            compute(t);
         }
     }
     DPS_WAIT_VMCNT(0);  // no DMA may still target this block's LDS
@@ -1112,9 +1152,9 @@ int gemm_rows_per_block(int variant)
 }
 int gemm_tokens_per_block(int variant)
 {
-    if (variant == GEMM_G4_128x64)
+    if (variant == GEMM_G4_128x64 || variant == GEMM_G4S_128x64)
         return 64;
-    if (variant == GEMM_G4_128x32)
+    if (variant == GEMM_G4_128x32 || variant == GEMM_G4S_128x32)
         return 32;
     return (variant == GEMM_DMA_256 || variant == GEMM_G3_256x256 || variant == GEMM_G3_128x256 ||
             variant == GEMM_G3_256x256_W16)
@@ -1143,7 +1183,7 @@ hipError_t launch_g3(const GemmArgs &a, const LinearPlan &plan, bool grouped, hi
     return hipGetLastError();
 }
 
-template <int MODE, int BM, int WS>
+template <int MODE, int BM, int WS, bool SPEC>
 hipError_t launch_g4(const GemmArgs &a, const LinearPlan &plan, bool grouped, hipStream_t stream)
 {
     const int64_t nt = (a.n + 127) / 128;
@@ -1153,10 +1193,11 @@ hipError_t launch_g4(const GemmArgs &a, const LinearPlan &plan, bool grouped, hi
         const int64_t total = nt * plan.splits * ((a.rows + BM - 1) / BM);
         grid = dim3((unsigned)((total + 7) / 8 * 8), 1, 1);
     }
+    const dim3 block(SPEC ? 768 : 512);
     if (MODE == MODE_FULL && plan.range_addr)
-        hipLaunchKernelGGL((gemm4_kernel<MODE, BM, WS, true>), grid, dim3(512), 0, stream, a);
+        hipLaunchKernelGGL((gemm4_kernel<MODE, BM, WS, true, SPEC>), grid, block, 0, stream, a);
     else
-        hipLaunchKernelGGL((gemm4_kernel<MODE, BM, WS, false>), grid, dim3(512), 0, stream, a);
+        hipLaunchKernelGGL((gemm4_kernel<MODE, BM, WS, false, SPEC>), grid, block, 0, stream, a);
     return hipGetLastError();
 }
 
@@ -1167,9 +1208,12 @@ hipError_t launch_g4_variant(const GemmArgs &a, const LinearPlan &plan, bool gro
 {
     constexpr bool FULL = MODE == MODE_FULL;
     switch (plan.variant) {
-    case GEMM_G4_128x128: return launch_g4<MODE, 128, FULL ? 3 : 6>(a, plan, grouped, stream);
-    case GEMM_G4_128x64: return launch_g4<MODE, 64, FULL ? 4 : 8>(a, plan, grouped, stream);
-    case GEMM_G4_128x32: return launch_g4<MODE, 32, FULL ? 4 : 9>(a, plan, grouped, stream);
+    case GEMM_G4_128x128: return launch_g4<MODE, 128, FULL ? 3 : 6, false>(a, plan, grouped, stream);
+    case GEMM_G4_128x64: return launch_g4<MODE, 64, FULL ? 4 : 8, false>(a, plan, grouped, stream);
+    case GEMM_G4_128x32: return launch_g4<MODE, 32, FULL ? 4 : 9, false>(a, plan, grouped, stream);
+    case GEMM_G4S_128x128: return launch_g4<MODE, 128, FULL ? 3 : 6, true>(a, plan, grouped, stream);
+    case GEMM_G4S_128x64: return launch_g4<MODE, 64, FULL ? 4 : 8, true>(a, plan, grouped, stream);
+    case GEMM_G4S_128x32: return launch_g4<MODE, 32, FULL ? 4 : 9, true>(a, plan, grouped, stream);
     default: return hipErrorInvalidValue;
     }
 }

@@ -52,7 +52,11 @@ enum GemmVariant {
     // loads, K split over waves
     GEMM_G4_128x128 = 8,
     GEMM_G4_128x64 = 9,
-    GEMM_G4_128x32 = 10
+    GEMM_G4_128x32 = 10,
+    // the same with four dedicated DMA waves
+    GEMM_G4S_128x128 = 11,
+    GEMM_G4S_128x64 = 12,
+    GEMM_G4S_128x32 = 13
 };
 // Decode-kernel variants 0..3 keep the weight stream in registers (tile
 // shapes differ); SKINNY_RING streams it through per-wave LDS rings.
