@@ -722,14 +722,13 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
 // about max(DMA, MFMA) instead of their sum.  Both kinds of wave meet at the
 // one barrier per stage.
 //
-// Weights and tokens stream through separate LDS rings: WS weight slots (the
-// weight stream comes from HBM and wants several stages in flight) and two
-// token slots (tokens are L2-resident).  Iteration t issues tokens of stage
-// t+1, then weights of stage t+WS-1; since the vector-memory counter retires
-// in issue order, waiting until only the last weight group is outstanding
-// retires exactly tokens t and weights t, and the later weight stages stay in
-// flight across the barrier.
-template <int MODE, int BM, int WS, int NISS>
+// Weights and tokens stream through separate LDS rings of WS and XS slots
+// (XS <= WS).  Iteration t issues tokens of stage t+XS-1, then weights of
+// stage t+WS-1.  The vector-memory counter retires in issue order, so waiting
+// until only the instructions issued after the later of tokens t and weights
+// t are outstanding (G4::OUTSTANDING) retires exactly those two, and the later
+// stages stay in flight across the barrier.
+template <int MODE, int BM, int WS, int XS, int NISS>
 struct G4 {
     static constexpr int PLANES = MODE == MODE_FULL ? 2 : 1;
     static constexpr int BK = 128;
@@ -738,11 +737,18 @@ struct G4 {
     static constexpr int W_SLOT = W_BYTES * PLANES;
     static constexpr int X_SLOT = BM * BK * 2;      // BM tokens, FP16
     static constexpr int X_BASE = W_SLOT * WS;
-    static constexpr int LDS = X_BASE + 2 * X_SLOT;
+    static constexpr int LDS = X_BASE + XS * X_SLOT;
     static constexpr int W_INSTR = W_BYTES / 1024 / NISS;  // per issuing wave per plane
     static constexpr int X_INSTR = X_SLOT / 1024 / NISS;
     static constexpr int NW = W_INSTR * PLANES;  // weight instructions per issuing wave per stage
-    static_assert(WS >= 3, "the counter scheme needs three weight slots");
+    static constexpr int NX = X_INSTR;
+    // Instructions that may stay outstanding at the wait for stage t: those
+    // issued after the later of tokens t and weights t.  With XS < WS that is
+    // tokens t, followed in its iteration by one weight group; with XS == WS
+    // both go out in the same iteration and weights t come last.
+    static constexpr int OUTSTANDING = (XS < WS ? NW : 0) + (XS - 2) * (NX + NW);
+    static_assert(WS >= 3 && XS >= 2 && XS <= WS, "ring depths of the counter scheme");
+    static_assert(OUTSTANDING <= 63, "vmcnt range");
     static_assert(BM == 32 || BM == 64 || BM == 128, "token tile");
     static_assert(X_INSTR >= 1 && W_INSTR >= 1, "DMA split over the issuing waves");
     static_assert(LDS <= 160 * 1024 && LDS >= 4 * 16384, "LDS (the K-half reduction needs 64 KiB)");
@@ -751,10 +757,10 @@ struct G4 {
 __device__ __forceinline__ int swz8(int r) { return (r >> 1) & 7; }
 __device__ __forceinline__ int swz16(int r) { return r & 15; }
 
-template <int MODE, int BM, int WS, bool RANGE, bool SPEC>
+template <int MODE, int BM, int WS, int XS, bool RANGE, bool SPEC>
 __global__ __launch_bounds__(SPEC ? 768 : 512) void gemm4_kernel(GemmArgs a)
 {
-    using C = G4<MODE, BM, WS, SPEC ? 4 : 8>;
+    using C = G4<MODE, BM, WS, XS, SPEC ? 4 : 8>;
     __shared__ __attribute__((aligned(16))) uint8_t smem[C::LDS];
 
     const int tid = threadIdx.x;
@@ -886,7 +892,7 @@ __global__ __launch_bounds__(SPEC ? 768 : 512) void gemm4_kernel(GemmArgs a)
         }
     };
     auto issue_x1 = [&](int jj, int64_t t) {
-        uint8_t *st = smem + C::X_BASE + (int)(t & 1) * C::X_SLOT;
+        uint8_t *st = smem + C::X_BASE + (int)(t % XS) * C::X_SLOT;
         const bool masked = t >= t_full;
         const int64_t off = t * C::BK;
         const int j = issuer * C::X_INSTR + jj;
@@ -928,7 +934,7 @@ __global__ __launch_bounds__(SPEC ? 768 : 512) void gemm4_kernel(GemmArgs a)
     // one stage of matrix work on the slots of stage t
     auto compute = [&](int64_t t) {
         const uint8_t *st = smem + (int)(t % WS) * C::W_SLOT;
-        const uint8_t *xs = smem + C::X_BASE + (int)(t & 1) * C::X_SLOT;
+        const uint8_t *xs = smem + C::X_BASE + (int)(t % XS) * C::X_SLOT;
         u32x4 hv[4], lv[4];
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt) {
@@ -940,7 +946,7 @@ __global__ __launch_bounds__(SPEC ? 768 : 512) void gemm4_kernel(GemmArgs a)
         // without DMA waves, this wave issues its share of the next stages'
         // DMA here, after its fragment reads (their latency overlaps the issue)
         if (!SPEC) {
-            issue_x(t + 1);
+            issue_x(t + XS - 1);
             issue_w(t + WS - 1);
         }
         half8 a0[4], a1[4];
@@ -962,16 +968,19 @@ __global__ __launch_bounds__(SPEC ? 768 : 512) void gemm4_kernel(GemmArgs a)
     };
 
     if (!SPEC || dma_wave) {
-        // prologue in the steady-state order: weights 0 .. WS-3, tokens 0, weights WS-2
+        // prologue: the steady-state issue of iterations -(WS-1) .. -1, keeping
+        // only stages >= 0, so the counter arithmetic holds from iteration 0
 #pragma unroll
-        for (int t = 0; t < WS - 2; ++t)
-            issue_w(t);
-        issue_x(0);
-        issue_w(WS - 2);
+        for (int u = -(WS - 1); u < 0; ++u) {
+            if (u + XS - 1 >= 0)
+                issue_x(u + XS - 1);
+            if (u + WS - 1 >= 0)
+                issue_w(u + WS - 1);
+        }
     }
     if (!SPEC) {
         for (int64_t t = 0; t < ntk; ++t) {
-            DPS_WAIT_VMCNT(C::NW);  // all but the newest weight group: tokens t, weights t
+            DPS_WAIT_VMCNT(C::OUTSTANDING);  // tokens t and weights t have landed
             stage_barrier();
             compute(t);
         }
@@ -979,9 +988,9 @@ __global__ __launch_bounds__(SPEC ? 768 : 512) void gemm4_kernel(GemmArgs a)
         // separate loops per role keep the DMA state out of the compute waves'
         // registers and the accumulators out of the DMA waves'
         for (int64_t t = 0; t < ntk; ++t) {
-            DPS_WAIT_VMCNT(C::NW);
+            DPS_WAIT_VMCNT(C::OUTSTANDING);
             stage_barrier();
-            issue_x(t + 1);
+            issue_x(t + XS - 1);
             issue_w(t + WS - 1);
         }
         DPS_WAIT_VMCNT(0);  // no DMA may still target this block's LDS
@@ -1183,7 +1192,7 @@ hipError_t launch_g3(const GemmArgs &a, const LinearPlan &plan, bool grouped, hi
     return hipGetLastError();
 }
 
-template <int MODE, int BM, int WS, bool SPEC>
+template <int MODE, int BM, int WS, int XS, bool SPEC>
 hipError_t launch_g4(const GemmArgs &a, const LinearPlan &plan, bool grouped, hipStream_t stream)
 {
     const int64_t nt = (a.n + 127) / 128;
@@ -1195,26 +1204,39 @@ hipError_t launch_g4(const GemmArgs &a, const LinearPlan &plan, bool grouped, hi
     }
     const dim3 block(SPEC ? 768 : 512);
     if (MODE == MODE_FULL && plan.range_addr)
-        hipLaunchKernelGGL((gemm4_kernel<MODE, BM, WS, true, SPEC>), grid, block, 0, stream, a);
+        hipLaunchKernelGGL((gemm4_kernel<MODE, BM, WS, XS, true, SPEC>), grid, block, 0, stream, a);
     else
-        hipLaunchKernelGGL((gemm4_kernel<MODE, BM, WS, false, SPEC>), grid, block, 0, stream, a);
+        hipLaunchKernelGGL((gemm4_kernel<MODE, BM, WS, XS, false, SPEC>), grid, block, 0, stream, a);
     return hipGetLastError();
 }
 
-// weight-ring depth per (mode, token tile): the deepest ring that fits 160 KiB
+// ring depths per (mode, token tile), within 160 KiB: weights want depth (HBM),
+// tokens at least a second slot ahead where it fits
 template <int MODE>
 hipError_t launch_g4_variant(const GemmArgs &a, const LinearPlan &plan, bool grouped,
                              hipStream_t stream)
 {
-    constexpr bool FULL = MODE == MODE_FULL;
-    switch (plan.variant) {
-    case GEMM_G4_128x128: return launch_g4<MODE, 128, FULL ? 3 : 6, false>(a, plan, grouped, stream);
-    case GEMM_G4_128x64: return launch_g4<MODE, 64, FULL ? 4 : 8, false>(a, plan, grouped, stream);
-    case GEMM_G4_128x32: return launch_g4<MODE, 32, FULL ? 4 : 9, false>(a, plan, grouped, stream);
-    case GEMM_G4S_128x128: return launch_g4<MODE, 128, FULL ? 3 : 6, true>(a, plan, grouped, stream);
-    case GEMM_G4S_128x64: return launch_g4<MODE, 64, FULL ? 4 : 8, true>(a, plan, grouped, stream);
-    case GEMM_G4S_128x32: return launch_g4<MODE, 32, FULL ? 4 : 9, true>(a, plan, grouped, stream);
-    default: return hipErrorInvalidValue;
+    // (token tile, weight slots, token slots) per mode, each within 160 KiB
+    if constexpr (MODE == MODE_FULL) {
+        switch (plan.variant) {
+        case GEMM_G4_128x128: return launch_g4<MODE, 128, 3, 2, false>(a, plan, grouped, stream);
+        case GEMM_G4_128x64: return launch_g4<MODE, 64, 4, 2, false>(a, plan, grouped, stream);
+        case GEMM_G4_128x32: return launch_g4<MODE, 32, 4, 4, false>(a, plan, grouped, stream);
+        case GEMM_G4S_128x128: return launch_g4<MODE, 128, 3, 2, true>(a, plan, grouped, stream);
+        case GEMM_G4S_128x64: return launch_g4<MODE, 64, 4, 2, true>(a, plan, grouped, stream);
+        case GEMM_G4S_128x32: return launch_g4<MODE, 32, 4, 4, true>(a, plan, grouped, stream);
+        default: return hipErrorInvalidValue;
+        }
+    } else {
+        switch (plan.variant) {
+        case GEMM_G4_128x128: return launch_g4<MODE, 128, 4, 3, false>(a, plan, grouped, stream);
+        case GEMM_G4_128x64: return launch_g4<MODE, 64, 6, 4, false>(a, plan, grouped, stream);
+        case GEMM_G4_128x32: return launch_g4<MODE, 32, 8, 4, false>(a, plan, grouped, stream);
+        case GEMM_G4S_128x128: return launch_g4<MODE, 128, 4, 3, true>(a, plan, grouped, stream);
+        case GEMM_G4S_128x64: return launch_g4<MODE, 64, 6, 4, true>(a, plan, grouped, stream);
+        case GEMM_G4S_128x32: return launch_g4<MODE, 32, 8, 4, true>(a, plan, grouped, stream);
+        default: return hipErrorInvalidValue;
+        }
     }
 }
 
