@@ -135,11 +135,12 @@ LinearPlan plan_linear(int mode, uint32_t flags, int64_t rows, int64_t n, int64_
         p.ksplit = round_up(cdiv(k, s), 128);
         p.splits = (int)cdiv(k, p.ksplit);
         p.ws_quant = align256(rows * k) + align256(rows * 4);
-    } else if (rows_per_expert <= 16) {
-        // Up to 16 tokens per expert the decode kernel streams the weights
-        // (LDS rings of 256-byte rows); from 17 tokens on, the wide-row GEMM
-        // below is as fast or faster on MI355X (at 32 tokens, full mode, the
-        // 28672 x 4096 layer takes 59 us against 95 us).
+    } else if (rows_per_expert <= 1 || (rows_per_expert <= 4 && n * k <= (int64_t(1) << 25))) {
+        // The decode kernel (per-wave LDS rings of 256-byte rows) serves one
+        // token per expert, and up to four on layers of at most 2^25 weights.
+        // Everywhere else the wide-row GEMM with 32-token tiles is as fast or
+        // faster on MI355X (8 tokens, hidden-4096 set, both modes: 182 us
+        // against 224 us; the full-mode 28672 x 4096 layer 50 us against 68).
         p.kind = KIND_SKINNY;
         // measured on MI355X: up to 8 tokens, the weight stream through shallow
         // per-wave LDS rings (two blocks per CU); above that, registers with
