@@ -127,7 +127,7 @@ dps_status dps_merge(const uint8_t *hi, const dps_residual *res, int64_t numel,
                      uint16_t *w_out, void *stream);
 
 /* Per-row FP8 quantization of activations for fast-mode prefill (this
- * build's reading of the dynamic per-token activations of Sec. V-A
+ * reading taken here of the dynamic per-token activations of Sec. V-A
  * "Baselines"): for row r, a = max_k |x[r][k]|, scale[r] = the smallest power
  * of two s with a <= 448 * s (1 when a == 0), xq[r][k] = OCP E4M3 nearest to
  * x[r][k] / s, ties to even.  The division is exact, so this is bit-exact.
