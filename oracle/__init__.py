@@ -18,6 +18,8 @@ _lib = None
 
 FULL = 0
 FAST = 1
+E5M2 = 0
+E4M3 = 1
 
 
 def _load():
@@ -40,21 +42,26 @@ def _load():
     lib.oracle_e4m3_rne.restype = ctypes.c_int
     lib.oracle_residual_addr.argtypes = [I64, P, I64, I32, I64]
     lib.oracle_residual_addr.restype = I64
-    lib.oracle_split.argtypes = [P, I64, P, P, I64, P, I64, I32]
+    C = ctypes.c_int
+    lib.oracle_fast_value.argtypes = [C, ctypes.c_uint8]
+    lib.oracle_fast_value.restype = ctypes.c_double
+    lib.oracle_select_enc.argtypes = [P, I64]
+    lib.oracle_select_enc.restype = ctypes.c_int
+    lib.oracle_split.argtypes = [C, P, I64, P, P, I64, P, I64, I32]
     lib.oracle_split.restype = ctypes.c_int
-    lib.oracle_merge.argtypes = [P, P, I64, P, I64, I32, I64, P]
+    lib.oracle_merge.argtypes = [C, P, P, I64, P, I64, I32, I64, P]
     lib.oracle_merge.restype = ctypes.c_int
-    lib.oracle_linear.argtypes = [ctypes.c_int, P, I64, I64, I64, P, P, I64, P, I64, I32, P]
+    lib.oracle_linear.argtypes = [C, C, P, I64, I64, I64, P, P, I64, P, I64, I32, P]
     lib.oracle_linear.restype = ctypes.c_int
-    lib.oracle_linear_grouped.argtypes = [ctypes.c_int, P, P, I64, I64, I64, P, P, I64,
+    lib.oracle_linear_grouped.argtypes = [C, C, P, P, I64, I64, I64, P, P, I64,
                                           P, I64, I32, P]
     lib.oracle_linear_grouped.restype = ctypes.c_int
-    lib.oracle_linear_rows.argtypes = [ctypes.c_int, P, P, I64, I64, I64, P, P, I64, P,
+    lib.oracle_linear_rows.argtypes = [C, C, P, P, I64, I64, I64, P, P, I64, P,
                                        I64, I32, P]
     lib.oracle_linear_rows.restype = ctypes.c_int
     lib.oracle_act_quant.argtypes = [P, I64, I64, P, P]
     lib.oracle_act_quant.restype = ctypes.c_int
-    lib.oracle_linear_fp8.argtypes = [P, P, I64, I64, I64, P, P]
+    lib.oracle_linear_fp8.argtypes = [C, P, P, I64, I64, I64, P, P]
     lib.oracle_linear_fp8.restype = ctypes.c_int
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
@@ -123,21 +130,33 @@ def residual_addr(i, res: Residual):
                                     res.log2_chunk, res.pool.size)
 
 
-def split(w, res: Residual):
+def fast_value(enc, code):
+    """Fast-mode weight value of one upper byte under encoding enc."""
+    return _load().oracle_fast_value(enc, int(code))
+
+
+def select_enc(w):
+    """Per-layer nested encoding for FP16 words w (any shape): E4M3 or E5M2."""
+    lib = _load()
+    w = _u16(w)
+    return lib.oracle_select_enc(_ptr(w), w.size)
+
+
+def split(w, res: Residual, enc=E5M2):
     """FP16 words (any shape) -> hi plane (same shape, uint8); writes res.pool."""
     lib = _load()
     w = _u16(w)
     hi = np.empty(w.shape, dtype=np.uint8)
-    _check(lib.oracle_split(_ptr(w), w.size, _ptr(hi), *res.args()), "split")
+    _check(lib.oracle_split(enc, _ptr(w), w.size, _ptr(hi), *res.args()), "split")
     return hi
 
 
-def merge(hi, res: Residual):
+def merge(hi, res: Residual, enc=E5M2):
     lib = _load()
     hi = np.ascontiguousarray(hi, dtype=np.uint8)
     out = np.empty(hi.shape, dtype=np.uint16)
     pool, pool_bytes, slots, n_chunks, log2c = res.args()
-    _check(lib.oracle_merge(_ptr(hi), pool, pool_bytes, slots, n_chunks, log2c, hi.size,
+    _check(lib.oracle_merge(enc, _ptr(hi), pool, pool_bytes, slots, n_chunks, log2c, hi.size,
                             _ptr(out)), "merge")
     return out
 
@@ -148,7 +167,7 @@ def _res_args(res):
     return res.args()
 
 
-def linear(mode, x, hi, res=None):
+def linear(mode, x, hi, res=None, enc=E5M2):
     """x: fp16 bits [m][k]; hi: uint8 [n][k] -> fp64 [m][n]."""
     lib = _load()
     x = _u16(x)
@@ -157,12 +176,12 @@ def linear(mode, x, hi, res=None):
     n = hi.shape[0]
     assert hi.shape == (n, k)
     y = np.empty((m, n), dtype=np.float64)
-    _check(lib.oracle_linear(mode, _ptr(x), m, n, k, _ptr(hi), *_res_args(res), _ptr(y)),
+    _check(lib.oracle_linear(mode, enc, _ptr(x), m, n, k, _ptr(hi), *_res_args(res), _ptr(y)),
            "linear")
     return y
 
 
-def linear_rows(mode, x, rows, hi, res=None):
+def linear_rows(mode, x, rows, hi, res=None, enc=E5M2):
     """Dense linear on the listed rows of x only -> fp64 [len(rows)][n]."""
     lib = _load()
     x = _u16(x)
@@ -173,12 +192,12 @@ def linear_rows(mode, x, rows, hi, res=None):
     assert hi.shape == (n, k)
     assert rows.size == 0 or (rows.min() >= 0 and rows.max() < x.shape[0])
     y = np.empty((rows.size, n), dtype=np.float64)
-    _check(lib.oracle_linear_rows(mode, _ptr(x), _ptr(rows), rows.size, n, k, _ptr(hi),
+    _check(lib.oracle_linear_rows(mode, enc, _ptr(x), _ptr(rows), rows.size, n, k, _ptr(hi),
                                   *_res_args(res), _ptr(y)), "linear_rows")
     return y
 
 
-def linear_grouped(mode, x_sorted, offsets, hi, res=None):
+def linear_grouped(mode, x_sorted, offsets, hi, res=None, enc=E5M2):
     """x_sorted fp16 bits [rows][k]; offsets int [E+1]; hi uint8 [E][n][k] -> fp64 [rows][n]."""
     lib = _load()
     x = _u16(x_sorted)
@@ -187,7 +206,7 @@ def linear_grouped(mode, x_sorted, offsets, hi, res=None):
     e, n, k = hi.shape
     assert offsets.size == e + 1 and x.shape[1] == k and offsets[-1] == x.shape[0]
     y = np.empty((x.shape[0], n), dtype=np.float64)
-    _check(lib.oracle_linear_grouped(mode, _ptr(x), _ptr(offsets), e, n, k, _ptr(hi),
+    _check(lib.oracle_linear_grouped(mode, enc, _ptr(x), _ptr(offsets), e, n, k, _ptr(hi),
                                      *_res_args(res), _ptr(y)), "linear_grouped")
     return y
 
@@ -203,7 +222,7 @@ def act_quant(x):
     return xq, s
 
 
-def linear_fp8(xq, scale, hi):
+def linear_fp8(xq, scale, hi, enc=E5M2):
     lib = _load()
     xq = np.ascontiguousarray(xq, dtype=np.uint8)
     scale = np.ascontiguousarray(scale, dtype=np.float64)
@@ -212,7 +231,7 @@ def linear_fp8(xq, scale, hi):
     n = hi.shape[0]
     assert hi.shape == (n, k) and scale.shape == (m,)
     y = np.empty((m, n), dtype=np.float64)
-    _check(lib.oracle_linear_fp8(_ptr(xq), _ptr(scale), m, n, k, _ptr(hi), _ptr(y)),
+    _check(lib.oracle_linear_fp8(enc, _ptr(xq), _ptr(scale), m, n, k, _ptr(hi), _ptr(y)),
            "linear_fp8")
     return y
 

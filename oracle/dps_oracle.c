@@ -27,8 +27,19 @@
  *     "Shared Region": physical units mapped behind one virtual tensor);
  *   - fast-mode prefill quantizes each activation row to OCP E4M3 with a
  *     dynamic power-of-two scale (per-token dynamic activations as in
- *     Sec. V-A "Baselines"; the power of two is this build's choice so that
- *     scaling is exact and only one rounding happens).
+ *     Sec. V-A "Baselines"; the power of two is chosen so that scaling is
+ *     exact and only one rounding happens);
+ *   - the E4M3 nesting (Sec. IV-B "Persistent Region") keeps the sign, the
+ *     four low exponent bits and the three leading mantissa bits; the dropped
+ *     exponent MSB is zero for every weight it is used on, so the FP8 part
+ *     read as OCP E4M3 (bias 7) is the FP16 value times 2^8, truncated, and
+ *     the fast-mode weight is E4M3(upper) * 2^-8.  The residual is the seven
+ *     low mantissa bits, kept in the low bits of a byte;
+ *   - the per-layer encoding choice (Sec. IV-C, "Dual-mode serving"
+ *     paragraph: E5M2 for layers whose range E4M3 cannot express) takes E4M3
+ *     exactly when every weight of the layer nests losslessly (exponent MSB
+ *     zero) and its E4M3 part is a number, i.e. |w| < 1.875; the largest
+ *     fast-mode magnitude is then 448 * 2^-8 = 1.75.
  */
 #include <math.h>
 #include <stdint.h>
@@ -156,36 +167,96 @@ static int check_residual(int64_t numel, const int32_t *slots, int64_t n_chunks,
 /* Split and merge (Sec. IV-A, Sec. IV-B "Persistent Region").               */
 /* ------------------------------------------------------------------------ */
 
-/* FP16 word b -> upper byte (the E5M2 part kept in the persistent region)
- * and lower byte (the residual, written through the chunk table).          */
-int oracle_split(const uint16_t *w, int64_t numel, uint8_t *hi, uint8_t *pool,
+enum { ORACLE_ENC_E5M2 = 0, ORACLE_ENC_E4M3 = 1 };
+
+/* The two nested parts of the FP16 word b with fields sign s, exponent e
+ * (5 bits), mantissa m (10 bits):
+ *   E5M2: upper = s | e | m's 2 leading bits,         residual = m's 8 low bits
+ *   E4M3: upper = s | e's 4 low bits | m's 3 leading, residual = m's 7 low bits
+ * Field arithmetic only, so each line can be checked against the layouts.  */
+static void nest_word(int enc, uint16_t b, uint8_t *hi, uint8_t *lo)
+{
+    int s = b / 32768, e = (b / 1024) % 32, m = b % 1024;
+    if (enc == ORACLE_ENC_E5M2) {
+        *hi = (uint8_t)(s * 128 + e * 4 + m / 256);
+        *lo = (uint8_t)(m % 256);
+    } else {
+        *hi = (uint8_t)(s * 128 + (e % 16) * 8 + m / 128);
+        *lo = (uint8_t)(m % 128);
+    }
+}
+
+/* Inverse of nest_word: the FP16 word the two parts describe.  For E4M3 the
+ * exponent MSB is zero and only the residual byte's seven low bits count.  */
+static uint16_t unnest_word(int enc, uint8_t hi, uint8_t lo)
+{
+    int s = hi / 128;
+    if (enc == ORACLE_ENC_E5M2) {
+        int e = (hi / 4) % 32, mh = hi % 4;
+        return (uint16_t)(s * 32768 + e * 1024 + mh * 256 + lo);
+    }
+    int e = (hi / 8) % 16, mh = hi % 8;
+    return (uint16_t)(s * 32768 + e * 1024 + mh * 128 + lo % 128);
+}
+
+/* Fast-mode weight value of an upper byte: E5M2 as stored, or E4M3 scaled
+ * back by 2^-8 (the E4M3 bias 7 against FP16's 15).                        */
+double oracle_fast_value(int enc, uint8_t hi)
+{
+    if (enc == ORACLE_ENC_E5M2)
+        return oracle_e5m2_value(hi);
+    return ldexp(oracle_e4m3_value(hi), -8);
+}
+
+/* Per-layer encoding: E4M3 when every word nests losslessly into it and its
+ * E4M3 part is a number, else E5M2.  An empty layer gets E4M3.             */
+int oracle_select_enc(const uint16_t *w, int64_t numel)
+{
+    for (int64_t i = 0; i < numel; ++i) {
+        int e = (w[i] / 1024) % 32;
+        uint8_t hi, lo;
+        nest_word(ORACLE_ENC_E4M3, w[i], &hi, &lo);
+        if (e >= 16 || isnan(oracle_e4m3_value(hi)))
+            return ORACLE_ENC_E5M2;
+    }
+    return ORACLE_ENC_E4M3;
+}
+
+/* FP16 words -> upper bytes (the FP8 part kept in the persistent region)
+ * and residual bytes (written through the chunk table).  E4M3 on a word
+ * whose exponent MSB is set keeps the fields above all the same (the MSB is
+ * lost); oracle_select_enc tells whether a layer has such words.          */
+int oracle_split(int enc, const uint16_t *w, int64_t numel, uint8_t *hi, uint8_t *pool,
                  int64_t pool_bytes, const int32_t *slots, int64_t n_chunks,
                  int32_t log2_chunk)
 {
+    if (enc != ORACLE_ENC_E5M2 && enc != ORACLE_ENC_E4M3)
+        return -1;
     if (check_residual(numel, slots, n_chunks, log2_chunk, pool_bytes))
         return -1;
     for (int64_t i = 0; i < numel; ++i) {
         int64_t p = oracle_residual_addr(i, slots, n_chunks, log2_chunk, pool_bytes);
         if (p < 0)
             return -1;
-        hi[i] = (uint8_t)(w[i] / 256);
-        pool[p] = (uint8_t)(w[i] % 256);
+        nest_word(enc, w[i], &hi[i], &pool[p]);
     }
     return 0;
 }
 
-/* Upper byte and residual byte -> the original FP16 word.                  */
-int oracle_merge(const uint8_t *hi, const uint8_t *pool, int64_t pool_bytes,
+/* Upper byte and residual byte -> the FP16 word.                          */
+int oracle_merge(int enc, const uint8_t *hi, const uint8_t *pool, int64_t pool_bytes,
                  const int32_t *slots, int64_t n_chunks, int32_t log2_chunk,
                  int64_t numel, uint16_t *w_out)
 {
+    if (enc != ORACLE_ENC_E5M2 && enc != ORACLE_ENC_E4M3)
+        return -1;
     if (check_residual(numel, slots, n_chunks, log2_chunk, pool_bytes))
         return -1;
     for (int64_t i = 0; i < numel; ++i) {
         int64_t p = oracle_residual_addr(i, slots, n_chunks, log2_chunk, pool_bytes);
         if (p < 0)
             return -1;
-        w_out[i] = (uint16_t)((uint16_t)hi[i] * 256 + pool[p]);
+        w_out[i] = unnest_word(enc, hi[i], pool[p]);
     }
     return 0;
 }
@@ -194,7 +265,7 @@ int oracle_merge(const uint8_t *hi, const uint8_t *pool, int64_t pool_bytes,
 /* Nested linear layer (Sec. IV-C "Overall concept" and the GroupedGEMM     */
 /* paragraph): Y[r][c] = sum_k X[r][k] * W[c][k].                           */
 /*   full mode : W = the FP16 value of (upper byte, residual byte)          */
-/*   fast mode : W = the E5M2 value of the upper byte; the residual is not  */
+/*   fast mode : W = oracle_fast_value(upper byte); the residual is not     */
 /*               read at all (pool and slots may be NULL).                  */
 /* ------------------------------------------------------------------------ */
 
@@ -203,7 +274,7 @@ enum { ORACLE_FULL = 0, ORACLE_FAST = 1 };
 /* Weight element (c, k) of the expert whose elements start at logical
  * offset w_base (e * n * k for expert e).  Fills row c of the decoded
  * weight into wrow[0..k).                                                  */
-static void decode_weight_row(int mode, const uint8_t *hi, const uint8_t *pool,
+static void decode_weight_row(int mode, int enc, const uint8_t *hi, const uint8_t *pool,
                               int64_t pool_bytes, const int32_t *slots,
                               int64_t n_chunks, int32_t log2_chunk,
                               int64_t w_base, int64_t c, int64_t k, double *wrow)
@@ -211,11 +282,10 @@ static void decode_weight_row(int mode, const uint8_t *hi, const uint8_t *pool,
     for (int64_t kk = 0; kk < k; ++kk) {
         int64_t i = w_base + c * k + kk;
         if (mode == ORACLE_FAST) {
-            wrow[kk] = oracle_e5m2_value(hi[i]);
+            wrow[kk] = oracle_fast_value(enc, hi[i]);
         } else {
             int64_t p = oracle_residual_addr(i, slots, n_chunks, log2_chunk, pool_bytes);
-            uint16_t word = (uint16_t)((uint16_t)hi[i] * 256 + (p < 0 ? 0 : pool[p]));
-            wrow[kk] = oracle_fp16_value(word);
+            wrow[kk] = oracle_fp16_value(unnest_word(enc, hi[i], p < 0 ? 0 : pool[p]));
         }
     }
 }
@@ -224,13 +294,15 @@ static void decode_weight_row(int mode, const uint8_t *hi, const uint8_t *pool,
  * e's weights (elements e*n*k ... (e+1)*n*k - 1 of hi and of the residual
  * stream).  Dense is experts == 1 with offsets {0, rows}.  y is fp64
  * [rows][n].  hi holds experts*n*k bytes.                                   */
-int oracle_linear_grouped(int mode, const uint16_t *x, const int64_t *offsets,
+int oracle_linear_grouped(int mode, int enc, const uint16_t *x, const int64_t *offsets,
                           int64_t experts, int64_t n, int64_t k,
                           const uint8_t *hi, const uint8_t *pool, int64_t pool_bytes,
                           const int32_t *slots, int64_t n_chunks, int32_t log2_chunk,
                           double *y)
 {
     if (mode != ORACLE_FULL && mode != ORACLE_FAST)
+        return -1;
+    if (enc != ORACLE_ENC_E5M2 && enc != ORACLE_ENC_E4M3)
         return -1;
     if (experts < 1 || n < 0 || k < 0 || offsets[0] != 0)
         return -1;
@@ -256,7 +328,7 @@ int oracle_linear_grouped(int mode, const uint16_t *x, const int64_t *offsets,
             } else {
 #pragma omp for schedule(static)
                 for (int64_t c = 0; c < n; ++c) {
-                    decode_weight_row(mode, hi, pool, pool_bytes, slots, n_chunks,
+                    decode_weight_row(mode, enc, hi, pool, pool_bytes, slots, n_chunks,
                                       log2_chunk, w_base, c, k, wrow);
                     for (int64_t r = r0; r < r1; ++r) {
                         double acc = 0.0;
@@ -272,24 +344,26 @@ int oracle_linear_grouped(int mode, const uint16_t *x, const int64_t *offsets,
     return bad ? -1 : 0;
 }
 
-int oracle_linear(int mode, const uint16_t *x, int64_t m, int64_t n, int64_t k,
+int oracle_linear(int mode, int enc, const uint16_t *x, int64_t m, int64_t n, int64_t k,
                   const uint8_t *hi, const uint8_t *pool, int64_t pool_bytes,
                   const int32_t *slots, int64_t n_chunks, int32_t log2_chunk,
                   double *y)
 {
     int64_t offsets[2] = {0, m};
-    return oracle_linear_grouped(mode, x, offsets, 1, n, k, hi, pool, pool_bytes,
+    return oracle_linear_grouped(mode, enc, x, offsets, 1, n, k, hi, pool, pool_bytes,
                                  slots, n_chunks, log2_chunk, y);
 }
 
 /* Dense linear restricted to the listed output rows (for sampled checks of
  * large problems): y[j][c] = sum_k X[rows[j]][k] * W[c][k].               */
-int oracle_linear_rows(int mode, const uint16_t *x, const int64_t *rows,
+int oracle_linear_rows(int mode, int enc, const uint16_t *x, const int64_t *rows,
                        int64_t n_rows, int64_t n, int64_t k, const uint8_t *hi,
                        const uint8_t *pool, int64_t pool_bytes, const int32_t *slots,
                        int64_t n_chunks, int32_t log2_chunk, double *y)
 {
     if (mode != ORACLE_FULL && mode != ORACLE_FAST)
+        return -1;
+    if (enc != ORACLE_ENC_E5M2 && enc != ORACLE_ENC_E4M3)
         return -1;
     if (mode == ORACLE_FULL &&
         check_residual(n * k, slots, n_chunks, log2_chunk, pool_bytes))
@@ -304,7 +378,7 @@ int oracle_linear_rows(int mode, const uint16_t *x, const int64_t *rows,
         } else {
 #pragma omp for schedule(static)
             for (int64_t c = 0; c < n; ++c) {
-                decode_weight_row(mode, hi, pool, pool_bytes, slots, n_chunks,
+                decode_weight_row(mode, enc, hi, pool, pool_bytes, slots, n_chunks,
                                   log2_chunk, 0, c, k, wrow);
                 for (int64_t j = 0; j < n_rows; ++j) {
                     double acc = 0.0;
@@ -353,16 +427,19 @@ int oracle_act_quant(const uint16_t *x, int64_t m, int64_t k, uint8_t *xq, doubl
     return 0;
 }
 
-/* Y[r][c] = s_r * sum_k E4M3(Xq[r][k]) * E5M2(hi[c][k]) in fp64.           */
-int oracle_linear_fp8(const uint8_t *xq, const double *scale, int64_t m, int64_t n,
+/* Y[r][c] = s_r * sum_k E4M3(Xq[r][k]) * oracle_fast_value(hi[c][k]).    */
+int oracle_linear_fp8(int enc, const uint8_t *xq, const double *scale, int64_t m, int64_t n,
                       int64_t k, const uint8_t *hi, double *y)
 {
+    if (enc != ORACLE_ENC_E5M2 && enc != ORACLE_ENC_E4M3)
+        return -1;
 #pragma omp parallel for schedule(static)
     for (int64_t c = 0; c < n; ++c) {
         for (int64_t r = 0; r < m; ++r) {
             double acc = 0.0;
             for (int64_t kk = 0; kk < k; ++kk)
-                acc += oracle_e4m3_value(xq[r * k + kk]) * oracle_e5m2_value(hi[c * k + kk]);
+                acc += oracle_e4m3_value(xq[r * k + kk]) *
+                       oracle_fast_value(enc, hi[c * k + kk]);
             y[r * n + c] = scale[r] * acc;
         }
     }

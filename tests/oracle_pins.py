@@ -316,10 +316,156 @@ def pin_linear_fp8():
     assert np.allclose(y, want, rtol=1e-12, atol=1e-14)
 
 
+# --------------------------------------------------------------------------
+# E4M3 nesting and the per-layer encoding choice
+# --------------------------------------------------------------------------
+
+def _e4m3_fast_lib(codes):
+    """Fast-mode weights of E4M3 upper bytes: torch float8_e4m3fn times 2^-8."""
+    return _e4m3_lib(codes) * 2.0 ** -8
+
+
+def _eligible_e4m3(bits):
+    """Words whose value is finite and below 1.875 in magnitude (numpy float16)."""
+    x = _fp16_lib(bits)
+    return np.isfinite(x) & (np.abs(x) < 1.875)
+
+
+def pin_golden_split_e4m3():
+    """Hand-worked E4M3 split examples (tests/golden/nested_split_e4m3_examples.txt)."""
+    rows = []
+    with open(os.path.join(GOLDEN, "nested_split_e4m3_examples.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                b, h, lo, fast, full, elig = line.split()
+                rows.append((int(b, 16), int(h, 16), int(lo, 16), float(fast), float(full),
+                             int(elig)))
+    w = np.array([r[0] for r in rows], dtype=np.uint16)
+    res = identity_residual(w.size, 8)
+    hi = oracle.split(w, res, enc=oracle.E4M3)
+    lo = residual_stream_by_indexing(res, w.size)
+    assert (hi == np.array([r[1] for r in rows], dtype=np.uint8)).all()
+    assert (lo == np.array([r[2] for r in rows], dtype=np.uint8)).all()
+    fast = np.array([oracle.fast_value(oracle.E4M3, int(h)) for h in hi])
+    full = np.array([oracle.fp16_value(int(b)) for b in oracle.merge(hi, res, enc=oracle.E4M3)])
+    assert _same(fast, [r[3] for r in rows]).all()
+    assert _same(full, [r[4] for r in rows]).all()
+    for r in rows:
+        want = oracle.E4M3 if r[5] else oracle.E5M2
+        assert oracle.select_enc(np.array([r[0]], dtype=np.uint16)) == want
+
+
+def pin_e4m3_split_is_truncation():
+    """For every FP16 x with |x| < 1.875 the E4M3 fast value is x truncated toward
+    zero onto the grid {E4M3 values * 2^-8} (grid from torch's float8_e4m3fn), and
+    its upper byte is the E4M3 code of that value."""
+    res = identity_residual(ALL16.size, 12)
+    hi = oracle.split(ALL16, res, enc=oracle.E4M3)
+    keep = _eligible_e4m3(ALL16)
+    x = _fp16_lib(ALL16)[keep]
+    fast = np.array([oracle.fast_value(oracle.E4M3, int(h)) for h in hi[keep]])
+    assert _same(fast, _e4m3_fast_lib(hi[keep])).all()
+    grid = _e4m3_fast_lib(np.arange(256, dtype=np.uint8))
+    mags = np.unique(np.abs(grid[np.isfinite(grid)]))
+    idx = np.searchsorted(mags, np.abs(x), side="right") - 1
+    assert _same(fast, np.copysign(mags[idx], x)).all()
+
+
+def pin_e4m3_split_merge():
+    """E4M3 split then merge returns every word whose exponent MSB is zero; a word
+    with that bit set comes back with only that bit cleared (the field-keeping
+    reading); residual bytes stay below 128, and a set top bit in a residual byte
+    does not change the merged word."""
+    for res in (identity_residual(ALL16.size, 16),
+                random_residual(ALL16.size, 8, 1024, seed=7, fill=True)):
+        hi = oracle.split(ALL16, res, enc=oracle.E4M3)
+        lo = residual_stream_by_indexing(res, ALL16.size)
+        assert (lo < 128).all()
+        back = oracle.merge(hi, res, enc=oracle.E4M3)
+        msb = (ALL16 & 0x4000) != 0
+        assert (back[~msb] == ALL16[~msb]).all()
+        assert ((back[msb] ^ ALL16[msb]) == 0x4000).all()
+        c = 1 << res.log2_chunk
+        res.pool.reshape(-1, c)[res.slots] |= 0x80
+        assert (oracle.merge(hi, res, enc=oracle.E4M3) == back).all()
+
+
+def pin_select_enc():
+    """Per-layer choice: E4M3 for a single word exactly when |x| < 1.875 and x is
+    finite (numpy float16), and for a layer exactly when all its words are."""
+    got = np.array([oracle.select_enc(ALL16[i:i + 1]) for i in range(ALL16.size)])
+    assert (got == np.where(_eligible_e4m3(ALL16), oracle.E4M3, oracle.E5M2)).all()
+    rng = np.random.default_rng(21)
+    ok = (rng.standard_normal(4096) * 0.3).clip(-1.8, 1.8).astype(np.float16)
+    assert oracle.select_enc(ok) == oracle.E4M3
+    assert oracle.select_enc(np.zeros(0, dtype=np.float16)) == oracle.E4M3
+    for bad in (1.875, -1.875, 2.0, 100.0, np.inf, np.nan):
+        w = ok.copy()
+        w[rng.integers(w.size)] = bad
+        assert oracle.select_enc(w) == oracle.E5M2, bad
+
+
+def pin_linear_e4m3():
+    """E4M3 layers: full mode == numpy fp64 matmul of the FP16 weights, fast mode ==
+    matmul of torch-decoded E4M3 upper bytes times 2^-8, and fast == full over an
+    all-zero residual; dense, one-hot, grouped and FP8-activation forms."""
+    rng = np.random.default_rng(22)
+    for (m, n, k, log2c) in ((1, 1, 16, 8), (3, 5, 32, 8), (7, 33, 48, 9), (5, 17, 80, 8)):
+        w = _rand_fp16((n, k), rng, 0.4)
+        w[_fp16_lib(w) > 1.8] = 0
+        w[_fp16_lib(w) < -1.8] = 0
+        x = _rand_fp16((m, k), rng)
+        res = random_residual(n * k, log2c, -(-n * k // (1 << log2c)) + 3, seed=m + n,
+                              fill=True)
+        hi = oracle.split(w, res, enc=oracle.E4M3)
+        xd = _fp16_lib(x)
+        y = oracle.linear(oracle.FULL, x, hi, res, enc=oracle.E4M3)
+        assert np.allclose(y, xd @ _fp16_lib(w).T, rtol=1e-12, atol=1e-14)
+        y = oracle.linear(oracle.FAST, x, hi, None, enc=oracle.E4M3)
+        assert np.allclose(y, xd @ _e4m3_fast_lib(hi).T, rtol=1e-12, atol=1e-14)
+        assert (oracle.linear_rows(oracle.FAST, x, np.arange(m), hi, None, enc=oracle.E4M3)
+                == y).all()
+        zero = identity_residual(n * k, 8)
+        assert (oracle.linear(oracle.FULL, x, hi, zero, enc=oracle.E4M3) == y).all()
+    # one-hot rows read the weights back exactly
+    n, k = 9, 32
+    w = _rand_fp16((n, k), rng, 0.3)
+    res = identity_residual(n * k, 8)
+    hi = oracle.split(w, res, enc=oracle.E4M3)
+    eye = np.eye(k, dtype=np.float16).view(np.uint16)
+    assert (oracle.linear(oracle.FULL, eye, hi, res, enc=oracle.E4M3) == _fp16_lib(w).T).all()
+    assert (oracle.linear(oracle.FAST, eye, hi, None, enc=oracle.E4M3)
+            == _e4m3_fast_lib(hi).T).all()
+    # grouped: expert e's rows against expert e's weights
+    e, n, k = 3, 6, 32
+    w = _rand_fp16((e, n, k), rng, 0.3)
+    offsets = np.array([0, 2, 2, 5], dtype=np.int64)
+    x = _rand_fp16((5, k), rng)
+    res = random_residual(e * n * k, 8, 12, seed=23, fill=True)
+    hi = oracle.split(w, res, enc=oracle.E4M3)
+    for mode in (oracle.FULL, oracle.FAST):
+        y = oracle.linear_grouped(mode, x, offsets, hi, res if mode == oracle.FULL else None,
+                                  enc=oracle.E4M3)
+        for ex in range(e):
+            r0, r1 = offsets[ex], offsets[ex + 1]
+            wd = _fp16_lib(w[ex]) if mode == oracle.FULL else _e4m3_fast_lib(hi[ex])
+            assert np.allclose(y[r0:r1], _fp16_lib(x[r0:r1]) @ wd.T, rtol=1e-12, atol=1e-14)
+    # FP8 activations against E4M3 weights
+    m, n, k = 6, 14, 96
+    x = _rand_fp16((m, k), rng, 3.0)
+    w = _rand_fp16((n, k), rng, 0.3)
+    hi = oracle.split(w, identity_residual(n * k, 8), enc=oracle.E4M3)
+    xq, s = oracle.act_quant(x)
+    y = oracle.linear_fp8(xq, s, hi, enc=oracle.E4M3)
+    want = (_e4m3_lib(xq) * s[:, None]) @ _e4m3_fast_lib(hi).T
+    assert np.allclose(y, want, rtol=1e-12, atol=1e-14)
+
+
 ALL_PINS = [
     pin_fp16_decode, pin_e5m2_decode, pin_e4m3_decode, pin_golden_split,
     pin_split_is_truncation, pin_split_merge_identity, pin_residual_addressing,
     pin_linear_small, pin_linear_one_hot, pin_fast_equals_full_with_zero_residual,
     pin_grouped_is_loop_of_dense, pin_linear_rows, pin_e4m3_rounding_exhaustive,
-    pin_act_scale, pin_linear_fp8,
+    pin_act_scale, pin_linear_fp8, pin_golden_split_e4m3, pin_e4m3_split_is_truncation,
+    pin_e4m3_split_merge, pin_select_enc, pin_linear_e4m3,
 ]

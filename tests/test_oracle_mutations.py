@@ -19,10 +19,10 @@ SRC = os.path.join(os.path.dirname(oracle.__file__), "dps_oracle.c")
 
 # (id, original text, mutated text)
 MUTATIONS = [
-    ("split_wrong_shift", "hi[i] = (uint8_t)(w[i] / 256);", "hi[i] = (uint8_t)(w[i] / 128);"),
-    ("residual_lost", "(uint8_t)(w[i] % 256);", "(uint8_t)(w[i] % 128);"),
-    ("merge_swapped", "w_out[i] = (uint16_t)((uint16_t)hi[i] * 256 + pool[p]);",
-     "w_out[i] = (uint16_t)((uint16_t)pool[p] * 256 + hi[i]);"),
+    ("split_wrong_shift", "*hi = (uint8_t)(s * 128 + e * 4 + m / 256);",
+     "*hi = (uint8_t)(s * 128 + e * 4 + m / 512);"),
+    ("residual_lost", "*lo = (uint8_t)(m % 256);", "*lo = (uint8_t)(m % 128);"),
+    ("merge_drops_residual_bit", "e * 1024 + mh * 256 + lo);", "e * 1024 + mh * 256 + lo / 2);"),
     ("e5m2_wrong_bias", "return sign * ldexp(1.0 + (double)m / 4.0, e - 15);",
      "return sign * ldexp(1.0 + (double)m / 4.0, e - 16);"),
     ("e5m2_subnormal_dropped", "return sign * ldexp((double)m / 4.0, -14);",
@@ -35,8 +35,8 @@ MUTATIONS = [
     ("weight_transposed", "int64_t i = w_base + c * k + kk;",
      "int64_t i = w_base + (kk % (c + 1)) * k + c % k;"),
     ("expert_base_dropped", "int64_t w_base = e * n * k;", "int64_t w_base = 0;"),
-    ("fast_rounds_up", "wrow[kk] = oracle_e5m2_value(hi[i]);",
-     "wrow[kk] = oracle_e5m2_value((uint8_t)(hi[i] + 1));"),
+    ("fast_rounds_up", "wrow[kk] = oracle_fast_value(enc, hi[i]);",
+     "wrow[kk] = oracle_fast_value(enc, (uint8_t)(hi[i] + 1));"),
     ("x_reversed", "acc += oracle_fp16_value(x[r * k + kk]) * wrow[kk];",
      "acc += oracle_fp16_value(x[r * k + (k - 1 - kk)]) * wrow[kk];"),
     ("tie_to_odd", "(c & 1) == 0 && (best & 1) == 1", "(c & 1) == 1 && (best & 1) == 0"),
@@ -44,6 +44,22 @@ MUTATIONS = [
     ("fp8_scale_dropped", "y[r * n + c] = scale[r] * acc;", "y[r * n + c] = acc;"),
     ("e4m3_bias", "return sign * ldexp(1.0 + (double)m / 8.0, e - 7);",
      "return sign * ldexp(1.0 + (double)m / 8.0, e - 8);"),
+    # E4M3 nesting and the encoding choice
+    ("e4m3_split_exponent", "*hi = (uint8_t)(s * 128 + (e % 16) * 8 + m / 128);",
+     "*hi = (uint8_t)(s * 128 + (e / 2) * 8 + m / 128);"),
+    ("e4m3_residual_width", "*lo = (uint8_t)(m % 128);", "*lo = (uint8_t)(m % 64);"),
+    ("e4m3_merge_reads_top_bit", "mh * 128 + lo % 128);", "mh * 128 + lo);"),
+    ("e4m3_merge_exponent", "int e = (hi / 8) % 16, mh = hi % 8;",
+     "int e = (hi / 8) % 16 + 1, mh = hi % 8;"),
+    ("e4m3_fast_scale", "return ldexp(oracle_e4m3_value(hi), -8);",
+     "return ldexp(oracle_e4m3_value(hi), -7);"),
+    ("select_ignores_nan", "if (e >= 16 || isnan(oracle_e4m3_value(hi)))", "if (e >= 16)"),
+    ("select_ignores_msb", "if (e >= 16 || isnan(oracle_e4m3_value(hi)))",
+     "if (e >= 17 || isnan(oracle_e4m3_value(hi)))"),
+    ("full_ignores_enc", "oracle_fp16_value(unnest_word(enc, hi[i], p < 0 ? 0 : pool[p]))",
+     "oracle_fp16_value(unnest_word(0, hi[i], p < 0 ? 0 : pool[p]))"),
+    ("fp8_ignores_enc", "oracle_fast_value(enc, hi[c * k + kk]);",
+     "oracle_e5m2_value(hi[c * k + kk]);"),
 ]
 
 
