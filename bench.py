@@ -2,8 +2,9 @@
 
 Workload (the metric's configuration): the hidden-4096 decode layer set --
 QKV 4096->6144, O 4096->4096, gate+up 4096->2x14336, down 14336->4096 --
-FP16 weights ~ N(0, 0.02) split into an E5M2 upper-byte plane and a residual
-plane in 2 MiB chunks, activations ~ N(0, 1), token batch M in
+FP16 weights ~ N(0, 0.02) split into an E5M2 upper-byte plane (--enc e4m3:
+the E4M3 nesting, which these weights qualify for) and a residual plane in
+2 MiB chunks, activations ~ N(0, 1), token batch M in
 {1, 8, 32, 128, 256}.  One step runs every layer at every M in fast mode and
 in full mode (40 nested-linear calls), captured once per weight copy as a
 HIP graph (the paper replays one captured graph per mode and batch size).
@@ -49,6 +50,8 @@ def parse():
                     help="LAYER:M:MODE -- run only that call (for rocprofv3) and a copy "
                          "kernel of known size, then exit")
     ap.add_argument("--probe-reps", type=int, default=20)
+    ap.add_argument("--enc", choices=("e5m2", "e4m3"), default="e5m2",
+                    help="nested encoding of every layer")
     return ap.parse_args()
 
 
@@ -74,8 +77,9 @@ def main():
     stream = torch.cuda.Stream()
 
     layers = workloads.H4096_SET
+    enc = dps.ENC_E4M3 if args.enc == "e4m3" else dps.ENC_E5M2
     if args.probe_call:
-        probe(args, torch, dps, workloads, layers, dev, stream)
+        probe(args, torch, dps, workloads, layers, dev, stream, enc)
         return
     ms = workloads.DECODE_M
     modes = (("fast", dps.MODE_FAST), ("full", dps.MODE_FULL))
@@ -88,7 +92,7 @@ def main():
             for li, (name, n, k) in enumerate(layers):
                 w = workloads.weight_fp16(n, k, seed=1000 * c + li, device=dev)
                 res = dps.make_residual(n * k, LOG2_CHUNK, dev)
-                nws.append(dps.split(w, res))
+                nws.append(dps.split(w, res, enc=enc))
                 del w
             copies.append(nws)
         xs = {m: {k: workloads.activations_fp16(m, k, seed=m * 7 + k, device=dev)
@@ -209,7 +213,7 @@ def main():
         roof = {"bound": "mfma", "achieved": round(flops / t_launch / 1e12, 1),
                 "peak": MFMA_F16_TFLOPS, "unit": "TFLOP/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = measured_traffic("%s:%d:%s" % (dom["layer"], dm, dom["mode"]))
+    roof["traffic"] = measured_traffic("%s:%d:%s" % (dom["layer"], dm, dom["mode"]), args.enc)
     roof["kernel"] = ("%s layer %dx%d, M=%d, %s mode" % (dom["layer"], dn, dk, dm, dom["mode"]))
     roof["probe_call"] = "%s:%d:%s" % (dom["layer"], dm, dom["mode"])
     roof["us_per_launch"] = round(t_launch * 1e6, 2)
@@ -240,7 +244,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f16",
         "data": "synthetic",
-        "config": {"workload": "decode_h4096",
+        "config": {"workload": "decode_h4096", "encoding": args.enc,
                    "layers": {name: [n, k] for name, n, k in layers},
                    "M": list(ms), "modes": ["fast", "full"], "chunk_bytes": 1 << LOG2_CHUNK,
                    "weight_copies_rotated": COPIES,
@@ -253,7 +257,7 @@ def main():
     print(json.dumps(out), flush=True)
 
 
-def measured_traffic(probe_call):
+def measured_traffic(probe_call, enc):
     """HBM bytes per launch of the dominant kernel from the committed rocprofv3
     counter record (profiles/*_traffic.md), or None when no record matches this
     call or the kernel sources changed since the counters were taken."""
@@ -272,12 +276,13 @@ def measured_traffic(probe_call):
                 line = line.strip()
                 if line.startswith("{") and "csrc_sha256" in line:
                     rec = json.loads(line)
-                    if rec.get("probe_call") == probe_call and rec.get("csrc_sha256") == digest:
+                    if (rec.get("probe_call") == probe_call and rec.get("csrc_sha256") == digest
+                            and rec.get("encoding", "e5m2") == enc):
                         return rec["traffic_bytes_per_launch"]
     return None
 
 
-def probe(args, torch, dps, workloads, layers, dev, stream):
+def probe(args, torch, dps, workloads, layers, dev, stream, enc):
     """One call of the decode set, launched back to back on rotating weight
     copies, then a device-to-device copy of 256 MiB (a kernel of known HBM
     traffic, to calibrate rocprofv3's FETCH_SIZE / WRITE_SIZE)."""
@@ -290,7 +295,7 @@ def probe(args, torch, dps, workloads, layers, dev, stream):
         nws = []
         for c in range(COPIES):
             w = workloads.weight_fp16(n, k, seed=1000 * c + li, device=dev)
-            nws.append(dps.split(w, dps.make_residual(n * k, LOG2_CHUNK, dev)))
+            nws.append(dps.split(w, dps.make_residual(n * k, LOG2_CHUNK, dev), enc=enc))
             del w
         x = workloads.activations_fp16(m, k, seed=m * 7 + k, device=dev)
         y = torch.empty((m, n), dtype=torch.float16, device=dev)

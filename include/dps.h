@@ -4,9 +4,9 @@
  *
  * The method (Sec. IV of the paper) keeps every FP16 weight as two bytes held
  * in two places:
- *   - the upper byte -- sign, all five exponent bits and the two leading
- *     mantissa bits, i.e. the FP16 value truncated to FP8 E5M2 -- in a
- *     persistent region (Sec. IV-B "Persistent Region");
+ *   - the upper byte -- an FP8 number, the FP16 value truncated to E5M2 or,
+ *     for layers of small range, to E4M3 scaled by 2^8 -- in a persistent
+ *     region (Sec. IV-B "Persistent Region");
  *   - the lower byte, the residual, in a shared region whose physical memory
  *     is made of relocatable units that may instead hold paged KV-cache
  *     blocks (Sec. IV-B "Shared Region"; Sec. IV-C, restoration paragraph).
@@ -55,20 +55,28 @@ typedef enum {
  * the precision switch"). */
 typedef enum {
     DPS_MODE_FULL = 0, /* FP16 rebuilt from upper byte + residual byte       */
-    DPS_MODE_FAST = 1  /* FP8 E5M2 upper byte only; residual never read      */
+    DPS_MODE_FAST = 1  /* FP8 upper byte only; residual never read           */
 } dps_mode;
 
-/* Nested encodings (Sec. IV-B "Persistent Region"): E5M2 keeps all five
- * exponent bits.  The E4M3 variant for small-range layers is not built. */
-enum { DPS_ENC_E5M2 = 0 };
+/* Nested encodings (Sec. IV-B "Persistent Region"), chosen per layer
+ * (Sec. IV-C, "Dual-mode serving" paragraph).  FP16 word w = sign s,
+ * exponent e (5 bits), mantissa m (10 bits):
+ *   DPS_ENC_E5M2: upper byte = s | e | m[9:8]   (w >> 8, E5M2 by truncation),
+ *                 residual byte = m[7:0];  fast-mode weight = E5M2(upper).
+ *   DPS_ENC_E4M3: upper byte = s | e[3:0] | m[9:7], residual byte = m[6:0]
+ *                 (top bit 0 when written, ignored when read); exact only
+ *                 when e's MSB is 0.  Fast-mode weight = OCP E4M3(upper) *
+ *                 2^-8, a number only when |w| < 1.875.  dps_select_enc
+ *                 says whether a whole layer qualifies. */
+enum { DPS_ENC_E5M2 = 0, DPS_ENC_E4M3 = 1 };
 
 /* Activation handling, `flags` argument of the linear calls.
  *   DPS_ACT_FP16: activations stay FP16; weights enter the FP16 matrix cores
- *     (fast mode: the E5M2 byte is the upper byte of an exact FP16 word).
+ *     (fast mode: the fast-mode weight is an exact FP16 word).
  *   DPS_ACT_FP8_ROWSCALE (fast mode only): each activation row is first
  *     quantized to OCP FP8 E4M3 with its own power-of-two scale (see
  *     dps_quant_rows_e4m3) and the product runs on the FP8 matrix cores with
- *     the weights' E5M2 byte as the second operand. */
+ *     the weights' upper byte (E5M2 or E4M3) as the second operand. */
 enum { DPS_ACT_FP16 = 0u, DPS_ACT_FP8_ROWSCALE = 1u };
 
 /* Residual plane of one weight tensor (Sec. IV-B "Shared Region": physical
@@ -100,7 +108,8 @@ typedef struct {
  * the upper-byte plane `hi` and the residual stream.
  *   hi   device uint8[experts][n][k], 16-byte aligned.
  *   k    multiple of 16, > 0.   n > 0.   experts >= 1.
- *   enc  DPS_ENC_E5M2. */
+ *   enc  DPS_ENC_E5M2 or DPS_ENC_E4M3: the encoding hi and the residual were
+ *        split with. */
 typedef struct {
     const uint8_t *hi;
     dps_residual res;
@@ -110,20 +119,34 @@ typedef struct {
     int32_t enc;
 } dps_weight;
 
+/* Per-layer encoding choice (Sec. IV-C, "Dual-mode serving" paragraph: E5M2
+ * for layers E4M3 cannot express): *enc_out = DPS_ENC_E4M3 if every word of
+ * w has |w| < 1.875 (exponent MSB zero and E4M3 part a number; NaN and
+ * infinities do not qualify), else DPS_ENC_E5M2.  numel == 0 gives E4M3.
+ *   w        device uint16 (FP16 bit patterns) [numel], 16-byte aligned.
+ *   enc_out  device int32, written by the enqueued work (read it after
+ *            synchronizing the stream). */
+dps_status dps_select_enc(const uint16_t *w, int64_t numel, int32_t *enc_out, void *stream);
+
 /* Split FP16 weights into the nested pair (Sec. IV-A "Dynamic Networks and a
- * Nested Model"; Sec. IV-B "Persistent Region"): hi[i] = w[i] >> 8 (the E5M2
- * truncation), residual byte i = w[i] & 0xFF written through the chunk table.
+ * Nested Model"; Sec. IV-B "Persistent Region"): hi[i] and residual byte i of
+ * w[i] under encoding `enc` (see the encoding table above), the residual
+ * written through the chunk table.  E4M3 on a word whose exponent MSB is set
+ * keeps the listed fields all the same and loses that bit.
+ *   enc    DPS_ENC_E5M2 or DPS_ENC_E4M3.
  *   w      device uint16 (FP16 bit patterns) [numel], 16-byte aligned.
  *   hi     device uint8[numel], 16-byte aligned.
  *   res    host pointer to the residual descriptor (its pool is written).
  * numel == 0 is a no-op.  Bit-exact. */
-dps_status dps_split(const uint16_t *w, int64_t numel, uint8_t *hi,
+dps_status dps_split(int enc, const uint16_t *w, int64_t numel, uint8_t *hi,
                      const dps_residual *res, void *stream);
 
-/* Rebuild the original FP16 words (Sec. IV-C "Overall concept": full mode
- * reconstructs the original FP16 values): w_out[i] = hi[i] << 8 | residual
- * byte i.  Same layouts as dps_split.  Bit-exact. */
-dps_status dps_merge(const uint8_t *hi, const dps_residual *res, int64_t numel,
+/* Rebuild the FP16 words (Sec. IV-C "Overall concept": full mode
+ * reconstructs the original FP16 values) from hi and the residual bytes
+ * under encoding `enc`: E5M2 w = hi << 8 | residual; E4M3 w = sign | 0 |
+ * hi's seven low bits | the residual byte's seven low bits.  Same layouts as
+ * dps_split.  Bit-exact. */
+dps_status dps_merge(int enc, const uint8_t *hi, const dps_residual *res, int64_t numel,
                      uint16_t *w_out, void *stream);
 
 /* Per-row FP8 quantization of activations for fast-mode prefill (this
@@ -147,7 +170,8 @@ size_t dps_workspace_bytes(int mode, uint32_t flags, int64_t rows, int64_t n,
 
 /* Nested linear layer, dense (Sec. IV-C, GroupedGEMM paragraph, dense case):
  *   full mode: Y = X . merge(hi, residual)^T   (exact FP16 weights)
- *   fast mode: Y = X . E5M2(hi)^T              (residual not read)
+ *   fast mode: Y = X . fast(hi)^T              (residual not read), fast =
+ *              E5M2(hi) or E4M3(hi) * 2^-8 per w->enc
  * fp32 accumulation, Y rounded to FP16 (round to nearest even).
  *   mode   DPS_MODE_FULL or DPS_MODE_FAST.
  *   flags  DPS_ACT_FP16, or DPS_ACT_FP8_ROWSCALE with DPS_MODE_FAST.

@@ -97,7 +97,8 @@ dps_status launched(hipError_t e)
 dps_status check_weight(const dps_weight *w, int mode)
 {
     REQUIRE(w != nullptr, DPS_ERR_INVALID_ARG, "weight descriptor is NULL");
-    REQUIRE(w->enc == DPS_ENC_E5M2, DPS_ERR_UNSUPPORTED, "only the E5M2 nested encoding is built");
+    REQUIRE(w->enc == DPS_ENC_E5M2 || w->enc == DPS_ENC_E4M3, DPS_ERR_INVALID_ARG,
+            "unknown nested encoding");
     REQUIRE(w->experts >= 1 && w->experts <= 65535, DPS_ERR_INVALID_ARG,
             "experts must be in 1..65535");
     REQUIRE(w->n > 0, DPS_ERR_INVALID_ARG, "n must be positive");
@@ -136,19 +137,20 @@ LinearPlan plan_linear(int mode, uint32_t flags, int64_t rows, int64_t n, int64_
         p.splits = (int)cdiv(k, p.ksplit);
         p.ws_quant = align256(rows * k) + align256(rows * 4);
     } else if (rows_per_expert <= 1 || (rows_per_expert <= 4 && n * k <= (int64_t(1) << 25))) {
-        // The decode kernel (per-wave LDS rings of 256-byte rows) serves one
-        // token per expert, and up to four on layers of at most 2^25 weights.
-        // Everywhere else the wide-row GEMM with 32-token tiles is as fast or
-        // faster on MI355X (8 tokens, hidden-4096 set, both modes: 182 us
-        // against 224 us; the full-mode 28672 x 4096 layer 50 us against 68).
+        // The decode kernel serves one token per expert, and up to four on
+        // layers of at most 2^25 weights.  Everywhere else the wide-row GEMM
+        // with 32-token tiles is as fast or faster on MI355X (8 tokens,
+        // hidden-4096 set, both modes: 182 us against 224 us; the full-mode
+        // 28672 x 4096 layer 50 us against 68).
         p.kind = KIND_SKINNY;
-        // measured on MI355X: up to 8 tokens, the weight stream through shallow
-        // per-wave LDS rings (two blocks per CU); above that, registers with
-        // 16 rows per wave up to 16 tokens and 32 rows (half batches) beyond
+        // measured on MI355X: up to 8 tokens, the weight stream through
+        // per-wave LDS rings (two blocks per CU); above that (grouped passes
+        // of 64 rows), registers with 16 rows per wave up to 16 tokens and 32
+        // rows (half batches) beyond
         const int64_t xr = skinny_pass_rows(rows, grouped);
-        p.variant = xr <= 16 ? 1 : 2;
-        if (xr <= 8 && skinny_max_ksplit(SKINNY_RING_HALF, mode, xr) > 0)
-            p.variant = SKINNY_RING_HALF;
+        p.variant = xr <= 16 ? 0 : 1;
+        if (xr <= 8 && skinny_max_ksplit(SKINNY_RING, mode, xr) > 0)
+            p.variant = SKINNY_RING;
         const int64_t kpb = skinny_k_per_batch(p.variant);
         // the block's X slice [pass rows][ksplit + 8] FP16 must fit its LDS share
         const int64_t kmax = skinny_max_ksplit(p.variant, mode, xr);
@@ -164,10 +166,10 @@ LinearPlan plan_linear(int mode, uint32_t flags, int64_t rows, int64_t n, int64_
         p.kind = KIND_GEMM_F16;
         // One plan for both modes, so that fast mode equals full mode over a
         // zero residual bit for bit (same tiles, same K ranges, same order).
-        // Every FP16 shape above 16 tokens per expert takes the wide-row
-        // GEMM (on MI355X it beat the register-staged and eight-wave kernels
-        // at 128 and 256 tokens and matched them at 2048), with a 32-, 64- or
-        // 128-token tile so that short calls stage no padding rows.  K is split
+        // Every other FP16 shape takes the wide-row GEMM (on MI355X it beat
+        // register-staged and eight-wave FP16 kernels at 128 and 256 tokens
+        // and matched them at 2048), with a 32-, 64- or 128-token tile so
+        // that short calls stage no padding rows.  K is split
         // so that about one block of eight waves per CU is resident (the split
         // count rounds down); each range keeps >= 1024 elements.
         // four dedicated DMA waves pay off from 64-token tiles on (MI355X:
@@ -205,10 +207,24 @@ DPS_EXPORT const char *dps_status_str(dps_status s)
 
 DPS_EXPORT const char *dps_last_error(void) { return g_err; }
 
-DPS_EXPORT dps_status dps_split(const uint16_t *w, int64_t numel, uint8_t *hi,
+DPS_EXPORT dps_status dps_select_enc(const uint16_t *w, int64_t numel, int32_t *enc_out,
+                                     void *stream)
+{
+    g_err[0] = 0;
+    REQUIRE(numel >= 0, DPS_ERR_INVALID_ARG, "numel is negative");
+    REQUIRE(enc_out != nullptr, DPS_ERR_INVALID_ARG, "enc_out is NULL");
+    REQUIRE(aligned(enc_out, 4), DPS_ERR_ALIGNMENT, "enc_out is not 4-byte aligned");
+    REQUIRE(numel == 0 || w != nullptr, DPS_ERR_INVALID_ARG, "w is NULL");
+    REQUIRE(aligned(w, 16), DPS_ERR_ALIGNMENT, "w is not 16-byte aligned");
+    return launched(dps::launch_select_enc(w, numel, enc_out, (hipStream_t)stream));
+}
+
+DPS_EXPORT dps_status dps_split(int enc, const uint16_t *w, int64_t numel, uint8_t *hi,
                                 const dps_residual *res, void *stream)
 {
     g_err[0] = 0;
+    REQUIRE(enc == DPS_ENC_E5M2 || enc == DPS_ENC_E4M3, DPS_ERR_INVALID_ARG,
+            "unknown nested encoding");
     REQUIRE(numel >= 0, DPS_ERR_INVALID_ARG, "numel is negative");
     if (numel == 0)
         return DPS_OK;
@@ -217,13 +233,15 @@ DPS_EXPORT dps_status dps_split(const uint16_t *w, int64_t numel, uint8_t *hi,
     dps_status s = check_residual(res, numel);
     if (s != DPS_OK)
         return s;
-    return launched(dps::launch_split(w, numel, hi, view_of(res), (hipStream_t)stream));
+    return launched(dps::launch_split(enc, w, numel, hi, view_of(res), (hipStream_t)stream));
 }
 
-DPS_EXPORT dps_status dps_merge(const uint8_t *hi, const dps_residual *res, int64_t numel,
-                                uint16_t *w_out, void *stream)
+DPS_EXPORT dps_status dps_merge(int enc, const uint8_t *hi, const dps_residual *res,
+                                int64_t numel, uint16_t *w_out, void *stream)
 {
     g_err[0] = 0;
+    REQUIRE(enc == DPS_ENC_E5M2 || enc == DPS_ENC_E4M3, DPS_ERR_INVALID_ARG,
+            "unknown nested encoding");
     REQUIRE(numel >= 0, DPS_ERR_INVALID_ARG, "numel is negative");
     if (numel == 0)
         return DPS_OK;
@@ -233,7 +251,7 @@ DPS_EXPORT dps_status dps_merge(const uint8_t *hi, const dps_residual *res, int6
     dps_status s = check_residual(res, numel);
     if (s != DPS_OK)
         return s;
-    return launched(dps::launch_merge(hi, view_of(res), numel, w_out, (hipStream_t)stream));
+    return launched(dps::launch_merge(enc, hi, view_of(res), numel, w_out, (hipStream_t)stream));
 }
 
 DPS_EXPORT dps_status dps_quant_rows_e4m3(const uint16_t *x, int64_t m, int64_t k, uint8_t *xq,
@@ -284,6 +302,7 @@ dps_status run_linear(int mode, uint32_t flags, const uint16_t *x, const int32_t
     float *partial = plan.splits > 1 ? static_cast<float *>(ws) : nullptr;
     dps::LinearProblem p;
     p.mode = mode;
+    p.enc = w->enc;
     p.x = x;
     p.offsets = offsets;
     p.rows = rows;
@@ -301,7 +320,7 @@ dps_status run_linear(int mode, uint32_t flags, const uint16_t *x, const int32_t
         st = launched(dps::launch_quant_rows(x, rows, w->k, xq, scale, stream));
         if (st != DPS_OK)
             return st;
-        st = launched(dps::launch_gemm_fp8(xq, scale, rows, w->n, w->k, w->hi, y, plan, partial,
+        st = launched(dps::launch_gemm_fp8(w->enc, xq, scale, rows, w->n, w->k, w->hi, y, plan, partial,
                                            stream));
     } else if (plan.kind == dps::KIND_SKINNY) {
         st = launched(dps::launch_skinny(p, plan, partial, stream));

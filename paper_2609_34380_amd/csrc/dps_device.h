@@ -6,11 +6,16 @@
 // kernels make is a 16-byte vector at a 16-byte-aligned logical offset, and
 // C >= 16, so a vector never straddles two chunks.
 //
-// Merge (Sec. IV-C "Overall concept"): an FP16 word is (upper byte << 8) |
-// residual byte.  The kernels build FP16 operands in registers with one byte
-// permute per two weights; fast mode feeds zero residual bytes through the
-// same permute, so a fast-mode product is bit-identical to a full-mode
-// product whose residual bytes are all zero.
+// Merge (Sec. IV-C "Overall concept"; nestings of Sec. IV-B "Persistent
+// Region"): with the E5M2 nesting an FP16 word is (upper byte << 8) |
+// residual byte; with the E4M3 nesting the upper byte holds the sign, the
+// four low exponent bits and three mantissa bits, the exponent MSB is zero
+// and the residual byte's seven low bits are the rest of the mantissa.  The
+// kernels build FP16 operands in registers with one byte permute per two
+// weights (plus three bit operations for E4M3).  The fast-mode weight is the
+// FP16 word with its residual bits cleared -- E5M2(hi), or E4M3(hi) * 2^-8 --
+// so a fast-mode product is bit-identical to a full-mode product whose
+// residual bytes are all zero.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -25,6 +30,7 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef int32_t i32x8 __attribute__((ext_vector_type(8)));
 
 enum { MODE_FULL = 0, MODE_FAST = 1 };
+enum { ENC_E5M2 = 0, ENC_E4M3 = 1 };
 
 // Kernel-argument form of a residual descriptor.
 struct ResidualView {
@@ -111,20 +117,67 @@ __device__ __forceinline__ u32x4 load_lo_lookup(const ResidualView &r, int64_t l
     return v;
 }
 
+// Two E4M3-nested words t = (hi << 8 | lo) per 16-bit half -> FP16 words:
+// the sign stays at bit 15, the seven bits below it move down one place
+// (the exponent MSB becomes 0) and the residual keeps its seven low bits.
+__device__ __forceinline__ uint32_t e4m3_words(uint32_t t)
+{
+    return (t & 0x807F807Fu) | ((t >> 1) & 0x3F803F80u);
+}
+
 // Four FP16 words from four upper bytes (hi4) and four residual bytes (lo4):
-// word j = hi byte j << 8 | lo byte j.  v_perm_b32 picks bytes 0-3 from its
-// second source and 4-7 from its first.
+// first word j = hi byte j << 8 | lo byte j (v_perm_b32 picks bytes 0-3 from
+// its second source and 4-7 from its first), then the E4M3 field move.
+template <int ENC>
 __device__ __forceinline__ u32x2 merge4(uint32_t hi4, uint32_t lo4)
 {
-    return u32x2{__builtin_amdgcn_perm(hi4, lo4, 0x05010400u),
-                 __builtin_amdgcn_perm(hi4, lo4, 0x07030602u)};
+    u32x2 t = {__builtin_amdgcn_perm(hi4, lo4, 0x05010400u),
+               __builtin_amdgcn_perm(hi4, lo4, 0x07030602u)};
+    if (ENC == ENC_E4M3) {
+        t.x = e4m3_words(t.x);
+        t.y = e4m3_words(t.y);
+    }
+    return t;
 }
 
 // Eight FP16 operands (one MFMA f16 operand) from 8 upper + 8 residual bytes.
+template <int ENC>
 __device__ __forceinline__ half8 merge8(uint32_t h0, uint32_t h1, uint32_t l0, uint32_t l1)
 {
-    const u32x2 p = merge4(h0, l0);
-    const u32x2 q = merge4(h1, l1);
+    const u32x2 p = merge4<ENC>(h0, l0);
+    const u32x2 q = merge4<ENC>(h1, l1);
+    const u32x4 w = {p.x, p.y, q.x, q.y};
+    return __builtin_bit_cast(half8, w);
+}
+
+typedef _Float16 half2v __attribute__((ext_vector_type(2)));
+
+// Fast-mode FP16 words of four upper bytes.  E5M2: the byte is the word's
+// upper byte (the merge with zero residual bytes).  E4M3: gfx950's packed
+// E4M3 -> FP16 conversion with scale 2^-8, one instruction per two words; it
+// is exact for every E4M3 number (E4M3 subnormals land on FP16 subnormals)
+// and gives the same words as the merge with zero residual bytes, except
+// for the E4M3 NaN pattern, which no layer chosen for E4M3 holds.
+template <int ENC>
+__device__ __forceinline__ u32x2 fast4(uint32_t hi4)
+{
+    if (ENC == ENC_E4M3) {
+        const half2v a = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(hi4, 0.00390625f, false);
+        const half2v b = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(hi4, 0.00390625f, true);
+        return u32x2{__builtin_bit_cast(uint32_t, a), __builtin_bit_cast(uint32_t, b)};
+    }
+    return merge4<ENC>(hi4, 0u);
+}
+
+// One MFMA f16 operand (eight weights) of the mode: merged from upper and
+// residual bytes (full) or from the upper bytes alone (fast).
+template <int MODE, int ENC>
+__device__ __forceinline__ half8 weight8(uint32_t h0, uint32_t h1, uint32_t l0, uint32_t l1)
+{
+    if (MODE == MODE_FULL)
+        return merge8<ENC>(h0, h1, l0, l1);
+    const u32x2 p = fast4<ENC>(h0);
+    const u32x2 q = fast4<ENC>(h1);
     const u32x4 w = {p.x, p.y, q.x, q.y};
     return __builtin_bit_cast(half8, w);
 }
@@ -142,11 +195,15 @@ __device__ __forceinline__ f32x4 mfma16x16x32(half8 a, half8 b, f32x4 c)
     return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
 }
 
-// D += A.B on a 16x16 fp32 tile, K = 128 FP8: A in E5M2 (format 1), B in
-// OCP E4M3 (format 0); 32 bytes of each operand per lane.
-__device__ __forceinline__ f32x4 mfma16x16x128_bf8_fp8(i32x8 a, i32x8 b, f32x4 c)
+// D += A.B on a 16x16 fp32 tile, K = 128 FP8: A (the upper bytes) in E5M2
+// (format 1) or OCP E4M3 (format 0), B in OCP E4M3; 32 bytes of each operand
+// per lane.  With both scale operands zero the compiler emits the unscaled
+// v_mfma_f32_16x16x128_f8f6f4 (cbsz selects the A format).
+template <int ENC>
+__device__ __forceinline__ f32x4 mfma16x16x128_fp8(i32x8 a, i32x8 b, f32x4 c)
 {
-    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 1, 0, 0, 0, 0, 0);
+    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, ENC == ENC_E5M2 ? 1 : 0, 0,
+                                                             0, 0, 0, 0);
 }
 
 }  // namespace dps

@@ -1,5 +1,6 @@
-// dps_elementwise.hip -- split, merge, FP8 row quantization and the split-K
-// reduction (gfx950).  All are bandwidth-bound streams of 16-byte vectors.
+// dps_elementwise.hip -- split, merge, the per-layer encoding choice, FP8 row
+// quantization and the split-K reduction (gfx950).  All are bandwidth-bound
+// streams of 16-byte vectors.
 #include "dps_internal.h"
 
 namespace dps {
@@ -18,6 +19,22 @@ __device__ __forceinline__ uint32_t low_bytes(uint32_t d0, uint32_t d1)
     return __builtin_amdgcn_perm(d1, d0, 0x06040200u);
 }
 
+// Two FP16 words per dword -> E4M3-nested words (per 16-bit half: upper byte
+// = sign | exponent bits 3..0 | mantissa bits 9..7, low byte = mantissa bits
+// 6..0).  The inverse of e4m3_words; bit 14 (the exponent MSB) is dropped.
+__device__ __forceinline__ uint32_t e4m3_nest(uint32_t d)
+{
+    return (d & 0x807F807Fu) | ((d << 1) & 0x7F007F00u);
+}
+
+// FP16 magnitude bits below 0x3F80 (1.875): the exponent MSB is zero and the
+// E4M3 part is a number (0x3F80 and up would give the E4M3 NaN pattern or
+// lose the exponent MSB; infinities and NaNs are above).
+__device__ __forceinline__ bool e4m3_fits(uint32_t word16)
+{
+    return (word16 & 0x7FFFu) < 0x3F80u;
+}
+
 int64_t grid_for(int64_t items)
 {
     int64_t blocks = (items + kThreads - 1) / kThreads;
@@ -28,7 +45,10 @@ int64_t grid_for(int64_t items)
     return blocks;
 }
 
-// Sec. IV-A / IV-B: hi = w >> 8 (E5M2 by truncation), residual = w & 0xFF.
+// Sec. IV-A / IV-B "Persistent Region": E5M2 keeps hi = w >> 8 (truncation)
+// and residual = w & 0xFF; E4M3 keeps sign, exponent bits 3..0 and mantissa
+// bits 9..7 in hi and mantissa bits 6..0 in the residual byte.
+template <int ENC>
 __global__ __launch_bounds__(kThreads) void split_kernel(const uint16_t *__restrict__ w,
                                                          int64_t numel, uint8_t *__restrict__ hi,
                                                          ResidualView res)
@@ -38,8 +58,12 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const uint16_t *__restr
     const int64_t stride = (int64_t)gridDim.x * kThreads;
     for (int64_t v = (int64_t)blockIdx.x * kThreads + threadIdx.x; v < nvec; v += stride) {
         const int64_t i0 = v << 4;
-        const u32x4 a = load16(w + i0);
-        const u32x4 b = load16(w + i0 + 8);
+        u32x4 a = load16(w + i0);
+        u32x4 b = load16(w + i0 + 8);
+        if (ENC == ENC_E4M3) {
+            a = u32x4{e4m3_nest(a.x), e4m3_nest(a.y), e4m3_nest(a.z), e4m3_nest(a.w)};
+            b = u32x4{e4m3_nest(b.x), e4m3_nest(b.y), e4m3_nest(b.z), e4m3_nest(b.w)};
+        }
         u32x4 h, l;
         h.x = high_bytes(a.x, a.y);
         h.y = high_bytes(a.z, a.w);
@@ -57,7 +81,7 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const uint16_t *__restr
     // ragged tail (< 16 words), one thread
     if (blockIdx.x == 0 && threadIdx.x == 0) {
         for (int64_t i = nvec << 4; i < numel; ++i) {
-            const uint16_t word = w[i];
+            const uint16_t word = ENC == ENC_E4M3 ? (uint16_t)e4m3_nest(w[i]) : w[i];
             hi[i] = (uint8_t)(word >> 8);
             const int64_t off = residual_offset(res, i);
             if (off >= 0)
@@ -66,7 +90,9 @@ __global__ __launch_bounds__(kThreads) void split_kernel(const uint16_t *__restr
     }
 }
 
-// Sec. IV-C "Overall concept": original FP16 = hi << 8 | residual byte.
+// Sec. IV-C "Overall concept": the FP16 word rebuilt from hi and the residual
+// byte (merge4 holds both nestings).
+template <int ENC>
 __global__ __launch_bounds__(kThreads) void merge_kernel(const uint8_t *__restrict__ hi,
                                                          ResidualView res, int64_t numel,
                                                          uint16_t *__restrict__ w)
@@ -77,8 +103,8 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(const uint8_t *__restri
         const int64_t i0 = v << 4;
         const u32x4 h = load16(hi + i0);
         const u32x4 l = load_lo_lookup(res, i0);
-        const u32x2 p0 = merge4(h.x, l.x), p1 = merge4(h.y, l.y);
-        const u32x2 p2 = merge4(h.z, l.z), p3 = merge4(h.w, l.w);
+        const u32x2 p0 = merge4<ENC>(h.x, l.x), p1 = merge4<ENC>(h.y, l.y);
+        const u32x2 p2 = merge4<ENC>(h.z, l.z), p3 = merge4<ENC>(h.w, l.w);
         const u32x4 a = {p0.x, p0.y, p1.x, p1.y};
         const u32x4 b = {p2.x, p2.y, p3.x, p3.y};
         *reinterpret_cast<u32x4 *>(w + i0) = a;
@@ -88,9 +114,39 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(const uint8_t *__restri
         for (int64_t i = nvec << 4; i < numel; ++i) {
             const int64_t off = residual_offset(res, i);
             const uint16_t lo = off >= 0 ? res.pool[off] : 0;
-            w[i] = (uint16_t)(((uint16_t)hi[i] << 8) | lo);
+            const uint32_t t = ((uint32_t)hi[i] << 8) | lo;
+            w[i] = (uint16_t)(ENC == ENC_E4M3 ? e4m3_words(t) : t);
         }
     }
+}
+
+// Per-layer encoding choice (Sec. IV-C, "Dual-mode serving" paragraph): a
+// block stores E5M2 into *out if any of its words does not fit E4M3; *out was
+// set to E4M3 by set_enc_kernel just before on the same stream.  Every
+// writer stores the same value, so the unordered stores need no atomics.
+__global__ void set_enc_kernel(int32_t *out)
+{
+    *out = ENC_E4M3;
+}
+
+__global__ __launch_bounds__(kThreads) void select_enc_kernel(const uint16_t *__restrict__ w,
+                                                              int64_t numel, int32_t *out)
+{
+    const int64_t nvec = numel >> 3;
+    const int64_t stride = (int64_t)gridDim.x * kThreads;
+    bool bad = false;
+    for (int64_t v = (int64_t)blockIdx.x * kThreads + threadIdx.x; v < nvec; v += stride) {
+        const u32x4 a = load16(w + (v << 3));
+        const uint32_t d[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            bad |= !e4m3_fits(d[j]) || !e4m3_fits(d[j] >> 16);
+    }
+    if (blockIdx.x == 0 && threadIdx.x == 0)
+        for (int64_t i = nvec << 3; i < numel; ++i)
+            bad |= !e4m3_fits(w[i]);
+    if (__syncthreads_or(bad) && threadIdx.x == 0)
+        *out = ENC_E5M2;
 }
 
 // Nearest OCP E4M3 code to v (|v| <= 448), ties to even, written from the
@@ -215,19 +271,43 @@ __global__ __launch_bounds__(kThreads) void splitk_reduce_kernel(const float *__
 
 }  // namespace
 
-hipError_t launch_split(const uint16_t *w, int64_t numel, uint8_t *hi, const ResidualView &res,
-                        hipStream_t stream)
+hipError_t launch_split(int enc, const uint16_t *w, int64_t numel, uint8_t *hi,
+                        const ResidualView &res, hipStream_t stream)
 {
-    hipLaunchKernelGGL(split_kernel, dim3((unsigned)grid_for(numel >> 4)), dim3(kThreads), 0,
-                       stream, w, numel, hi, res);
+    const dim3 grid((unsigned)grid_for(numel >> 4));
+    if (enc == ENC_E4M3)
+        hipLaunchKernelGGL(split_kernel<ENC_E4M3>, grid, dim3(kThreads), 0, stream, w, numel, hi,
+                           res);
+    else
+        hipLaunchKernelGGL(split_kernel<ENC_E5M2>, grid, dim3(kThreads), 0, stream, w, numel, hi,
+                           res);
     return hipGetLastError();
 }
 
-hipError_t launch_merge(const uint8_t *hi, const ResidualView &res, int64_t numel,
+hipError_t launch_merge(int enc, const uint8_t *hi, const ResidualView &res, int64_t numel,
                         uint16_t *w_out, hipStream_t stream)
 {
-    hipLaunchKernelGGL(merge_kernel, dim3((unsigned)grid_for(numel >> 4)), dim3(kThreads), 0,
-                       stream, hi, res, numel, w_out);
+    const dim3 grid((unsigned)grid_for(numel >> 4));
+    if (enc == ENC_E4M3)
+        hipLaunchKernelGGL(merge_kernel<ENC_E4M3>, grid, dim3(kThreads), 0, stream, hi, res, numel,
+                           w_out);
+    else
+        hipLaunchKernelGGL(merge_kernel<ENC_E5M2>, grid, dim3(kThreads), 0, stream, hi, res, numel,
+                           w_out);
+    return hipGetLastError();
+}
+
+hipError_t launch_select_enc(const uint16_t *w, int64_t numel, int32_t *enc_out,
+                             hipStream_t stream)
+{
+    hipLaunchKernelGGL(set_enc_kernel, dim3(1), dim3(1), 0, stream, enc_out);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || numel == 0)
+        return e;
+    int64_t blocks = grid_for(numel >> 3);
+    blocks = blocks < 1024 ? blocks : 1024;  // at most 1024 stores of the verdict
+    hipLaunchKernelGGL(select_enc_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, stream, w,
+                       numel, enc_out);
     return hipGetLastError();
 }
 

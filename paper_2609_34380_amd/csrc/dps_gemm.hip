@@ -1,28 +1,27 @@
 // dps_gemm.hip -- prefill-shaped nested linear on the matrix cores (gfx950).
 //
-// gemm_f16_kernel: Y = X . W^T with W's upper-byte tile (and, in full mode,
-// its residual-byte tile) staged in LDS as bytes -- half the LDS bytes of an
-// FP16 tile each -- and merged into FP16 operands in registers right before
-// v_mfma_f32_16x16x32_f16 (Sec. IV-C: reconstruction during computation).
-// gemm_fp8_kernel: fast mode with FP8 activations; the E5M2 upper bytes are
-// used as-is as the A operand of v_mfma_f32_16x16x128_f8f6f4 against E4M3
-// activations, and the row scale is applied to the fp32 accumulator.
+// gemm4_kernel: FP16 activations, full and fast mode.  The weight tile's
+// upper-byte plane (and, in full mode, its residual plane) is staged in LDS
+// as bytes and merged into FP16 operands in registers right before
+// v_mfma_f32_16x16x32_f16 (Sec. IV-C: reconstruction during computation);
+// fast mode feeds zero residual bytes through the same merge.
+// gemm3_kernel: fast mode with FP8 activations.  The upper bytes go to
+// v_mfma_f32_16x16x128_f8f6f4 as they are stored -- E5M2, or E4M3 whose
+// fast-mode value is E4M3 * 2^-8 -- against E4M3 activations, and the row
+// scale (times 2^-8 for E4M3 weights) is applied to the fp32 accumulator.
 //
-// Block tile 128 (weight rows) x 128 (tokens), 4 waves in a 2 x 2 grid, each
-// wave 64 x 64 = 4 x 4 MFMA tiles.  Global -> register -> LDS double
-// buffering: tile t+1 is fetched while tile t is multiplied, one barrier per
-// K tile.  The weight rows are the MFMA A operand, so a lane ends up holding
-// four consecutive output features of one token (8-byte FP16 stores).
-// Grouped (MoE) calls map grid.y onto (expert, token tile) by scanning the
-// device offsets, so only `experts` blocks at most find no work.
+// Both stream their tiles global -> LDS with direct-to-LDS loads through
+// rings of stages, one barrier per stage.  Dense calls walk a 1-D grid
+// remapped for the 8 XCDs; grouped (MoE) calls map grid.y onto (expert,
+// token tile) by scanning the device offsets, so only `experts` blocks at
+// most find no work.
 #include "dps_internal.h"
 
 namespace dps {
 
 namespace {
 
-constexpr int BM = 128;  // tokens per block
-constexpr int BN = 128;  // weight rows per block
+constexpr int BM = 128;  // default token tile of block_rows
 
 struct GemmArgs {
     const void *x;  // FP16 [rows][k] or E4M3 [rows][k]
@@ -96,163 +95,6 @@ __device__ __forceinline__ void store_tile_out(const GemmArgs &a, int s, int64_t
     }
 }
 
-// ------------------------------------------------------------------------------
-// FP16 matrix cores, weights merged in registers
-// ------------------------------------------------------------------------------
-constexpr int BK16 = 64;          // K elements per tile
-constexpr int XP16 = BK16 + 8;    // X tile pitch, halfs (144 B)
-constexpr int WP16 = BK16 + 16;   // weight byte tile pitch (80 B)
-
-template <int MODE, bool RANGE>
-__global__ __launch_bounds__(256) void gemm_f16_kernel(GemmArgs a)
-{
-    __shared__ __attribute__((aligned(16))) uint16_t xs[2][BM * XP16];
-    __shared__ __attribute__((aligned(16))) uint8_t hs[2][BN * WP16];
-    __shared__ __attribute__((aligned(16))) uint8_t ls[MODE == MODE_FULL ? 2 : 1][BN * WP16];
-
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int li = lane & 15;
-    const int lg = lane >> 4;
-
-    int64_t e, mrow0, mrow1;
-    if (!block_rows(a, e, mrow0, mrow1))
-        return;
-    const int ntile = blockIdx.x / a.splits;
-    const int s = blockIdx.x % a.splits;
-    const int64_t n0 = (int64_t)ntile * BN;
-    const int64_t kb0 = (int64_t)s * a.ksplit;
-    const int64_t ke = kb0 + a.ksplit < a.k ? kb0 + a.ksplit : a.k;
-    const uint16_t *x = static_cast<const uint16_t *>(a.x);
-
-    // global load assignment (fixed rows per thread)
-    const int64_t xr0 = tid >> 3;                // + 32 * j, j < 4
-    const int xc = (tid & 7) * 8;                // halfs
-    const int64_t wr0 = tid >> 2;                // + 64 * j, j < 2
-    const int wc = (tid & 3) * 16;               // bytes
-    int64_t lrow[2];
-    bool wok[2];
-    RangeResidual rr[2];
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-        const int64_t nr = n0 + wr0 + 64 * j;
-        wok[j] = nr < a.n;
-        lrow[j] = (e * a.n + nr) * a.k;
-        if (MODE == MODE_FULL && RANGE) {
-            rr[j].ok0 = rr[j].ok1 = false;
-            rr[j].delta0 = rr[j].delta1 = 0;
-            rr[j].bnd = 0;
-            if (wok[j] && ke > kb0)
-                rr[j] = range_residual(a.res, lrow[j] + kb0, lrow[j] + ke);
-        }
-    }
-
-    u32x4 xreg[4], hreg[2], lreg[2];
-    auto gload = [&](int64_t kt) {
-        const u32x4 z = {0u, 0u, 0u, 0u};
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int64_t m = mrow0 + xr0 + 32 * j;
-            xreg[j] = z;
-            if (m < mrow1 && kt + xc < ke)
-                xreg[j] = load16(x + m * a.k + kt + xc);
-        }
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            hreg[j] = z;
-            lreg[j] = z;
-            if (wok[j] && kt + wc < ke) {
-                hreg[j] = load16(a.hi + lrow[j] + kt + wc);
-                if (MODE == MODE_FULL)
-                    lreg[j] = RANGE ? load_lo_range(a.res, rr[j], lrow[j] + kt + wc)
-                                    : load_lo_lookup(a.res, lrow[j] + kt + wc);
-            }
-        }
-    };
-    auto sstore = [&](int b) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-            *reinterpret_cast<u32x4 *>(&xs[b][(xr0 + 32 * j) * XP16 + xc]) = xreg[j];
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            *reinterpret_cast<u32x4 *>(&hs[b][(wr0 + 64 * j) * WP16 + wc]) = hreg[j];
-            if (MODE == MODE_FULL)
-                *reinterpret_cast<u32x4 *>(&ls[b][(wr0 + 64 * j) * WP16 + wc]) = lreg[j];
-        }
-    };
-
-    const int wn = wave & 1;
-    const int wm = wave >> 1;
-    f32x4 acc[4][4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-            acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    const int64_t ntk = ke > kb0 ? (ke - kb0 + BK16 - 1) / BK16 : 0;
-    if (ntk > 0) {
-        gload(kb0);
-        sstore(0);
-    }
-    __syncthreads();
-    for (int64_t t = 0; t < ntk; ++t) {
-        const int b = (int)(t & 1);
-        if (t + 1 < ntk)
-            gload(kb0 + (t + 1) * BK16);
-        half8 a0[4], a1[4];
-#pragma unroll
-        for (int nt = 0; nt < 4; ++nt) {
-            const int row = wn * 64 + nt * 16 + li;
-            const u32x4 h = *reinterpret_cast<const u32x4 *>(&hs[b][row * WP16 + lg * 16]);
-            u32x4 l = {0u, 0u, 0u, 0u};
-            if (MODE == MODE_FULL)
-                l = *reinterpret_cast<const u32x4 *>(&ls[b][row * WP16 + lg * 16]);
-            a0[nt] = merge8(h.x, h.y, l.x, l.y);
-            a1[nt] = merge8(h.z, h.w, l.z, l.w);
-        }
-#pragma unroll
-        for (int mt = 0; mt < 4; ++mt) {
-            const int row = wm * 64 + mt * 16 + li;
-            const half8 b0 = as_half8(*reinterpret_cast<const u32x4 *>(&xs[b][row * XP16 + lg * 16]));
-            const half8 b1 =
-                as_half8(*reinterpret_cast<const u32x4 *>(&xs[b][row * XP16 + lg * 16 + 8]));
-#pragma unroll
-            for (int nt = 0; nt < 4; ++nt) {
-                acc[nt][mt] = mfma16x16x32(a0[nt], b0, acc[nt][mt]);
-                acc[nt][mt] = mfma16x16x32(a1[nt], b1, acc[nt][mt]);
-            }
-        }
-        if (t + 1 < ntk)
-            sstore(b ^ 1);
-        __syncthreads();
-    }
-
-#pragma unroll
-    for (int nt = 0; nt < 4; ++nt)
-#pragma unroll
-        for (int mt = 0; mt < 4; ++mt)
-            store_tile_out(a, s, mrow0 + wm * 64 + mt * 16 + li, n0 + wn * 64 + nt * 16 + lg * 4,
-                           acc[nt][mt], mrow1);
-}
-
-// ------------------------------------------------------------------------------
-// FP16 matrix cores, LDS-DMA pipeline (gfx950 global_load_lds_dwordx4)
-// ------------------------------------------------------------------------------
-// Tiles stream global -> LDS with direct-to-LDS loads (no registers in flight)
-// through a ring of DMA_STAGES stages; each stage holds, for 64 K elements,
-// the 128-row upper-byte tile, the residual-byte tile (full mode) and the
-// BM-token X tile.  A DMA instruction writes 64 lanes x 16 bytes contiguously,
-// so each lane is pointed at the global chunk that belongs at its LDS slot;
-// the slot order is XOR-swizzled per row so that the MFMA-layout reads below
-// are free of bank conflicts.  Lanes whose chunk is past the K range, or whose
-// residual chunk has no valid slot, load from a zero vector instead (a DMA
-// cannot zero-fill).  One barrier per stage.
-constexpr int DMA_BK = 64;
-constexpr int DMA_STAGES = 3;
-constexpr int DMA_W_BYTES = BN * DMA_BK;  // one byte plane, 8 KiB
-
 __device__ __attribute__((aligned(16))) const uint8_t g_zero16[16] = {0};
 
 #define DPS_LDS(p) ((__attribute__((address_space(3))) void *)(p))
@@ -282,216 +124,42 @@ __device__ __forceinline__ void stage_barrier()
     asm volatile("" ::: "memory");
 }
 
-template <int MODE, int BM>
-struct DmaCfg {
-    static constexpr int X_BYTES = BM * DMA_BK * 2;
-    static constexpr int PLANES = MODE == MODE_FULL ? 2 : 1;
-    static constexpr int STAGE = DMA_W_BYTES * PLANES + X_BYTES;
-    static constexpr int LDS = STAGE * DMA_STAGES;
-    static constexpr int X_INSTR = X_BYTES / 1024 / 4;          // per wave per stage
-    static constexpr int W_INSTR = DMA_W_BYTES / 1024 / 4;      // per wave per plane per stage
-    static constexpr int NI = W_INSTR * PLANES + X_INSTR;       // DMA instructions per wave per stage
-    static constexpr int MT = BM / 32;                          // 16-token tiles per wave
-};
-
-template <int MODE, int BM, bool RANGE>
-__global__ __launch_bounds__(256) void gemm_f16_dma_kernel(GemmArgs a)
-{
-    using C = DmaCfg<MODE, BM>;
-    __shared__ __attribute__((aligned(16))) uint8_t smem[C::LDS];
-
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int li = lane & 15;
-    const int lg = lane >> 4;
-
-    int64_t e, mrow0, mrow1;
-    if (!block_rows(a, e, mrow0, mrow1, BM))
-        return;
-    const int ntile = blockIdx.x / a.splits;
-    const int s = blockIdx.x % a.splits;
-    const int64_t n0 = (int64_t)ntile * BN;
-    const int64_t kb0 = (int64_t)s * a.ksplit;
-    const int64_t ke = kb0 + a.ksplit < a.k ? kb0 + a.ksplit : a.k;
-    const int64_t ntk = ke > kb0 ? (ke - kb0 + DMA_BK - 1) / DMA_BK : 0;
-    const uint16_t *x = static_cast<const uint16_t *>(a.x);
-
-    // ---- per-lane DMA sources that do not change with the K stage ---------------
-    // weight rows: instruction j (= wave * W_INSTR + jj) covers rows 16j .. 16j+15,
-    // lane l -> row 16j + l/4, LDS chunk slot l%4 holding logical chunk
-    // (l%4) ^ ((row >> 2) & 3)
-    const uint8_t *wsrc[C::W_INSTR];
-    int64_t wl[C::W_INSTR];
-    int wchunk[C::W_INSTR];
-    RangeResidual rr[C::W_INSTR];
-#pragma unroll
-    for (int jj = 0; jj < C::W_INSTR; ++jj) {
-        const int j = wave * C::W_INSTR + jj;
-        const int r = 16 * j + (lane >> 2);
-        int64_t nr = n0 + r;
-        nr = nr < a.n ? nr : a.n - 1;
-        wl[jj] = (e * a.n + nr) * a.k;
-        wsrc[jj] = a.hi + wl[jj];
-        wchunk[jj] = (lane & 3) ^ ((r >> 2) & 3);
-        rr[jj].ok0 = rr[jj].ok1 = false;
-        rr[jj].delta0 = rr[jj].delta1 = 0;
-        rr[jj].bnd = 0;
-        if (MODE == MODE_FULL && RANGE && ke > kb0)
-            rr[jj] = range_residual(a.res, wl[jj] + kb0, wl[jj] + ke);
-    }
-    // X rows: instruction j covers rows 8j .. 8j+7, lane l -> row 8j + l/8,
-    // slot l%8 holding logical chunk (l%8) ^ (row & 7) (8 halfs per chunk)
-    const uint16_t *xsrc[C::X_INSTR];
-    int xchunk[C::X_INSTR];
-#pragma unroll
-    for (int jj = 0; jj < C::X_INSTR; ++jj) {
-        const int j = wave * C::X_INSTR + jj;
-        const int r = 8 * j + (lane >> 3);
-        int64_t m = mrow0 + r;
-        m = m < mrow1 ? m : mrow1 - 1;
-        xsrc[jj] = x + m * a.k;
-        xchunk[jj] = (lane & 7) ^ (r & 7);
-    }
-
-    auto issue = [&](int64_t t) {
-        uint8_t *st = smem + (int)(t % DMA_STAGES) * C::STAGE;
-        const bool live = t < ntk;
-        const int64_t kt = kb0 + t * DMA_BK;
-#pragma unroll
-        for (int jj = 0; jj < C::W_INSTR; ++jj) {
-            const int j = wave * C::W_INSTR + jj;
-            const int64_t kk = kt + wchunk[jj] * 16;
-            const bool ok = live && kk < ke;
-            dma16(ok ? (const void *)(wsrc[jj] + kk) : (const void *)g_zero16, st + j * 1024);
-            if (MODE == MODE_FULL) {
-                const int64_t li2 = wl[jj] + (ok ? kk : kb0);
-                const void *src = g_zero16;
-                if (RANGE) {
-                    const bool second = li2 >= rr[jj].bnd;
-                    const bool cok = second ? rr[jj].ok1 : rr[jj].ok0;
-                    const int64_t d = second ? rr[jj].delta1 : rr[jj].delta0;
-                    if (ok && cok)
-                        src = a.res.pool + (d + li2);
-                } else {
-                    const int64_t off = residual_offset(a.res, li2);
-                    if (ok && off >= 0)
-                        src = a.res.pool + off;
-                }
-                dma16(src, st + DMA_W_BYTES + j * 1024);
-            }
-        }
-#pragma unroll
-        for (int jj = 0; jj < C::X_INSTR; ++jj) {
-            const int j = wave * C::X_INSTR + jj;
-            const int64_t kk = kt + xchunk[jj] * 8;
-            const bool ok = live && kk < ke;
-            dma16(ok ? (const void *)(xsrc[jj] + kk) : (const void *)g_zero16,
-                  st + DMA_W_BYTES * C::PLANES + j * 1024);
-        }
-    };
-
-    const int wn = wave & 1;
-    const int wm = wave >> 1;
-    f32x4 acc[4][C::MT];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < C::MT; ++j)
-            acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-#pragma unroll
-    for (int t = 0; t < DMA_STAGES - 1; ++t)
-        issue(t);
-    for (int64_t t = 0; t < ntk; ++t) {
-        DPS_WAIT_VMCNT(C::NI * (DMA_STAGES - 2));
-        stage_barrier();
-        issue(t + DMA_STAGES - 1);
-        const uint8_t *st = smem + (int)(t % DMA_STAGES) * C::STAGE;
-        const uint8_t *xs = st + DMA_W_BYTES * C::PLANES;
-        half8 a0[4], a1[4];
-#pragma unroll
-        for (int nt = 0; nt < 4; ++nt) {
-            const int r = wn * 64 + nt * 16 + li;
-            const int off = r * DMA_BK + ((lg ^ ((r >> 2) & 3)) << 4);
-            const u32x4 h = *reinterpret_cast<const u32x4 *>(st + off);
-            u32x4 l = {0u, 0u, 0u, 0u};
-            if (MODE == MODE_FULL)
-                l = *reinterpret_cast<const u32x4 *>(st + DMA_W_BYTES + off);
-            a0[nt] = merge8(h.x, h.y, l.x, l.y);
-            a1[nt] = merge8(h.z, h.w, l.z, l.w);
-        }
-#pragma unroll
-        for (int mt = 0; mt < C::MT; ++mt) {
-            const int r = wm * (BM / 2) + mt * 16 + li;
-            const uint8_t *row = xs + r * (DMA_BK * 2);
-            const half8 b0 = as_half8(*reinterpret_cast<const u32x4 *>(row + (((2 * lg) ^ (r & 7)) << 4)));
-            const half8 b1 =
-                as_half8(*reinterpret_cast<const u32x4 *>(row + (((2 * lg + 1) ^ (r & 7)) << 4)));
-#pragma unroll
-            for (int nt = 0; nt < 4; ++nt) {
-                acc[nt][mt] = mfma16x16x32(a0[nt], b0, acc[nt][mt]);
-                acc[nt][mt] = mfma16x16x32(a1[nt], b1, acc[nt][mt]);
-            }
-        }
-    }
-    DPS_WAIT_VMCNT(0);  // no DMA may still target this block's LDS when it exits
-
-#pragma unroll
-    for (int nt = 0; nt < 4; ++nt)
-#pragma unroll
-        for (int mt = 0; mt < C::MT; ++mt)
-            store_tile_out(a, s, mrow0 + wm * (BM / 2) + mt * 16 + li,
-                           n0 + wn * 64 + nt * 16 + lg * 4, acc[nt][mt], mrow1);
-}
 
 // ------------------------------------------------------------------------------
-// Eight-wave LDS-DMA GEMM (two waves per SIMD), FP16 full/fast and FP8 fast
+// Eight-wave LDS-DMA GEMM (two waves per SIMD), fast mode with FP8 activations
 // ------------------------------------------------------------------------------
 // Block tile BN weight rows x BM tokens, waves in a WN x WM grid, each wave
-// (BN/WN) x (BM/WM).  A stage covers BK K elements: 64 for FP16 (processed as
-// two 32-wide MFMA steps), 128 for FP8 (one 16x16x128 step).  Stages stream
-// global -> LDS by direct-to-LDS loads through a ring of NSTAGE slots, one
-// barrier per stage.  LDS rows hold 16-byte chunks at slot chunk ^ swz(row),
-// swz(row) = (row / rows-per-256-bytes) % chunks-per-row, so the 16 rows a
-// fragment read touches land in 16 distinct 16-byte bank groups.
-//   FP16 step h, lane (i, g): A = weight row i, K 32h+8g .. +7 (8 bytes per
-//   plane, merged into FP16 in registers); B = token row i, same K.
-//   FP8, lane (i, g): A and B = bytes 32g .. 32g+31 of the stage.
-enum { G3_FULL = 0, G3_FAST = 1, G3_FP8 = 2 };
-
-template <int KIND, int BN_, int BM_, int WN, int WM, int NSTAGE>
+// (BN/WN) x (BM/WM).  A stage covers 128 K elements (one 16x16x128 MFMA
+// step).  Stages stream global -> LDS by direct-to-LDS loads through a ring
+// of NSTAGE slots, one barrier per stage.  LDS rows hold 16-byte chunks at
+// slot chunk ^ swz(row), swz(row) = (row / 2) % 8 for the 128-byte rows, so
+// the 16 rows a fragment read touches land in 16 distinct 16-byte bank
+// groups.  Lane (i, g): A = weight row i and B = token row i, bytes
+// 32g .. 32g+31 of the stage.
+template <int BN_, int BM_, int WN, int WM, int NSTAGE>
 struct G3 {
-    static constexpr bool FP8 = KIND == G3_FP8;
-    static constexpr int PLANES = KIND == G3_FULL ? 2 : 1;
-    static constexpr int BK = FP8 ? 128 : 64;
-    static constexpr int WROW = BK;                  // bytes per weight row per plane
-    static constexpr int XROW = FP8 ? BK : 2 * BK;   // bytes per token row
-    static constexpr int W_BYTES = BN_ * WROW;
-    static constexpr int X_BYTES = BM_ * XROW;
-    static constexpr int STAGE = W_BYTES * PLANES + X_BYTES;
+    static constexpr int BK = 128;
+    static constexpr int ROW = BK;                   // bytes per row, both operands
+    static constexpr int W_BYTES = BN_ * ROW;
+    static constexpr int X_BYTES = BM_ * ROW;
+    static constexpr int STAGE = W_BYTES + X_BYTES;
     static constexpr int LDS = STAGE * NSTAGE;
     static constexpr int NWAVES = WN * WM;
     static constexpr int W_INSTR = W_BYTES / 1024 / NWAVES;
     static constexpr int X_INSTR = X_BYTES / 1024 / NWAVES;
-    static constexpr int NI = W_INSTR * PLANES + X_INSTR;
+    static constexpr int NI = W_INSTR + X_INSTR;
     static constexpr int TN = BN_ / WN, TM = BM_ / WM;
     static constexpr int NT = TN / 16, MT = TM / 16;
     static_assert(W_BYTES % (1024 * NWAVES) == 0 && X_BYTES % (1024 * NWAVES) == 0, "tiling");
     static_assert(LDS <= 160 * 1024, "LDS");
 };
 
-// slot swizzle for rows of `rowbytes` bytes (64 or 128)
-template <int ROWBYTES>
-__device__ __forceinline__ int g3_swz(int r)
-{
-    return (r / (256 / ROWBYTES)) % (ROWBYTES / 16);
-}
+__device__ __forceinline__ int g3_swz(int r) { return (r >> 1) & 7; }
 
-template <int KIND, int BN_, int BM_, int WN, int WM, int NSTAGE, bool RANGE>
+template <int ENC, int BN_, int BM_, int WN, int WM, int NSTAGE>
 __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
 {
-    using C = G3<KIND, BN_, BM_, WN, WM, NSTAGE>;
+    using C = G3<BN_, BM_, WN, WM, NSTAGE>;
     __shared__ __attribute__((aligned(16))) uint8_t smem[C::LDS];
 
     const int tid = threadIdx.x;
@@ -500,77 +168,52 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
     const int li = lane & 15;
     const int lg = lane >> 4;
 
-    int64_t e, mrow0, mrow1;
-    int ntile, s;
-    if (a.offsets) {
-        if (!block_rows(a, e, mrow0, mrow1, BM_))
-            return;
-        ntile = blockIdx.x / a.splits;
-        s = blockIdx.x % a.splits;
-    } else {
-        // Dense calls use a 1-D grid remapped for the 8 XCDs: block L runs on
-        // XCD L % 8, so XCD x is given the contiguous tile range
-        // [x * per_xcd, (x+1) * per_xcd), walked with the token tile fastest.
-        // Blocks sharing a weight tile then run together on one XCD and fetch
-        // it into that XCD's L2 once.
-        const int64_t mtiles = (a.rows + BM_ - 1) / BM_;
-        const int64_t ntiles = (a.n + BN_ - 1) / BN_;
-        const int64_t total = mtiles * ntiles * a.splits;
-        const int64_t per_xcd = (total + 7) / 8;
-        const int64_t lin = blockIdx.x;
-        const int64_t t = (lin % 8) * per_xcd + lin / 8;
-        if (t >= total)
-            return;
-        const int64_t mt = t % mtiles;
-        ntile = (int)((t / mtiles) % ntiles);
-        s = (int)(t / (mtiles * ntiles));
-        e = 0;
-        mrow0 = mt * BM_;
-        mrow1 = mrow0 + BM_ < a.rows ? mrow0 + BM_ : a.rows;
-    }
+    // 1-D grid remapped for the 8 XCDs: block L runs on XCD L % 8, so XCD x
+    // is given the contiguous tile range [x * per_xcd, (x+1) * per_xcd),
+    // walked with the token tile fastest.  Blocks sharing a weight tile then
+    // run together on one XCD and fetch it into that XCD's L2 once.
+    const int64_t mtiles = (a.rows + BM_ - 1) / BM_;
+    const int64_t ntiles = (a.n + BN_ - 1) / BN_;
+    const int64_t total = mtiles * ntiles * a.splits;
+    const int64_t per_xcd = (total + 7) / 8;
+    const int64_t lin = blockIdx.x;
+    const int64_t t0 = (lin % 8) * per_xcd + lin / 8;
+    if (t0 >= total)
+        return;
+    const int64_t mtile = t0 % mtiles;
+    const int ntile = (int)((t0 / mtiles) % ntiles);
+    const int s = (int)(t0 / (mtiles * ntiles));
+    const int64_t mrow0 = mtile * BM_;
+    const int64_t mrow1 = mrow0 + BM_ < a.rows ? mrow0 + BM_ : a.rows;
     const int64_t n0 = (int64_t)ntile * BN_;
     const int64_t kb0 = (int64_t)s * a.ksplit;
     const int64_t ke = kb0 + a.ksplit < a.k ? kb0 + a.ksplit : a.k;
     const int64_t ntk = ke > kb0 ? (ke - kb0 + C::BK - 1) / C::BK : 0;
 
-    // ---- per-lane DMA descriptors (fixed across stages) ---------------------------
-    // weight instruction j: LDS bytes j*1024 .. +1023 of the plane tile
+    // ---- per-lane DMA sources (fixed across stages) ------------------------------
+    // instruction j covers LDS bytes j*1024 .. +1023 of its operand tile:
+    // rows 8j .. 8j+7, lane -> row 8j + lane/8, slot lane%8
     const uint8_t *wsrc[C::W_INSTR];
-    int64_t wl[C::W_INSTR];
-    int wel[C::W_INSTR];  // element offset of this lane's chunk within the stage
-    RangeResidual rr[C::W_INSTR];
+    int wel[C::W_INSTR];  // K offset of this lane's chunk within the stage
 #pragma unroll
     for (int jj = 0; jj < C::W_INSTR; ++jj) {
         const int j = wave * C::W_INSTR + jj;
-        const int pos = j * 1024 + lane * 16;
-        const int r = pos / C::WROW;
-        const int slot = (pos % C::WROW) / 16;
-        const int chunk = slot ^ g3_swz<C::WROW>(r);
+        const int r = 8 * j + (lane >> 3);
         int64_t nr = n0 + r;
         nr = nr < a.n ? nr : a.n - 1;
-        wl[jj] = (e * a.n + nr) * a.k;
-        wsrc[jj] = a.hi + wl[jj];
-        wel[jj] = chunk * 16;
-        rr[jj].ok0 = rr[jj].ok1 = false;
-        rr[jj].delta0 = rr[jj].delta1 = 0;
-        rr[jj].bnd = 0;
-        if (KIND == G3_FULL && RANGE && ke > kb0)
-            rr[jj] = range_residual(a.res, wl[jj] + kb0, wl[jj] + ke);
+        wsrc[jj] = a.hi + nr * a.k;
+        wel[jj] = ((lane & 7) ^ g3_swz(r)) * 16;
     }
     const uint8_t *xsrc[C::X_INSTR];
     int xel[C::X_INSTR];
-    constexpr int XELEM = C::FP8 ? 1 : 2;  // bytes per X element
 #pragma unroll
     for (int jj = 0; jj < C::X_INSTR; ++jj) {
         const int j = wave * C::X_INSTR + jj;
-        const int pos = j * 1024 + lane * 16;
-        const int r = pos / C::XROW;
-        const int slot = (pos % C::XROW) / 16;
-        const int chunk = slot ^ g3_swz<C::XROW>(r);
+        const int r = 8 * j + (lane >> 3);
         int64_t m = mrow0 + r;
         m = m < mrow1 ? m : mrow1 - 1;
-        xsrc[jj] = static_cast<const uint8_t *>(a.x) + m * a.k * XELEM;
-        xel[jj] = chunk * (16 / XELEM);
+        xsrc[jj] = static_cast<const uint8_t *>(a.x) + m * a.k;
+        xel[jj] = ((lane & 7) ^ g3_swz(r)) * 16;
     }
 
     auto issue = [&](int64_t t) {
@@ -583,30 +226,14 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
             const int64_t kk = kt + wel[jj];
             const bool ok = live && kk < ke;
             dma16(ok ? (const void *)(wsrc[jj] + kk) : (const void *)g_zero16, st + j * 1024);
-            if (KIND == G3_FULL) {
-                const int64_t lo = wl[jj] + (ok ? kk : kb0);
-                const void *src = g_zero16;
-                if (RANGE) {
-                    const bool second = lo >= rr[jj].bnd;
-                    const bool cok = second ? rr[jj].ok1 : rr[jj].ok0;
-                    const int64_t d = second ? rr[jj].delta1 : rr[jj].delta0;
-                    if (ok && cok)
-                        src = a.res.pool + (d + lo);
-                } else {
-                    const int64_t off = residual_offset(a.res, lo);
-                    if (ok && off >= 0)
-                        src = a.res.pool + off;
-                }
-                dma16(src, st + C::W_BYTES + j * 1024);
-            }
         }
 #pragma unroll
         for (int jj = 0; jj < C::X_INSTR; ++jj) {
             const int j = wave * C::X_INSTR + jj;
             const int64_t kk = kt + xel[jj];
             const bool ok = live && kk < ke;
-            dma16(ok ? (const void *)(xsrc[jj] + kk * XELEM) : (const void *)g_zero16,
-                  st + C::W_BYTES * C::PLANES + j * 1024);
+            dma16(ok ? (const void *)(xsrc[jj] + kk) : (const void *)g_zero16,
+                  st + C::W_BYTES + j * 1024);
         }
     };
 
@@ -627,76 +254,49 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
         stage_barrier();
         issue(t + NSTAGE - 1);
         const uint8_t *st = smem + (int)(t % NSTAGE) * C::STAGE;
-        const uint8_t *xs = st + C::W_BYTES * C::PLANES;
-        if (C::FP8) {
-            i32x8 av[C::NT];
+        const uint8_t *xs = st + C::W_BYTES;
+        i32x8 av[C::NT];
 #pragma unroll
-            for (int nt = 0; nt < C::NT; ++nt) {
-                const int r = wn * C::TN + nt * 16 + li;
-                const uint8_t *row = st + r * C::WROW;
-                const int sw = g3_swz<C::WROW>(r);
-                const u32x4 p = *reinterpret_cast<const u32x4 *>(row + (((2 * lg) ^ sw) << 4));
-                const u32x4 q = *reinterpret_cast<const u32x4 *>(row + (((2 * lg + 1) ^ sw) << 4));
-                av[nt] = i32x8{(int)p.x, (int)p.y, (int)p.z, (int)p.w,
-                               (int)q.x, (int)q.y, (int)q.z, (int)q.w};
-            }
+        for (int nt = 0; nt < C::NT; ++nt) {
+            const int r = wn * C::TN + nt * 16 + li;
+            const uint8_t *row = st + r * C::ROW;
+            const int sw = g3_swz(r);
+            const u32x4 p = *reinterpret_cast<const u32x4 *>(row + (((2 * lg) ^ sw) << 4));
+            const u32x4 q = *reinterpret_cast<const u32x4 *>(row + (((2 * lg + 1) ^ sw) << 4));
+            av[nt] = i32x8{(int)p.x, (int)p.y, (int)p.z, (int)p.w,
+                           (int)q.x, (int)q.y, (int)q.z, (int)q.w};
+        }
 #pragma unroll
-            for (int mt = 0; mt < C::MT; ++mt) {
-                const int r = wm * C::TM + mt * 16 + li;
-                const uint8_t *row = xs + r * C::XROW;
-                const int sw = g3_swz<C::XROW>(r);
-                const u32x4 p = *reinterpret_cast<const u32x4 *>(row + (((2 * lg) ^ sw) << 4));
-                const u32x4 q = *reinterpret_cast<const u32x4 *>(row + (((2 * lg + 1) ^ sw) << 4));
-                const i32x8 bv = {(int)p.x, (int)p.y, (int)p.z, (int)p.w,
-                                  (int)q.x, (int)q.y, (int)q.z, (int)q.w};
+        for (int mt = 0; mt < C::MT; ++mt) {
+            const int r = wm * C::TM + mt * 16 + li;
+            const uint8_t *row = xs + r * C::ROW;
+            const int sw = g3_swz(r);
+            const u32x4 p = *reinterpret_cast<const u32x4 *>(row + (((2 * lg) ^ sw) << 4));
+            const u32x4 q = *reinterpret_cast<const u32x4 *>(row + (((2 * lg + 1) ^ sw) << 4));
+            const i32x8 bv = {(int)p.x, (int)p.y, (int)p.z, (int)p.w,
+                              (int)q.x, (int)q.y, (int)q.z, (int)q.w};
 #pragma unroll
-                for (int nt = 0; nt < C::NT; ++nt)
-                    acc[nt][mt] = mfma16x16x128_bf8_fp8(av[nt], bv, acc[nt][mt]);
-            }
-        } else {
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                half8 av[C::NT];
-#pragma unroll
-                for (int nt = 0; nt < C::NT; ++nt) {
-                    const int r = wn * C::TN + nt * 16 + li;
-                    const int off = r * C::WROW +
-                                    (((2 * h + (lg >> 1)) ^ g3_swz<C::WROW>(r)) << 4) + ((lg & 1) << 3);
-                    const u32x2 hv = *reinterpret_cast<const u32x2 *>(st + off);
-                    u32x2 lv = {0u, 0u};
-                    if (KIND == G3_FULL)
-                        lv = *reinterpret_cast<const u32x2 *>(st + C::W_BYTES + off);
-                    av[nt] = merge8(hv.x, hv.y, lv.x, lv.y);
-                }
-#pragma unroll
-                for (int mt = 0; mt < C::MT; ++mt) {
-                    const int r = wm * C::TM + mt * 16 + li;
-                    const half8 bv = as_half8(*reinterpret_cast<const u32x4 *>(
-                        xs + r * C::XROW + (((4 * h + lg) ^ g3_swz<C::XROW>(r)) << 4)));
-#pragma unroll
-                    for (int nt = 0; nt < C::NT; ++nt)
-                        acc[nt][mt] = mfma16x16x32(av[nt], bv, acc[nt][mt]);
-                }
-            }
+            for (int nt = 0; nt < C::NT; ++nt)
+                acc[nt][mt] = mfma16x16x128_fp8<ENC>(av[nt], bv, acc[nt][mt]);
         }
     }
     DPS_WAIT_VMCNT(0);  // no DMA may still target this block's LDS when it exits
 
+    // E4M3 weights carry the fast-mode factor 2^-8 (exact in fp32)
+    constexpr float wscale = ENC == ENC_E4M3 ? 0.00390625f : 1.f;
 #pragma unroll
     for (int mt = 0; mt < C::MT; ++mt) {
         const int64_t m = mrow0 + wm * C::TM + mt * 16 + li;
-        float sc = 1.f;
-        if (C::FP8)
-            sc = m < mrow1 ? a.scale[m] : 0.f;
+        const float sc = m < mrow1 ? a.scale[m] * wscale : 0.f;
 #pragma unroll
         for (int nt = 0; nt < C::NT; ++nt)
-            store_tile_out(a, s, m, n0 + wn * C::TN + nt * 16 + lg * 4,
-                           C::FP8 ? acc[nt][mt] * sc : acc[nt][mt], mrow1);
+            store_tile_out(a, s, m, n0 + wn * C::TN + nt * 16 + lg * 4, acc[nt][mt] * sc,
+                           mrow1);
     }
 }
 
 // ------------------------------------------------------------------------------
-// Wide-row LDS-DMA GEMM, FP16 full/fast: 128 x 128 tiles, 128-element stages
+// Wide-row LDS-DMA GEMM, FP16 full/fast: 128 weight rows, 128-element stages
 // ------------------------------------------------------------------------------
 // On gfx950 an LDS-DMA (or plain) load instruction runs at about half speed
 // when each row it touches gets 64 contiguous bytes instead of >= 128 (MI355X,
@@ -757,7 +357,7 @@ struct G4 {
 __device__ __forceinline__ int swz8(int r) { return (r >> 1) & 7; }
 __device__ __forceinline__ int swz16(int r) { return r & 15; }
 
-template <int MODE, int BM, int WS, int XS, bool RANGE, bool SPEC>
+template <int MODE, int ENC, int BM, int WS, int XS, bool RANGE, bool SPEC>
 __global__ __launch_bounds__(SPEC ? 768 : 512) void gemm4_kernel(GemmArgs a)
 {
     using C = G4<MODE, BM, WS, XS, SPEC ? 4 : 8>;
@@ -952,8 +552,8 @@ __global__ __launch_bounds__(SPEC ? 768 : 512) void gemm4_kernel(GemmArgs a)
         half8 a0[4], a1[4];
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt) {
-            a0[nt] = merge8(hv[nt].x, hv[nt].y, lv[nt].x, lv[nt].y);
-            a1[nt] = merge8(hv[nt].z, hv[nt].w, lv[nt].z, lv[nt].w);
+            a0[nt] = weight8<MODE, ENC>(hv[nt].x, hv[nt].y, lv[nt].x, lv[nt].y);
+            a1[nt] = weight8<MODE, ENC>(hv[nt].z, hv[nt].w, lv[nt].z, lv[nt].w);
         }
 #pragma unroll
         for (int sidx = 0; sidx < 2; ++sidx) {
@@ -1028,230 +628,100 @@ __global__ __launch_bounds__(SPEC ? 768 : 512) void gemm4_kernel(GemmArgs a)
     }
 }
 
-// ------------------------------------------------------------------------------
-// FP8 matrix cores: E5M2 weights x E4M3 activations
-// ------------------------------------------------------------------------------
-constexpr int BK8 = 128;        // K elements (= bytes) per tile
-constexpr int P8 = BK8 + 16;    // tile pitch, bytes
-
-__global__ __launch_bounds__(256) void gemm_fp8_kernel(GemmArgs a)
-{
-    __shared__ __attribute__((aligned(16))) uint8_t xs[2][BM * P8];
-    __shared__ __attribute__((aligned(16))) uint8_t hs[2][BN * P8];
-
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int li = lane & 15;
-    const int lg = lane >> 4;
-
-    int64_t e, mrow0, mrow1;
-    if (!block_rows(a, e, mrow0, mrow1))
-        return;
-    const int ntile = blockIdx.x / a.splits;
-    const int s = blockIdx.x % a.splits;
-    const int64_t n0 = (int64_t)ntile * BN;
-    const int64_t kb0 = (int64_t)s * a.ksplit;
-    const int64_t ke = kb0 + a.ksplit < a.k ? kb0 + a.ksplit : a.k;
-    const uint8_t *xq = static_cast<const uint8_t *>(a.x);
-
-    const int64_t r0 = tid >> 3;      // + 32 * j, j < 4 (both tiles)
-    const int c0 = (tid & 7) * 16;    // bytes
-    u32x4 xreg[4], hreg[4];
-    auto gload = [&](int64_t kt) {
-        const u32x4 z = {0u, 0u, 0u, 0u};
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int64_t m = mrow0 + r0 + 32 * j;
-            const int64_t nr = n0 + r0 + 32 * j;
-            xreg[j] = z;
-            hreg[j] = z;
-            if (kt + c0 < ke) {
-                if (m < mrow1)
-                    xreg[j] = load16(xq + m * a.k + kt + c0);
-                if (nr < a.n)
-                    hreg[j] = load16(a.hi + (e * a.n + nr) * a.k + kt + c0);
-            }
-        }
-    };
-    auto sstore = [&](int b) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            *reinterpret_cast<u32x4 *>(&xs[b][(r0 + 32 * j) * P8 + c0]) = xreg[j];
-            *reinterpret_cast<u32x4 *>(&hs[b][(r0 + 32 * j) * P8 + c0]) = hreg[j];
-        }
-    };
-
-    const int wn = wave & 1;
-    const int wm = wave >> 1;
-    f32x4 acc[4][4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-            acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    const int64_t ntk = ke > kb0 ? (ke - kb0 + BK8 - 1) / BK8 : 0;
-    if (ntk > 0) {
-        gload(kb0);
-        sstore(0);
-    }
-    __syncthreads();
-    for (int64_t t = 0; t < ntk; ++t) {
-        const int b = (int)(t & 1);
-        if (t + 1 < ntk)
-            gload(kb0 + (t + 1) * BK8);
-        i32x8 av[4];
-#pragma unroll
-        for (int nt = 0; nt < 4; ++nt) {
-            const int row = wn * 64 + nt * 16 + li;
-            const u32x4 p = *reinterpret_cast<const u32x4 *>(&hs[b][row * P8 + lg * 32]);
-            const u32x4 q = *reinterpret_cast<const u32x4 *>(&hs[b][row * P8 + lg * 32 + 16]);
-            av[nt] = i32x8{(int)p.x, (int)p.y, (int)p.z, (int)p.w,
-                           (int)q.x, (int)q.y, (int)q.z, (int)q.w};
-        }
-#pragma unroll
-        for (int mt = 0; mt < 4; ++mt) {
-            const int row = wm * 64 + mt * 16 + li;
-            const u32x4 p = *reinterpret_cast<const u32x4 *>(&xs[b][row * P8 + lg * 32]);
-            const u32x4 q = *reinterpret_cast<const u32x4 *>(&xs[b][row * P8 + lg * 32 + 16]);
-            const i32x8 bv = {(int)p.x, (int)p.y, (int)p.z, (int)p.w,
-                              (int)q.x, (int)q.y, (int)q.z, (int)q.w};
-#pragma unroll
-            for (int nt = 0; nt < 4; ++nt)
-                acc[nt][mt] = mfma16x16x128_bf8_fp8(av[nt], bv, acc[nt][mt]);
-        }
-        if (t + 1 < ntk)
-            sstore(b ^ 1);
-        __syncthreads();
-    }
-
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
-        const int64_t m = mrow0 + wm * 64 + mt * 16 + li;
-        const float sc = m < mrow1 ? a.scale[m] : 0.f;
-#pragma unroll
-        for (int nt = 0; nt < 4; ++nt)
-            store_tile_out(a, s, m, n0 + wn * 64 + nt * 16 + lg * 4, acc[nt][mt] * sc, mrow1);
-    }
-}
-
 int64_t token_tiles(int64_t rows, int64_t experts, bool grouped, int bm = BM)
 {
     return grouped ? (rows + bm - 1) / bm + experts : (rows + bm - 1) / bm;
-}
-
-template <int MODE, int BMT>
-void launch_dma(const GemmArgs &a, const LinearPlan &plan, dim3 grid, hipStream_t stream)
-{
-    if (MODE == MODE_FULL && plan.range_addr)
-        hipLaunchKernelGGL((gemm_f16_dma_kernel<MODE, BMT, true>), grid, dim3(256), 0, stream, a);
-    else
-        hipLaunchKernelGGL((gemm_f16_dma_kernel<MODE, BMT, false>), grid, dim3(256), 0, stream, a);
 }
 
 }  // namespace
 
 int gemm_rows_per_block(int variant)
 {
-    return (variant == GEMM_G3_256x256 || variant == GEMM_G3_256x128 ||
-            variant == GEMM_G3_256x256_W16)
-               ? 256
-               : BN;  // GEMM_G4_128x128 included
+    return (variant == GEMM_G3_256x256 || variant == GEMM_G3_256x128) ? 256 : 128;
 }
 int gemm_tokens_per_block(int variant)
 {
-    if (variant == GEMM_G4_128x64 || variant == GEMM_G4S_128x64)
-        return 64;
-    if (variant == GEMM_G4_128x32 || variant == GEMM_G4S_128x32)
-        return 32;
-    return (variant == GEMM_DMA_256 || variant == GEMM_G3_256x256 || variant == GEMM_G3_128x256 ||
-            variant == GEMM_G3_256x256_W16)
-               ? 256
-               : BM;
+    switch (variant) {
+    case GEMM_G3_256x256: return 256;
+    case GEMM_G4_128x64:
+    case GEMM_G4S_128x64: return 64;
+    case GEMM_G4_128x32:
+    case GEMM_G4S_128x32: return 32;
+    default: return 128;
+    }
 }
 
 namespace {
 
-template <int KIND, int BN_, int BM_, int WN, int WM, int NS>
-hipError_t launch_g3(const GemmArgs &a, const LinearPlan &plan, bool grouped, hipStream_t stream)
+// dense calls: a 1-D grid, padded to a multiple of the 8 XCDs
+dim3 dense_grid(int64_t tiles)
+{
+    return dim3((unsigned)((tiles + 7) / 8 * 8), 1, 1);
+}
+
+template <int ENC, int BN_, int BM_, int WN, int WM, int NS>
+hipError_t launch_g3(const GemmArgs &a, const LinearPlan &plan, hipStream_t stream)
 {
     const int64_t nt = (a.n + BN_ - 1) / BN_;
-    dim3 grid((unsigned)(nt * plan.splits),
-              (unsigned)token_tiles(a.rows, a.experts, grouped, BM_), 1);
-    if (!grouped) {
-        const int64_t total = nt * plan.splits * ((a.rows + BM_ - 1) / BM_);
-        grid = dim3((unsigned)((total + 7) / 8 * 8), 1, 1);
-    }
-    if (KIND == G3_FULL && plan.range_addr)
-        hipLaunchKernelGGL((gemm3_kernel<KIND, BN_, BM_, WN, WM, NS, true>), grid,
-                           dim3(WN * WM * 64), 0, stream, a);
-    else
-        hipLaunchKernelGGL((gemm3_kernel<KIND, BN_, BM_, WN, WM, NS, false>), grid,
-                           dim3(WN * WM * 64), 0, stream, a);
+    const dim3 grid = dense_grid(nt * plan.splits * ((a.rows + BM_ - 1) / BM_));
+    hipLaunchKernelGGL((gemm3_kernel<ENC, BN_, BM_, WN, WM, NS>), grid, dim3(WN * WM * 64), 0,
+                       stream, a);
     return hipGetLastError();
 }
 
-template <int MODE, int BM, int WS, int XS, bool SPEC>
+template <int ENC>
+hipError_t launch_g3_variant(const GemmArgs &a, const LinearPlan &plan, hipStream_t stream)
+{
+    switch (plan.variant) {
+    case GEMM_G3_256x256: return launch_g3<ENC, 256, 256, 2, 4, 2>(a, plan, stream);
+    case GEMM_G3_256x128: return launch_g3<ENC, 256, 128, 4, 2, 3>(a, plan, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+template <int MODE, int ENC, int BM, int WS, int XS, bool SPEC>
 hipError_t launch_g4(const GemmArgs &a, const LinearPlan &plan, bool grouped, hipStream_t stream)
 {
     const int64_t nt = (a.n + 127) / 128;
-    dim3 grid((unsigned)(nt * plan.splits), (unsigned)token_tiles(a.rows, a.experts, grouped, BM),
-              1);
-    if (!grouped) {
-        const int64_t total = nt * plan.splits * ((a.rows + BM - 1) / BM);
-        grid = dim3((unsigned)((total + 7) / 8 * 8), 1, 1);
-    }
+    const dim3 grid = grouped ? dim3((unsigned)(nt * plan.splits),
+                                     (unsigned)token_tiles(a.rows, a.experts, true, BM), 1)
+                              : dense_grid(nt * plan.splits * ((a.rows + BM - 1) / BM));
     const dim3 block(SPEC ? 768 : 512);
     if (MODE == MODE_FULL && plan.range_addr)
-        hipLaunchKernelGGL((gemm4_kernel<MODE, BM, WS, XS, true, SPEC>), grid, block, 0, stream, a);
+        hipLaunchKernelGGL((gemm4_kernel<MODE, ENC, BM, WS, XS, true, SPEC>), grid, block, 0,
+                           stream, a);
     else
-        hipLaunchKernelGGL((gemm4_kernel<MODE, BM, WS, XS, false, SPEC>), grid, block, 0, stream, a);
+        hipLaunchKernelGGL((gemm4_kernel<MODE, ENC, BM, WS, XS, false, SPEC>), grid, block, 0,
+                           stream, a);
     return hipGetLastError();
 }
 
-// ring depths per (mode, token tile), within 160 KiB: weights want depth (HBM),
-// tokens at least a second slot ahead where it fits
-template <int MODE>
+// (token tile, weight slots, token slots) per mode, each within 160 KiB:
+// weights want depth (HBM), tokens at least a second slot ahead where it fits
+template <int MODE, int ENC>
 hipError_t launch_g4_variant(const GemmArgs &a, const LinearPlan &plan, bool grouped,
                              hipStream_t stream)
 {
-    // (token tile, weight slots, token slots) per mode, each within 160 KiB
     if constexpr (MODE == MODE_FULL) {
         switch (plan.variant) {
-        case GEMM_G4_128x128: return launch_g4<MODE, 128, 3, 2, false>(a, plan, grouped, stream);
-        case GEMM_G4_128x64: return launch_g4<MODE, 64, 4, 2, false>(a, plan, grouped, stream);
-        case GEMM_G4_128x32: return launch_g4<MODE, 32, 4, 4, false>(a, plan, grouped, stream);
-        case GEMM_G4S_128x128: return launch_g4<MODE, 128, 3, 2, true>(a, plan, grouped, stream);
-        case GEMM_G4S_128x64: return launch_g4<MODE, 64, 4, 2, true>(a, plan, grouped, stream);
-        case GEMM_G4S_128x32: return launch_g4<MODE, 32, 4, 4, true>(a, plan, grouped, stream);
+        case GEMM_G4_128x128: return launch_g4<MODE, ENC, 128, 3, 2, false>(a, plan, grouped, stream);
+        case GEMM_G4_128x64: return launch_g4<MODE, ENC, 64, 4, 2, false>(a, plan, grouped, stream);
+        case GEMM_G4_128x32: return launch_g4<MODE, ENC, 32, 4, 4, false>(a, plan, grouped, stream);
+        case GEMM_G4S_128x128: return launch_g4<MODE, ENC, 128, 3, 2, true>(a, plan, grouped, stream);
+        case GEMM_G4S_128x64: return launch_g4<MODE, ENC, 64, 4, 2, true>(a, plan, grouped, stream);
+        case GEMM_G4S_128x32: return launch_g4<MODE, ENC, 32, 4, 4, true>(a, plan, grouped, stream);
         default: return hipErrorInvalidValue;
         }
     } else {
         switch (plan.variant) {
-        case GEMM_G4_128x128: return launch_g4<MODE, 128, 4, 3, false>(a, plan, grouped, stream);
-        case GEMM_G4_128x64: return launch_g4<MODE, 64, 6, 4, false>(a, plan, grouped, stream);
-        case GEMM_G4_128x32: return launch_g4<MODE, 32, 8, 4, false>(a, plan, grouped, stream);
-        case GEMM_G4S_128x128: return launch_g4<MODE, 128, 4, 3, true>(a, plan, grouped, stream);
-        case GEMM_G4S_128x64: return launch_g4<MODE, 64, 6, 4, true>(a, plan, grouped, stream);
-        case GEMM_G4S_128x32: return launch_g4<MODE, 32, 8, 4, true>(a, plan, grouped, stream);
+        case GEMM_G4_128x128: return launch_g4<MODE, ENC, 128, 4, 3, false>(a, plan, grouped, stream);
+        case GEMM_G4_128x64: return launch_g4<MODE, ENC, 64, 6, 4, false>(a, plan, grouped, stream);
+        case GEMM_G4_128x32: return launch_g4<MODE, ENC, 32, 8, 4, false>(a, plan, grouped, stream);
+        case GEMM_G4S_128x128: return launch_g4<MODE, ENC, 128, 4, 3, true>(a, plan, grouped, stream);
+        case GEMM_G4S_128x64: return launch_g4<MODE, ENC, 64, 6, 4, true>(a, plan, grouped, stream);
+        case GEMM_G4S_128x32: return launch_g4<MODE, ENC, 32, 8, 4, true>(a, plan, grouped, stream);
         default: return hipErrorInvalidValue;
         }
-    }
-}
-
-template <int KIND>
-hipError_t launch_g3_variant(const GemmArgs &a, const LinearPlan &plan, bool grouped,
-                             hipStream_t stream)
-{
-    constexpr bool TWO = KIND == G3_FULL;  // two byte planes: shallower rings
-    switch (plan.variant) {
-    case GEMM_G3_256x256: return launch_g3<KIND, 256, 256, 2, 4, TWO ? 2 : (KIND == G3_FP8 ? 2 : 3)>(a, plan, grouped, stream);
-    case GEMM_G3_128x256: return launch_g3<KIND, 128, 256, 2, 4, 3>(a, plan, grouped, stream);
-    case GEMM_G3_256x128: return launch_g3<KIND, 256, 128, 4, 2, 3>(a, plan, grouped, stream);
-    case GEMM_G3_128x128: return launch_g3<KIND, 128, 128, 2, 4, 3>(a, plan, grouped, stream);
-    case GEMM_G3_256x256_W16: return launch_g3<KIND, 256, 256, 4, 4, TWO ? 2 : (KIND == G3_FP8 ? 2 : 3)>(a, plan, grouped, stream);
-    default: return hipErrorInvalidValue;
     }
 }
 
@@ -1274,44 +744,15 @@ hipError_t launch_gemm_f16(const LinearProblem &p, const LinearPlan &plan, float
     a.y = p.y;
     a.partial = partial;
     a.scale = nullptr;
-    const int64_t nt = (p.n + BN - 1) / BN;
-    if (plan.variant >= GEMM_G4_128x128)
-        return p.mode == MODE_FULL ? launch_g4_variant<MODE_FULL>(a, plan, p.offsets != nullptr, stream)
-                                   : launch_g4_variant<MODE_FAST>(a, plan, p.offsets != nullptr, stream);
-    if (plan.variant >= GEMM_G3_256x256)
-        return p.mode == MODE_FULL ? launch_g3_variant<G3_FULL>(a, plan, p.offsets != nullptr, stream)
-                                   : launch_g3_variant<G3_FAST>(a, plan, p.offsets != nullptr, stream);
-    if (plan.variant == GEMM_DMA_128 || plan.variant == GEMM_DMA_256) {
-        const int bm = plan.variant == GEMM_DMA_256 ? 256 : 128;
-        dim3 grid((unsigned)(nt * plan.splits),
-                  (unsigned)token_tiles(p.rows, p.experts, p.offsets != nullptr, bm), 1);
-        if (p.mode == MODE_FULL) {
-            if (bm == 256)
-                launch_dma<MODE_FULL, 256>(a, plan, grid, stream);
-            else
-                launch_dma<MODE_FULL, 128>(a, plan, grid, stream);
-        } else {
-            if (bm == 256)
-                launch_dma<MODE_FAST, 256>(a, plan, grid, stream);
-            else
-                launch_dma<MODE_FAST, 128>(a, plan, grid, stream);
-        }
-        return hipGetLastError();
-    }
-    dim3 grid((unsigned)(nt * plan.splits),
-              (unsigned)token_tiles(p.rows, p.experts, p.offsets != nullptr), 1);
-    if (p.mode == MODE_FULL) {
-        if (plan.range_addr)
-            hipLaunchKernelGGL((gemm_f16_kernel<MODE_FULL, true>), grid, dim3(256), 0, stream, a);
-        else
-            hipLaunchKernelGGL((gemm_f16_kernel<MODE_FULL, false>), grid, dim3(256), 0, stream, a);
-    } else {
-        hipLaunchKernelGGL((gemm_f16_kernel<MODE_FAST, false>), grid, dim3(256), 0, stream, a);
-    }
-    return hipGetLastError();
+    const bool grouped = p.offsets != nullptr;
+    if (p.enc == ENC_E4M3)
+        return p.mode == MODE_FULL ? launch_g4_variant<MODE_FULL, ENC_E4M3>(a, plan, grouped, stream)
+                                   : launch_g4_variant<MODE_FAST, ENC_E4M3>(a, plan, grouped, stream);
+    return p.mode == MODE_FULL ? launch_g4_variant<MODE_FULL, ENC_E5M2>(a, plan, grouped, stream)
+                               : launch_g4_variant<MODE_FAST, ENC_E5M2>(a, plan, grouped, stream);
 }
 
-hipError_t launch_gemm_fp8(const uint8_t *xq, const float *scale, int64_t m, int64_t n,
+hipError_t launch_gemm_fp8(int enc, const uint8_t *xq, const float *scale, int64_t m, int64_t n,
                            int64_t k, const uint8_t *hi, uint16_t *y, const LinearPlan &plan,
                            float *partial, hipStream_t stream)
 {
@@ -1329,12 +770,8 @@ hipError_t launch_gemm_fp8(const uint8_t *xq, const float *scale, int64_t m, int
     a.y = y;
     a.partial = partial;
     a.scale = scale;
-    if (plan.variant >= GEMM_G3_256x256)
-        return launch_g3_variant<G3_FP8>(a, plan, false, stream);
-    const int64_t nt = (n + BN - 1) / BN;
-    dim3 grid((unsigned)(nt * plan.splits), (unsigned)token_tiles(m, 1, false), 1);
-    hipLaunchKernelGGL(gemm_fp8_kernel, grid, dim3(256), 0, stream, a);
-    return hipGetLastError();
+    return enc == ENC_E4M3 ? launch_g3_variant<ENC_E4M3>(a, plan, stream)
+                           : launch_g3_variant<ENC_E5M2>(a, plan, stream);
 }
 
 }  // namespace dps

@@ -11,10 +11,14 @@
 namespace dps {
 
 // ---- elementwise ------------------------------------------------------------
-hipError_t launch_split(const uint16_t *w, int64_t numel, uint8_t *hi, const ResidualView &res,
-                        hipStream_t stream);
-hipError_t launch_merge(const uint8_t *hi, const ResidualView &res, int64_t numel,
+hipError_t launch_split(int enc, const uint16_t *w, int64_t numel, uint8_t *hi,
+                        const ResidualView &res, hipStream_t stream);
+hipError_t launch_merge(int enc, const uint8_t *hi, const ResidualView &res, int64_t numel,
                         uint16_t *w_out, hipStream_t stream);
+// *enc_out = ENC_E4M3 if every word nests losslessly into E4M3 with a finite
+// E4M3 part, else ENC_E5M2 (two launches: set, then clear on any misfit).
+hipError_t launch_select_enc(const uint16_t *w, int64_t numel, int32_t *enc_out,
+                             hipStream_t stream);
 hipError_t launch_quant_rows(const uint16_t *x, int64_t m, int64_t k, uint8_t *xq, float *scale,
                              hipStream_t stream);
 // y[r][c] = fp16(sum_s partial[s][r][c]) for r < rows, c < n, s in order.
@@ -26,6 +30,7 @@ hipError_t launch_splitk_reduce(const float *partial, int splits, int64_t rows, 
 // expert owning rows [0, rows)), weights [experts][n][k].
 struct LinearProblem {
     int mode;
+    int enc;
     const uint16_t *x;
     const int32_t *offsets;  // device, experts + 1 entries, or nullptr
     int64_t rows;
@@ -36,31 +41,24 @@ struct LinearProblem {
 };
 
 enum KernelKind { KIND_SKINNY = 0, KIND_GEMM_F16 = 1, KIND_GEMM_FP8 = 2 };
-// FP16 GEMM variants: register-staged 128-token tiles, or the LDS-DMA pipeline
-// with 128- or 256-token tiles (128 weight rows each).
+// GEMM tile variants (weight rows x tokens per block).
 enum GemmVariant {
-    GEMM_REG_128 = 0,
-    GEMM_DMA_128 = 1,
-    GEMM_DMA_256 = 2,
-    // eight-wave LDS-DMA kernels: weight rows x tokens per block
-    GEMM_G3_256x256 = 3,
-    GEMM_G3_128x256 = 4,
-    GEMM_G3_256x128 = 5,
-    GEMM_G3_128x128 = 6,
-    GEMM_G3_256x256_W16 = 7,  // 256 x 256 with sixteen waves (four per SIMD)
-    // 128 weight rows x 128/64/32 tokens, 128-element stages with wide-row
-    // loads, K split over waves
-    GEMM_G4_128x128 = 8,
-    GEMM_G4_128x64 = 9,
-    GEMM_G4_128x32 = 10,
+    // FP8 activations: eight-wave LDS-DMA kernel
+    GEMM_G3_256x256 = 0,
+    GEMM_G3_256x128 = 1,
+    // FP16 activations: 128-element stages with wide-row loads, K split over
+    // waves
+    GEMM_G4_128x128 = 2,
+    GEMM_G4_128x64 = 3,
+    GEMM_G4_128x32 = 4,
     // the same with four dedicated DMA waves
-    GEMM_G4S_128x128 = 11,
-    GEMM_G4S_128x64 = 12,
-    GEMM_G4S_128x32 = 13
+    GEMM_G4S_128x128 = 5,
+    GEMM_G4S_128x64 = 6,
+    GEMM_G4S_128x32 = 7
 };
-// Decode-kernel variants 0..3 keep the weight stream in registers (tile
-// shapes differ); SKINNY_RING streams it through per-wave LDS rings.
-enum { SKINNY_RING = 4, SKINNY_RING_HALF = 5 };
+// Decode-kernel variants 0 and 1 keep the weight stream in registers (16 or
+// 32 weight rows per wave); SKINNY_RING streams it through per-wave LDS rings.
+enum { SKINNY_RING = 2 };
 
 // Kernel choice and work split for one call.  plan_linear is the single
 // place that decides; dps_workspace_bytes and the launch both call it.
@@ -81,7 +79,7 @@ hipError_t launch_skinny(const LinearProblem &p, const LinearPlan &plan, float *
                          hipStream_t stream);
 hipError_t launch_gemm_f16(const LinearProblem &p, const LinearPlan &plan, float *partial,
                            hipStream_t stream);
-hipError_t launch_gemm_fp8(const uint8_t *xq, const float *scale, int64_t m, int64_t n,
+hipError_t launch_gemm_fp8(int enc, const uint8_t *xq, const float *scale, int64_t m, int64_t n,
                            int64_t k, const uint8_t *hi, uint16_t *y, const LinearPlan &plan,
                            float *partial, hipStream_t stream);
 

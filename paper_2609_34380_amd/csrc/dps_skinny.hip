@@ -107,7 +107,7 @@ struct WBatch {
     }
 };
 
-template <int MODE, int RT, int MT, int U, bool RANGE>
+template <int MODE, int ENC, int RT, int MT, int U, bool RANGE>
 __device__ __forceinline__ void compute_batch(const WBatch<MODE, RT, U, RANGE> &w,
                                               const uint16_t *xs, int xpitch, int xrow_last,
                                               int64_t kb, int64_t kb0, int64_t ke,
@@ -132,8 +132,8 @@ __device__ __forceinline__ void compute_batch(const WBatch<MODE, RT, U, RANGE> &
         for (int rt = 0; rt < RT; ++rt) {
             const u32x4 h = w.h[u][rt];
             const u32x4 l = MODE == MODE_FULL ? w.l[u][rt] : u32x4{0u, 0u, 0u, 0u};
-            const half8 a0 = merge8(h.x, h.y, l.x, l.y);
-            const half8 a1 = merge8(h.z, h.w, l.z, l.w);
+            const half8 a0 = weight8<MODE, ENC>(h.x, h.y, l.x, l.y);
+            const half8 a1 = weight8<MODE, ENC>(h.z, h.w, l.z, l.w);
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
                 acc[rt][mt] = mfma16x16x32(a0, b0[mt], acc[rt][mt]);
@@ -143,7 +143,7 @@ __device__ __forceinline__ void compute_batch(const WBatch<MODE, RT, U, RANGE> &
     }
 }
 
-template <int MODE, int RT, int MT, int U, bool RANGE>
+template <int MODE, int ENC, int RT, int MT, int U, bool RANGE>
 __global__ __launch_bounds__(kWaves * 64) void skinny_kernel(SkinnyArgs a)
 {
     extern __shared__ __attribute__((aligned(16))) uint16_t xs[];
@@ -221,11 +221,11 @@ __global__ __launch_bounds__(kWaves * 64) void skinny_kernel(SkinnyArgs a)
         wa.load(st, a.res, kb0, ke, klast, nbatch > 0, lg);
         for (int64_t b = 0; b < nbatch; b += 2) {
             wb.load(st, a.res, kb0 + (b + 1) * KB, ke, klast, b + 1 < nbatch, lg);
-            compute_batch<MODE, RT, MT, U, RANGE>(wa, xs, xpitch, xrow_last, kb0 + b * KB, kb0,
+            compute_batch<MODE, ENC, RT, MT, U, RANGE>(wa, xs, xpitch, xrow_last, kb0 + b * KB, kb0,
                                                   ke, xok, li, lg, acc);
             wa.load(st, a.res, kb0 + (b + 2) * KB, ke, klast, b + 2 < nbatch, lg);
             if (b + 1 < nbatch)
-                compute_batch<MODE, RT, MT, U, RANGE>(wb, xs, xpitch, xrow_last,
+                compute_batch<MODE, ENC, RT, MT, U, RANGE>(wb, xs, xpitch, xrow_last,
                                                       kb0 + (b + 1) * KB, kb0, ke, xok, li, lg,
                                                       acc);
         }
@@ -286,7 +286,7 @@ __device__ __attribute__((aligned(16))) const uint8_t g_zero16_s[16] = {0};
 #define DPS_WAIT_VM(n) \
     __builtin_amdgcn_s_waitcnt(((n) & 0xF) | ((((n) >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8))
 
-template <int MODE, int MT, int RING, bool RANGE>
+template <int MODE, int ENC, int MT, int RING, bool RANGE>
 __global__ __launch_bounds__(kWaves * 64) void ring_kernel(SkinnyArgs a)
 {
     constexpr int PLANES = MODE == MODE_FULL ? 2 : 1;
@@ -415,8 +415,8 @@ __global__ __launch_bounds__(kWaves * 64) void ring_kernel(SkinnyArgs a)
                 u32x4 l = {0u, 0u, 0u, 0u};
                 if (MODE == MODE_FULL)
                     l = *reinterpret_cast<const u32x4 *>(st + RING_STAGE_PLANE + li * RING_SK + slot);
-                const half8 a0 = merge8(h.x, h.y, l.x, l.y);
-                const half8 a1 = merge8(h.z, h.w, l.z, l.w);
+                const half8 a0 = weight8<MODE, ENC>(h.x, h.y, l.x, l.y);
+                const half8 a1 = weight8<MODE, ENC>(h.z, h.w, l.z, l.w);
                 const int64_t kk = kt + q * 64 + lg * 16;
                 const bool kin = kk < ke;
                 const int64_t kc = (kin ? kk : kb0) - kb0;
@@ -469,14 +469,14 @@ __global__ __launch_bounds__(kWaves * 64) void ring_kernel(SkinnyArgs a)
     }
 }
 
-// Tile variants (rows per wave = 16 * RT, K elements per batch = 64 * U).
+// Register-stream tile variants (rows per wave = 16 * RT, K elements per
+// batch = 64 * U); SKINNY_RING streams through the LDS rings instead.
 struct SkinnyVariant {
     int rt, u;
 };
-constexpr SkinnyVariant kVariants[] = {{2, 4}, {1, 4}, {2, 2}, {1, 8}};
-constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
+constexpr SkinnyVariant kVariants[] = {{1, 4}, {2, 2}};
 
-template <int MODE, int RT, int MT, int U>
+template <int MODE, int ENC, int RT, int MT, int U>
 hipError_t launch_t(const SkinnyArgs &args, const LinearPlan &plan, int64_t experts,
                     hipStream_t stream)
 {
@@ -485,98 +485,90 @@ hipError_t launch_t(const SkinnyArgs &args, const LinearPlan &plan, int64_t expe
               (unsigned)experts);
     const size_t lds = (size_t)args.x_rows * (size_t)(args.ksplit + 8) * 2;
     if (plan.range_addr)
-        hipLaunchKernelGGL((skinny_kernel<MODE, RT, MT, U, true>), grid, dim3(kWaves * 64), lds,
-                           stream, args);
+        hipLaunchKernelGGL((skinny_kernel<MODE, ENC, RT, MT, U, true>), grid, dim3(kWaves * 64),
+                           lds, stream, args);
     else
-        hipLaunchKernelGGL((skinny_kernel<MODE, RT, MT, U, false>), grid, dim3(kWaves * 64), lds,
-                           stream, args);
+        hipLaunchKernelGGL((skinny_kernel<MODE, ENC, RT, MT, U, false>), grid, dim3(kWaves * 64),
+                           lds, stream, args);
     return hipGetLastError();
 }
 
-// LDS per block: the deep rings take the whole 160 KiB of a gfx950 CU (one
-// block per CU); the shallow rings take half, so two blocks share a CU.
-template <bool DEEP>
-constexpr int ring_lds() { return DEEP ? 160 * 1024 : 80 * 1024; }
+// The rings take half of a gfx950 CU's 160 KiB LDS, so two blocks share a CU.
+constexpr int kRingLds = 80 * 1024;
 
-template <int MODE, bool DEEP>
-constexpr int ring_depth() { return MODE == MODE_FULL ? (DEEP ? 3 : 2) : (DEEP ? 6 : 3); }
+template <int MODE>
+constexpr int ring_depth() { return MODE == MODE_FULL ? 2 : 3; }
 
-template <int MODE, bool DEEP>
+template <int MODE>
 constexpr int ring_bytes()
 {
-    return kWaves * ring_depth<MODE, DEEP>() * RING_STAGE_PLANE * (MODE == MODE_FULL ? 2 : 1);
+    return kWaves * ring_depth<MODE>() * RING_STAGE_PLANE * (MODE == MODE_FULL ? 2 : 1);
 }
 
-template <int MODE, int MT, bool DEEP>
+template <int MODE, int ENC, int MT>
 hipError_t launch_ring(const SkinnyArgs &args, const LinearPlan &plan, int64_t experts,
                        hipStream_t stream)
 {
-    constexpr int RING = ring_depth<MODE, DEEP>();
-    constexpr int kRingLds = ring_lds<DEEP>();
+    constexpr int RING = ring_depth<MODE>();
     const size_t xbytes = ((size_t)args.x_rows * (size_t)(args.ksplit + 8) * 2 + 255) & ~(size_t)255;
-    const size_t lds = xbytes + ring_bytes<MODE, DEEP>();
+    const size_t lds = xbytes + ring_bytes<MODE>();
     if (lds > (size_t)kRingLds)
         return hipErrorInvalidValue;
     dim3 grid((unsigned)((args.n + kWaves * 16 - 1) / (kWaves * 16)), (unsigned)plan.splits,
               (unsigned)experts);
+    // more than 64 KiB of dynamic LDS needs the per-kernel limit raised once
     if (plan.range_addr) {
-        static bool attr = false;
-        if (!attr) {
-            hipFuncSetAttribute((const void *)ring_kernel<MODE, MT, RING, true>,
+        static const hipError_t attr =
+            hipFuncSetAttribute((const void *)ring_kernel<MODE, ENC, MT, RING, true>,
                                 hipFuncAttributeMaxDynamicSharedMemorySize, kRingLds);
-            attr = true;
-        }
-        hipLaunchKernelGGL((ring_kernel<MODE, MT, RING, true>), grid, dim3(kWaves * 64), lds,
+        if (attr != hipSuccess)
+            return attr;
+        hipLaunchKernelGGL((ring_kernel<MODE, ENC, MT, RING, true>), grid, dim3(kWaves * 64), lds,
                            stream, args);
     } else {
-        static bool attr = false;
-        if (!attr) {
-            hipFuncSetAttribute((const void *)ring_kernel<MODE, MT, RING, false>,
+        static const hipError_t attr =
+            hipFuncSetAttribute((const void *)ring_kernel<MODE, ENC, MT, RING, false>,
                                 hipFuncAttributeMaxDynamicSharedMemorySize, kRingLds);
-            attr = true;
-        }
-        hipLaunchKernelGGL((ring_kernel<MODE, MT, RING, false>), grid, dim3(kWaves * 64), lds,
-                           stream, args);
+        if (attr != hipSuccess)
+            return attr;
+        hipLaunchKernelGGL((ring_kernel<MODE, ENC, MT, RING, false>), grid, dim3(kWaves * 64),
+                           lds, stream, args);
     }
     return hipGetLastError();
 }
 
-template <int MODE, int MT>
+template <int MODE, int ENC, int MT>
 hipError_t launch_mt(const SkinnyArgs &args, const LinearPlan &plan, int64_t experts,
                      hipStream_t stream)
 {
     switch (plan.variant) {
-    case SKINNY_RING: return launch_ring<MODE, MT, true>(args, plan, experts, stream);
-    case SKINNY_RING_HALF: return launch_ring<MODE, MT, false>(args, plan, experts, stream);
-    case 0: return launch_t<MODE, 2, MT, 4>(args, plan, experts, stream);
-    case 1: return launch_t<MODE, 1, MT, 4>(args, plan, experts, stream);
-    case 2: return launch_t<MODE, 2, MT, 2>(args, plan, experts, stream);
-    case 3: return launch_t<MODE, 1, MT, 8>(args, plan, experts, stream);
+    case SKINNY_RING: return launch_ring<MODE, ENC, MT>(args, plan, experts, stream);
+    case 0: return launch_t<MODE, ENC, 1, MT, 4>(args, plan, experts, stream);
+    case 1: return launch_t<MODE, ENC, 2, MT, 2>(args, plan, experts, stream);
     default: return hipErrorInvalidValue;
     }
 }
 
-template <int MODE>
+template <int MODE, int ENC>
 hipError_t launch_mode(const SkinnyArgs &args, const LinearPlan &plan, int mt, int64_t experts,
                        hipStream_t stream)
 {
     switch (mt) {
-    case 1: return launch_mt<MODE, 1>(args, plan, experts, stream);
-    case 2: return launch_mt<MODE, 2>(args, plan, experts, stream);
-    default: return launch_mt<MODE, 4>(args, plan, experts, stream);
+    case 1: return launch_mt<MODE, ENC, 1>(args, plan, experts, stream);
+    case 2: return launch_mt<MODE, ENC, 2>(args, plan, experts, stream);
+    default: return launch_mt<MODE, ENC, 4>(args, plan, experts, stream);
     }
 }
 
 }  // namespace
 
-int skinny_variant_count() { return kNumVariants; }
 int skinny_rows_per_block(int variant)
 {
-    return variant >= SKINNY_RING ? kWaves * 16 : kWaves * kVariants[variant].rt * 16;
+    return variant == SKINNY_RING ? kWaves * 16 : kWaves * kVariants[variant].rt * 16;
 }
 int skinny_k_per_batch(int variant)
 {
-    return variant >= SKINNY_RING ? RING_SK : kVariants[variant].u * 64;
+    return variant == SKINNY_RING ? RING_SK : kVariants[variant].u * 64;
 }
 // Largest K range (multiple of the batch) whose X slice fits the block's LDS.
 int64_t skinny_max_ksplit(int variant, int mode, int64_t pass_rows)
@@ -584,11 +576,8 @@ int64_t skinny_max_ksplit(int variant, int mode, int64_t pass_rows)
     const int64_t kpb = skinny_k_per_batch(variant);
     int64_t budget = 65536;
     if (variant == SKINNY_RING)
-        budget = ring_lds<true>() - 256 -
-                 (mode == MODE_FULL ? ring_bytes<MODE_FULL, true>() : ring_bytes<MODE_FAST, true>());
-    if (variant == SKINNY_RING_HALF)
-        budget = ring_lds<false>() - 256 -
-                 (mode == MODE_FULL ? ring_bytes<MODE_FULL, false>() : ring_bytes<MODE_FAST, false>());
+        budget = kRingLds - 256 -
+                 (mode == MODE_FULL ? ring_bytes<MODE_FULL>() : ring_bytes<MODE_FAST>());
     const int64_t kmax = (budget / 2 / pass_rows - 8) / kpb * kpb;
     return kmax < kpb ? 0 : kmax;  // 0: this variant cannot hold the X slice
 }
@@ -618,8 +607,12 @@ hipError_t launch_skinny(const LinearProblem &p, const LinearPlan &plan, float *
     args.splits = plan.splits;
     args.x_rows = skinny_pass_rows(p.rows, p.offsets != nullptr);
     const int mt = (args.x_rows + 15) / 16;
-    return p.mode == MODE_FULL ? launch_mode<MODE_FULL>(args, plan, mt, p.experts, stream)
-                               : launch_mode<MODE_FAST>(args, plan, mt, p.experts, stream);
+    if (p.enc == ENC_E4M3)
+        return p.mode == MODE_FULL
+                   ? launch_mode<MODE_FULL, ENC_E4M3>(args, plan, mt, p.experts, stream)
+                   : launch_mode<MODE_FAST, ENC_E4M3>(args, plan, mt, p.experts, stream);
+    return p.mode == MODE_FULL ? launch_mode<MODE_FULL, ENC_E5M2>(args, plan, mt, p.experts, stream)
+                               : launch_mode<MODE_FAST, ENC_E5M2>(args, plan, mt, p.experts, stream);
 }
 
 }  // namespace dps

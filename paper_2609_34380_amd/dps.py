@@ -16,13 +16,14 @@ LIB_PATH = os.path.join(_HERE, "libdps.so")
 MODE_FULL = 0
 MODE_FAST = 1
 ENC_E5M2 = 0
+ENC_E4M3 = 1
 ACT_FP16 = 0
 ACT_FP8_ROWSCALE = 1
 
 _STATUS = {0: "DPS_OK", 1: "DPS_ERR_INVALID_ARG", 2: "DPS_ERR_ALIGNMENT",
            3: "DPS_ERR_UNSUPPORTED", 4: "DPS_ERR_WORKSPACE", 5: "DPS_ERR_HIP"}
 
-EXPORTED = ("dps_split", "dps_merge", "dps_quant_rows_e4m3", "dps_workspace_bytes",
+EXPORTED = ("dps_select_enc", "dps_split", "dps_merge", "dps_quant_rows_e4m3", "dps_workspace_bytes",
             "dps_linear", "dps_linear_grouped", "dps_status_str", "dps_last_error")
 
 
@@ -58,9 +59,11 @@ def load_library(path=LIB_PATH):
     lib = ctypes.CDLL(path)
     P, I64, I32, U32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32
     ST = ctypes.c_int
-    lib.dps_split.argtypes = [P, I64, P, ctypes.POINTER(CResidual), P]
+    lib.dps_select_enc.argtypes = [P, I64, P, P]
+    lib.dps_select_enc.restype = ST
+    lib.dps_split.argtypes = [ctypes.c_int, P, I64, P, ctypes.POINTER(CResidual), P]
     lib.dps_split.restype = ST
-    lib.dps_merge.argtypes = [P, ctypes.POINTER(CResidual), I64, P, P]
+    lib.dps_merge.argtypes = [ctypes.c_int, P, ctypes.POINTER(CResidual), I64, P, P]
     lib.dps_merge.restype = ST
     lib.dps_quant_rows_e4m3.argtypes = [P, I64, I64, P, P, P]
     lib.dps_quant_rows_e4m3.restype = ST
@@ -121,14 +124,17 @@ def _null_residual():
 
 
 class NestedWeight:
-    """A nested weight: upper-byte plane hi ([n][k] or [experts][n][k], uint8)
-    and its residual (None when only fast mode will be used)."""
+    """A nested weight: upper-byte plane hi ([n][k] or [experts][n][k], uint8),
+    its residual (None when only fast mode will be used) and the encoding
+    (ENC_E5M2 or ENC_E4M3) both were split with."""
 
-    def __init__(self, hi, residual):
+    def __init__(self, hi, residual, enc=ENC_E5M2):
         _require_cuda(hi)
         assert hi.dtype == torch.uint8 and hi.is_contiguous()
+        assert enc in (ENC_E5M2, ENC_E4M3)
         self.hi = hi
         self.residual = residual
+        self.enc = enc
         if hi.dim() == 2:
             self.experts, self.n, self.k = 1, hi.shape[0], hi.shape[1]
         elif hi.dim() == 3:
@@ -140,11 +146,23 @@ class NestedWeight:
     def c(self):
         if self._c is None:
             res = self.residual.c() if self.residual is not None else _null_residual()
-            self._c = CWeight(self.hi.data_ptr(), res, self.experts, self.n, self.k, ENC_E5M2)
+            self._c = CWeight(self.hi.data_ptr(), res, self.experts, self.n, self.k, self.enc)
         return self._c
 
 
-def split(w, residual, hi=None):
+def select_enc(w, out=None):
+    """Per-layer encoding for FP16 weights w (dps_select_enc): an int32 device
+    tensor of one element holding ENC_E4M3 or ENC_E5M2 once the stream runs."""
+    lib = load_library()
+    _require_cuda(w)
+    assert w.dtype == torch.float16 and w.is_contiguous()
+    if out is None:
+        out = torch.empty(1, dtype=torch.int32, device=w.device)
+    _check(lib.dps_select_enc(_ptr(w), w.numel(), _ptr(out), _stream()))
+    return out
+
+
+def split(w, residual, hi=None, enc=ENC_E5M2):
     """FP16 weights -> NestedWeight; the residual bytes are written into
     residual.pool through its chunk table (dps_split)."""
     lib = load_library()
@@ -153,17 +171,18 @@ def split(w, residual, hi=None):
     if hi is None:
         hi = torch.empty(w.shape, dtype=torch.uint8, device=w.device)
     res = residual.c()
-    _check(lib.dps_split(_ptr(w), w.numel(), _ptr(hi), ctypes.byref(res), _stream()))
-    return NestedWeight(hi, residual)
+    _check(lib.dps_split(enc, _ptr(w), w.numel(), _ptr(hi), ctypes.byref(res), _stream()))
+    return NestedWeight(hi, residual, enc)
 
 
 def merge(nw, out=None):
-    """NestedWeight -> the original FP16 weights (dps_merge)."""
+    """NestedWeight -> the FP16 weights its two parts describe (dps_merge)."""
     lib = load_library()
     if out is None:
         out = torch.empty(nw.hi.shape, dtype=torch.float16, device=nw.hi.device)
     res = nw.residual.c()
-    _check(lib.dps_merge(_ptr(nw.hi), ctypes.byref(res), nw.hi.numel(), _ptr(out), _stream()))
+    _check(lib.dps_merge(nw.enc, _ptr(nw.hi), ctypes.byref(res), nw.hi.numel(), _ptr(out),
+                         _stream()))
     return out
 
 

@@ -37,14 +37,16 @@ def make_residual_host(numel, log2c, n_slots=None, slot_seed=None, filler_seed=N
 class Nested:
     """One weight tensor split on both sides: GPU (dps) and oracle (CPU)."""
 
-    def __init__(self, w_fp16, log2c, n_slots=None, slot_seed=None, filler_seed=None):
+    def __init__(self, w_fp16, log2c, n_slots=None, slot_seed=None, filler_seed=None,
+                 enc=dps.ENC_E5M2):
         numel = w_fp16.numel()
         pool, slots = make_residual_host(numel, log2c, n_slots, slot_seed, filler_seed)
+        self.enc = enc
         self.res_ref = oracle.Residual(pool.copy(), slots, log2c)
-        self.hi_ref = oracle.split(u16(w_fp16).reshape(w_fp16.shape), self.res_ref)
+        self.hi_ref = oracle.split(u16(w_fp16).reshape(w_fp16.shape), self.res_ref, enc=enc)
         self.res = dps.Residual(torch.from_numpy(pool).to(DEV), torch.from_numpy(slots).to(DEV),
                                 log2c)
-        self.nw = dps.split(w_fp16.to(DEV), self.res)
+        self.nw = dps.split(w_fp16.to(DEV), self.res, enc=enc)
         self.shape = tuple(w_fp16.shape)
 
     def check_planes(self):

@@ -29,9 +29,9 @@ def lib():
 
 def test_header_declares_the_boundary():
     names = _declared()
-    for expected in ("dps_split", "dps_merge", "dps_linear", "dps_linear_grouped",
-                     "dps_quant_rows_e4m3", "dps_workspace_bytes", "dps_status_str",
-                     "dps_last_error"):
+    for expected in ("dps_select_enc", "dps_split", "dps_merge", "dps_linear",
+                     "dps_linear_grouped", "dps_quant_rows_e4m3", "dps_workspace_bytes",
+                     "dps_status_str", "dps_last_error"):
         assert expected in names
 
 
@@ -64,7 +64,7 @@ def _linear(lib, mode=0, flags=0, x=0x4000, m=4, w=None, y=0x5000, ws=None, ws_b
     (dict(mode=0, flags=1), 1),                      # FP8 activations need fast mode
     (dict(w=_weight(k=40)), 1),                      # k % 16 != 0
     (dict(w=_weight(n=0)), 1),
-    (dict(w=_weight(enc=1)), 3),                     # E4M3 nesting not built
+    (dict(w=_weight(enc=2)), 1),                     # unknown nested encoding
     (dict(w=_weight(experts=2)), 1),                 # dense call with stacked experts
     (dict(w=_weight(hi=0x1001)), 2),                 # misaligned plane
     (dict(x=0x4008), 2),
@@ -108,12 +108,20 @@ def test_split_merge_reject_bad_arguments(lib):
     # every call here fails validation (or is empty) before any launch
     res = dps.CResidual(0x2000, 1 << 8, 0x3000, 4, 8)
     bad = dps.CResidual(0x2000, 1 << 8, 0x3000, 3, 8)   # 3 chunks of 256 < 1024 bytes
-    assert lib.dps_split(0x1000, 1024, 0x4000, ctypes.byref(bad), None) == 1
-    assert lib.dps_split(0x1000, -1, 0x4000, ctypes.byref(res), None) == 1
-    assert lib.dps_split(0x1000, 0, 0x4000, ctypes.byref(res), None) == 0
-    assert lib.dps_split(0x1004, 1024, 0x4000, ctypes.byref(res), None) == 2
-    assert lib.dps_merge(0x4000, None, 1024, 0x1000, None) == 1
-    assert lib.dps_merge(0x4000, ctypes.byref(bad), 1024, 0x1000, None) == 1
+    for enc in (0, 1):
+        assert lib.dps_split(enc, 0x1000, 1024, 0x4000, ctypes.byref(bad), None) == 1
+        assert lib.dps_split(enc, 0x1000, -1, 0x4000, ctypes.byref(res), None) == 1
+        assert lib.dps_split(enc, 0x1000, 0, 0x4000, ctypes.byref(res), None) == 0
+        assert lib.dps_split(enc, 0x1004, 1024, 0x4000, ctypes.byref(res), None) == 2
+        assert lib.dps_merge(enc, 0x4000, None, 1024, 0x1000, None) == 1
+        assert lib.dps_merge(enc, 0x4000, ctypes.byref(bad), 1024, 0x1000, None) == 1
+    assert lib.dps_split(2, 0x1000, 1024, 0x4000, ctypes.byref(res), None) == 1
+    assert lib.dps_merge(-1, 0x4000, ctypes.byref(res), 1024, 0x1000, None) == 1
+    assert lib.dps_select_enc(0x1000, -1, 0x2000, None) == 1
+    assert lib.dps_select_enc(0x1000, 64, 0, None) == 1
+    assert lib.dps_select_enc(0x1000, 64, 0x2002, None) == 2
+    assert lib.dps_select_enc(0x1008, 64, 0x2000, None) == 2
+    assert lib.dps_select_enc(0, 64, 0x2000, None) == 1
     assert lib.dps_quant_rows_e4m3(0x1000, 4, 24, 0x2000, 0x3000, None) == 1
     assert lib.dps_quant_rows_e4m3(0x1000, 0, 32, 0x2000, 0x3000, None) == 0
 

@@ -1,0 +1,294 @@
+"""HIP path vs the CPU oracle for the E4M3 nesting and the per-layer encoding
+choice (Sec. IV-B "Persistent Region"; Sec. IV-C, "Dual-mode serving"
+paragraph).
+
+Bit-exact: the encoding choice, split planes and merge.  Tolerance (relative
+Frobenius <= 1e-3 and max abs <= 2e-2 against the fp64 oracle): every linear
+output.  The fast-mode weight is E4M3(hi) * 2^-8; one-hot rows check that
+value exactly against torch's float8_e4m3fn decode.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_helpers import DEV, Nested, assert_close, u16
+from paper_2609_34380_amd import dps, workloads
+
+pytestmark = pytest.mark.gpu
+
+FAST, FULL = dps.MODE_FAST, dps.MODE_FULL
+E4M3, E5M2 = dps.ENC_E4M3, dps.ENC_E5M2
+
+ALL16 = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+
+
+def _omode(mode):
+    return oracle.FAST if mode == FAST else oracle.FULL
+
+
+def _fp16(bits):
+    return torch.from_numpy(np.ascontiguousarray(bits, dtype=np.uint16).view(np.int16).copy()) \
+        .view(torch.float16)
+
+
+def _wide_weight(n, k, seed, experts=None):
+    """Weights spread over most of the E4M3 range: N(0, 0.4) clipped to +-1.8,
+    a column of FP16 subnormals whose E4M3 part is subnormal too, a column at
+    the largest fast value 1.75."""
+    w = workloads.weight_fp16(n, k, seed, std=0.4, experts=experts).float().clamp(-1.8, 1.8)
+    w[..., 1] = 3.0e-5
+    w[..., 2] = -1.75
+    return w.half()
+
+
+def _acts(m, k, seed, wide, **kw):
+    """Activations ~ N(0, 1); against wide weights scaled by 1/16, so outputs
+    stay in the O(1) range the absolute error bound is stated for."""
+    x = workloads.activations_fp16(m, k, seed=seed, **kw)
+    return (x.float() / 16).half() if wide else x
+
+
+# -----------------------------------------------------------------------------
+# encoding choice: bit-exact against the oracle
+# -----------------------------------------------------------------------------
+
+def test_select_enc_every_pattern():
+    """Each of the 65536 FP16 patterns alone, as a 1-word layer (row i of a
+    [65536][8] tensor, so every layer starts 16-byte aligned)."""
+    rows = np.zeros((ALL16.size, 8), dtype=np.uint16)
+    rows[:, 0] = ALL16
+    w = _fp16(rows).to(DEV)
+    out = torch.empty(ALL16.size, dtype=torch.int32, device=DEV)
+    for i in range(ALL16.size):
+        dps.select_enc(w[i, :1], out=out[i:i + 1])
+    torch.cuda.synchronize()
+    want = np.array([oracle.select_enc(ALL16[i:i + 1]) for i in range(ALL16.size)])
+    assert np.array_equal(out.cpu().numpy(), want)
+
+
+@pytest.mark.parametrize("numel", [0, 7, 4096 * 4096 + 5])
+def test_select_enc_layers(numel):
+    """A layer of trained-like weights qualifies; one misfit anywhere (first
+    vector, middle, ragged tail) flips it to E5M2."""
+    n = max(numel, 1)
+    w = workloads.weight_fp16(1, n, seed=numel).reshape(-1)[:numel].contiguous()
+    assert oracle.select_enc(u16(w)) == E4M3
+    got = dps.select_enc(w.to(DEV))
+    torch.cuda.synchronize()
+    assert got.item() == E4M3
+    for pos in sorted({0, numel // 2, numel - 1}) if numel else []:
+        for bad in (1.875, -2.0, float("inf"), float("nan")):
+            wb = w.clone()
+            wb[pos] = bad
+            assert oracle.select_enc(u16(wb)) == E5M2
+            got = dps.select_enc(wb.to(DEV))
+            torch.cuda.synchronize()
+            assert got.item() == E5M2, (pos, bad)
+
+
+# -----------------------------------------------------------------------------
+# split / merge: bit-exact
+# -----------------------------------------------------------------------------
+
+def test_split_merge_e4m3_all_patterns_scattered():
+    """All 65536 patterns plus a ragged tail, 256-byte chunks at random slots
+    among KV filler: planes equal the oracle's, and merge returns the oracle's
+    words (every word with a zero exponent MSB comes back unchanged)."""
+    rng = np.random.default_rng(13)
+    bits = np.concatenate([ALL16, rng.integers(0, 65536, 11).astype(np.uint16)])
+    w = _fp16(bits)
+    nst = Nested(w, 8, n_slots=600, slot_seed=14, filler_seed=15, enc=E4M3)
+    nst.check_planes()
+    back = dps.merge(nst.nw)
+    torch.cuda.synchronize()
+    want = oracle.merge(nst.hi_ref, nst.res_ref, enc=oracle.E4M3)
+    got = back.cpu().view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(got, want)
+    keep = (bits & 0x4000) == 0
+    assert np.array_equal(got[keep], bits[keep])
+
+
+def test_merge_e4m3_ignores_residual_top_bit():
+    """Residual bytes with their top bit set merge to the same words."""
+    w = workloads.weight_fp16(64, 1024, seed=16)
+    nst = Nested(w, 10, enc=E4M3)
+    pool = nst.res.pool.clone()
+    nst.res.pool |= 0x80
+    back = dps.merge(nst.nw)
+    torch.cuda.synchronize()
+    assert torch.equal(back.cpu().view(torch.int16), w.view(torch.int16))
+    nst.res.pool.copy_(pool)
+
+
+@pytest.mark.parametrize("numel,log2c,n_slots", [(1_000_003, 12, 400), (4096 * 4096, 21, 12)])
+def test_split_e4m3_large(numel, log2c, n_slots):
+    w = workloads.weight_fp16(1, numel, seed=numel).reshape(-1)
+    nst = Nested(w, log2c, n_slots=n_slots, slot_seed=17, filler_seed=18, enc=E4M3)
+    nst.check_planes()
+    back = dps.merge(nst.nw)
+    torch.cuda.synchronize()
+    assert torch.equal(back.cpu().view(torch.int16), w.view(torch.int16))
+
+
+# -----------------------------------------------------------------------------
+# linear: tolerance against the fp64 oracle
+# -----------------------------------------------------------------------------
+
+# (m, n, k, log2c, scattered, wide): decode kernel (1-4 tokens), wide-row GEMM
+# (32/64/128-token tiles); wide = weights over most of the E4M3 range
+E4M3_CASES = [
+    (4, 1024, 1024, 16, False, False),
+    (1, 1000, 1040, 12, True, True),
+    (3, 520, 2048, 8, True, True),
+    (17, 520, 4096, 21, True, False),
+    (32, 768, 2048, 14, True, True),
+    (65, 384, 1024, 12, True, True),
+    (130, 260, 2048, 8, True, False),
+    (300, 512, 512, 16, True, True),
+]
+
+
+def _case_id(c):
+    return "m%d_n%d_k%d_c%d%s%s" % (c[0], c[1], c[2], c[3], "_scat" if c[4] else "",
+                                    "_wide" if c[5] else "")
+
+
+@pytest.fixture(scope="module", params=E4M3_CASES, ids=_case_id)
+def e4m3_case(request):
+    m, n, k, log2c, scattered, wide = request.param
+    w = _wide_weight(n, k, seed=300 + n) if wide else workloads.weight_fp16(n, k, seed=300 + n)
+    x = _acts(m, k, 400 + m, wide)
+    assert oracle.select_enc(u16(w)) == oracle.E4M3
+    n_chunks = -(-(n * k) // (1 << log2c))
+    if scattered:
+        nst = Nested(w, log2c, n_slots=2 * n_chunks + 3, slot_seed=n + k, filler_seed=m,
+                     enc=E4M3)
+    else:
+        nst = Nested(w, log2c, enc=E4M3)
+    return m, n, k, w, x, nst
+
+
+def test_e4m3_linear_planes(e4m3_case):
+    e4m3_case[-1].check_planes()
+
+
+@pytest.mark.parametrize("mode", [FAST, FULL], ids=["fast", "full"])
+def test_e4m3_linear_matches_oracle(e4m3_case, mode):
+    m, n, k, w, x, nst = e4m3_case
+    y = dps.linear(x.to(DEV), nst.nw, mode)
+    torch.cuda.synchronize()
+    ref = oracle.linear(_omode(mode), u16(x), nst.hi_ref,
+                        nst.res_ref if mode == FULL else None, enc=oracle.E4M3)
+    assert_close(y, ref, "mode=%d" % mode)
+
+
+def test_e4m3_fast_equals_full_with_zero_residual(e4m3_case):
+    m, n, k, w, x, nst = e4m3_case
+    zero_res = dps.Residual(torch.zeros_like(nst.res.pool), nst.res.slots, nst.res.log2_chunk)
+    nw0 = dps.NestedWeight(nst.nw.hi, zero_res, E4M3)
+    xd = x.to(DEV)
+    y_fast = dps.linear(xd, nst.nw, FAST)
+    y_full0 = dps.linear(xd, nw0, FULL)
+    torch.cuda.synchronize()
+    assert torch.equal(y_fast.view(torch.int16), y_full0.view(torch.int16))
+
+
+def test_e4m3_fast_never_reads_residual(e4m3_case):
+    m, n, k, w, x, nst = e4m3_case
+    xd = x.to(DEV)
+    y_clean = dps.linear(xd, nst.nw, FAST)
+    y_none = dps.linear(xd, dps.NestedWeight(nst.nw.hi, None, E4M3), FAST)
+    torch.cuda.synchronize()
+    assert torch.equal(y_clean.view(torch.int16), y_none.view(torch.int16))
+
+
+@pytest.mark.parametrize("m", [1, 16, 200])
+def test_e4m3_one_hot_rows_select_weights_exactly(m):
+    """x[r] = e_{j_r}: Y[r][c] is exactly W[c][j_r] (full) or E4M3(hi) * 2^-8
+    (fast, torch's float8_e4m3fn decode)."""
+    n, k = 272, 1024
+    w = _wide_weight(n, k, seed=35)
+    nst = Nested(w, 9, n_slots=4000, slot_seed=36, filler_seed=37, enc=E4M3)
+    cols = torch.randperm(k, generator=torch.Generator().manual_seed(38))[:m]
+    x = torch.zeros((m, k), dtype=torch.float16)
+    x[torch.arange(m), cols] = 1.0
+    for mode in (FULL, FAST):
+        y = dps.linear(x.to(DEV), nst.nw, mode)
+        torch.cuda.synchronize()
+        if mode == FULL:
+            want = w[:, cols].t().contiguous().float()
+        else:
+            want = torch.from_numpy(nst.hi_ref[:, cols.numpy()].T.copy()).view(
+                torch.float8_e4m3fn).float() * 2.0 ** -8
+        assert torch.equal(y.cpu().float(), want), mode
+
+
+@pytest.mark.parametrize("m", [1, 4, 64])
+def test_e4m3_fast_weight_every_code(m):
+    """Row r of the weight holds FP16 words whose E4M3 part is code r (all 254
+    codes that are numbers; the two NaN codes give rows of zeros) with random
+    residual bits.  One-hot activations read back E4M3(r) * 2^-8 exactly in
+    fast mode, and the FP16 words exactly in full mode, on the decode kernel
+    (1 and 4 tokens) and the GEMM (64 tokens)."""
+    n, k = 256, 256
+    rng = np.random.default_rng(90 + m)
+    codes = np.arange(256, dtype=np.uint16)
+    codes[[0x7F, 0xFF]] = 0
+    # E4M3 code c = s | e[3:0] | m[9:7]  ->  FP16 word s | 0 | e[3:0] | m[9:7] | m[6:0]
+    hi_part = ((codes & 0x80) << 8) | ((codes & 0x7F) << 7)
+    words = hi_part[:, None] | rng.integers(0, 128, (n, k)).astype(np.uint16)
+    w = _fp16(words).reshape(n, k)
+    assert oracle.select_enc(words) == oracle.E4M3
+    nst = Nested(w, 12, enc=E4M3)
+    nst.check_planes()
+    cols = rng.permutation(k)[:m]
+    x = torch.zeros((m, k), dtype=torch.float16)
+    x[torch.arange(m), torch.from_numpy(cols)] = 1.0
+    fast_vals = torch.from_numpy(codes.astype(np.uint8)).view(torch.float8_e4m3fn).float() \
+        * 2.0 ** -8
+    for mode in (FAST, FULL):
+        y = dps.linear(x.to(DEV), nst.nw, mode)
+        torch.cuda.synchronize()
+        if mode == FAST:
+            want = fast_vals[None, :].expand(m, n)
+        else:
+            want = w[:, torch.from_numpy(cols)].t().float()
+        assert torch.equal(y.cpu().float(), want), mode
+
+
+@pytest.mark.parametrize("m,n,k", [(128, 256, 1024), (200, 300, 2048), (513, 640, 1152)])
+def test_e4m3_linear_fp8_matches_oracle(m, n, k):
+    """FP8 activations against E4M3 weights (E4M3 x E4M3 matrix cores)."""
+    w = _wide_weight(n, k, seed=55 + m)
+    x = _acts(m, k, 56 + m, True, outlier_frac=0.01, outlier_scale=20.0)
+    nst = Nested(w, 21, enc=E4M3)
+    y = dps.linear(x.to(DEV), nst.nw, FAST, act="fp8")
+    torch.cuda.synchronize()
+    xq, s = oracle.act_quant(u16(x))
+    ref = oracle.linear_fp8(xq, s, nst.hi_ref, enc=oracle.E4M3)
+    assert_close(y, ref)
+
+
+@pytest.mark.parametrize("counts,n,k,log2c", [
+    ((5, 0, 17, 64, 1, 3), 192, 512, 12),
+    ((100, 0, 300, 129, 7), 160, 1024, 10),
+    ((1, 1, 0, 1), 256, 768, 11),
+])
+@pytest.mark.parametrize("mode", [FAST, FULL], ids=["fast", "full"])
+def test_e4m3_grouped_matches_oracle(counts, n, k, log2c, mode):
+    e = len(counts)
+    rows = sum(counts)
+    w = _wide_weight(n, k, seed=65, experts=e)
+    x = _acts(rows, k, 66, True)
+    offsets = np.zeros(e + 1, dtype=np.int64)
+    offsets[1:] = np.cumsum(counts)
+    n_chunks = -(-(e * n * k) // (1 << log2c))
+    nst = Nested(w, log2c, n_slots=n_chunks + 5, slot_seed=67, filler_seed=68, enc=E4M3)
+    nst.check_planes()
+    off_dev = torch.from_numpy(offsets.astype(np.int32)).to(DEV)
+    y = dps.linear_grouped(x.to(DEV), off_dev, nst.nw, mode)
+    torch.cuda.synchronize()
+    ref = oracle.linear_grouped(_omode(mode), u16(x), offsets, nst.hi_ref,
+                                nst.res_ref if mode == FULL else None, enc=oracle.E4M3)
+    assert_close(y, ref)
