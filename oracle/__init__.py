@@ -51,6 +51,10 @@ def _load():
     lib.oracle_split.restype = ctypes.c_int
     lib.oracle_merge.argtypes = [C, P, P, I64, P, I64, I32, I64, P]
     lib.oracle_merge.restype = ctypes.c_int
+    lib.oracle_restore.argtypes = [P, I64, I64, I64, P, I64, P, I64, I32]
+    lib.oracle_restore.restype = ctypes.c_int
+    lib.oracle_backup.argtypes = [P, I64, P, I64, I32, I64, P]
+    lib.oracle_backup.restype = ctypes.c_int
     lib.oracle_linear.argtypes = [C, C, P, I64, I64, I64, P, P, I64, P, I64, I32, P]
     lib.oracle_linear.restype = ctypes.c_int
     lib.oracle_linear_grouped.argtypes = [C, C, P, P, I64, I64, I64, P, P, I64,
@@ -158,6 +162,29 @@ def merge(hi, res: Residual, enc=E5M2):
     pool, pool_bytes, slots, n_chunks, log2c = res.args()
     _check(lib.oracle_merge(enc, _ptr(hi), pool, pool_bytes, slots, n_chunks, log2c, hi.size,
                             _ptr(out)), "merge")
+    return out
+
+
+def restore(backup, res: Residual, c0=0, c1=None):
+    """Write logical chunks [c0, c1) of the residual stream `backup` (uint8,
+    numel bytes) into res.pool through the table (in place)."""
+    lib = _load()
+    backup = np.ascontiguousarray(backup, dtype=np.uint8)
+    c = 1 << res.log2_chunk
+    if c1 is None:
+        c1 = -(-backup.size // c)
+    pool, pool_bytes, slots, n_chunks, log2c = res.args()
+    _check(lib.oracle_restore(_ptr(backup), backup.size, int(c0), int(c1), pool, pool_bytes,
+                              slots, n_chunks, log2c), "restore")
+
+
+def backup(res: Residual, numel):
+    """The residual's logical byte stream (numel bytes) read through the table."""
+    lib = _load()
+    out = np.empty(int(numel), dtype=np.uint8)
+    pool, pool_bytes, slots, n_chunks, log2c = res.args()
+    _check(lib.oracle_backup(pool, pool_bytes, slots, n_chunks, log2c, out.size, _ptr(out)),
+           "backup")
     return out
 
 

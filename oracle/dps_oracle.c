@@ -262,6 +262,49 @@ int oracle_merge(int enc, const uint8_t *hi, const uint8_t *pool, int64_t pool_b
 }
 
 /* ------------------------------------------------------------------------ */
+/* Residual backup and restore (Sec. IV-B "Residual Backup"; Sec. IV-C,     */
+/* restoration paragraph).  The backup is the residual's logical byte       */
+/* stream, contiguous in host memory.                                       */
+/* ------------------------------------------------------------------------ */
+
+/* Restore logical chunks [c0, c1) of a residual from its backup: byte i of
+ * those chunks (i < numel) is written to the pool where the chunk table puts
+ * it.  Every other pool byte is left as it was.                            */
+int oracle_restore(const uint8_t *backup, int64_t numel, int64_t c0, int64_t c1,
+                   uint8_t *pool, int64_t pool_bytes, const int32_t *slots,
+                   int64_t n_chunks, int32_t log2_chunk)
+{
+    if (check_residual(numel, slots, n_chunks, log2_chunk, pool_bytes))
+        return -1;
+    int64_t chunk_bytes = (int64_t)1 << log2_chunk;
+    int64_t used = numel == 0 ? 0 : (numel - 1) / chunk_bytes + 1;  /* chunks holding bytes */
+    if (c0 < 0 || c1 < c0 || c1 > used)
+        return -1;
+    for (int64_t i = c0 * chunk_bytes; i < c1 * chunk_bytes && i < numel; ++i) {
+        int64_t p = oracle_residual_addr(i, slots, n_chunks, log2_chunk, pool_bytes);
+        if (p < 0)
+            return -1;
+        pool[p] = backup[i];
+    }
+    return 0;
+}
+
+/* The backup itself: the logical stream read back through the table.      */
+int oracle_backup(const uint8_t *pool, int64_t pool_bytes, const int32_t *slots,
+                  int64_t n_chunks, int32_t log2_chunk, int64_t numel, uint8_t *backup)
+{
+    if (check_residual(numel, slots, n_chunks, log2_chunk, pool_bytes))
+        return -1;
+    for (int64_t i = 0; i < numel; ++i) {
+        int64_t p = oracle_residual_addr(i, slots, n_chunks, log2_chunk, pool_bytes);
+        if (p < 0)
+            return -1;
+        backup[i] = pool[p];
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
 /* Nested linear layer (Sec. IV-C "Overall concept" and the GroupedGEMM     */
 /* paragraph): Y[r][c] = sum_k X[r][k] * W[c][k].                           */
 /*   full mode : W = the FP16 value of (upper byte, residual byte)          */

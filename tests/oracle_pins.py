@@ -461,11 +461,54 @@ def pin_linear_e4m3():
     assert np.allclose(y, want, rtol=1e-12, atol=1e-14)
 
 
+# --------------------------------------------------------------------------
+# Residual backup and restore
+# --------------------------------------------------------------------------
+
+def pin_backup_restore():
+    """The backup is the split's residual stream (numpy fancy-index gather);
+    restoring chunk ranges [c0, c1) of it into a pool overwritten with KV-like
+    filler writes exactly those chunks' bytes (numpy scatter through the
+    table) and leaves every other byte alone; the empty range is a no-op."""
+    rng = np.random.default_rng(24)
+    numel, log2c, n_slots = 5000, 8, 64
+    w = _rand_fp16(numel, rng, 0.05)
+    for enc in (oracle.E5M2, oracle.E4M3):
+        res = random_residual(numel, log2c, n_slots, seed=25, fill=True)
+        oracle.split(w, res, enc=enc)
+        bk = oracle.backup(res, numel)
+        assert (bk == residual_stream_by_indexing(res, numel)).all()
+        c = 1 << log2c
+        n_chunks = res.slots.size
+        for c0, c1 in ((0, n_chunks), (3, 7), (n_chunks - 1, n_chunks), (5, 5)):
+            pool = rng.integers(0, 256, res.pool.size, dtype=np.uint8)
+            want = pool.copy().reshape(-1, c)
+            lo, hi = c0 * c, min(c1 * c, numel)
+            stream = np.zeros(c1 * c if c1 > c0 else 0, dtype=np.uint8)
+            stream[:hi - lo] = bk[lo:hi]
+            blocks = stream.reshape(-1, c)
+            for j, chunk in enumerate(range(c0, c1)):
+                nb = min(c, numel - chunk * c)
+                want[res.slots[chunk], :nb] = blocks[j, :nb]
+            r2 = oracle.Residual(pool, res.slots, log2c)
+            oracle.restore(bk, r2, c0, c1)
+            assert (r2.pool == want.reshape(-1)).all(), (c0, c1)
+    # out-of-range chunk ranges are rejected
+    res = random_residual(numel, log2c, n_slots, seed=26)
+    bk = np.zeros(numel, dtype=np.uint8)
+    for c0, c1 in ((-1, 2), (4, 3), (0, res.slots.size + 1)):
+        try:
+            oracle.restore(bk, res, c0, c1)
+        except ValueError:
+            continue
+        raise AssertionError("range (%d, %d) accepted" % (c0, c1))
+
+
 ALL_PINS = [
     pin_fp16_decode, pin_e5m2_decode, pin_e4m3_decode, pin_golden_split,
     pin_split_is_truncation, pin_split_merge_identity, pin_residual_addressing,
     pin_linear_small, pin_linear_one_hot, pin_fast_equals_full_with_zero_residual,
     pin_grouped_is_loop_of_dense, pin_linear_rows, pin_e4m3_rounding_exhaustive,
     pin_act_scale, pin_linear_fp8, pin_golden_split_e4m3, pin_e4m3_split_is_truncation,
-    pin_e4m3_split_merge, pin_select_enc, pin_linear_e4m3,
+    pin_e4m3_split_merge, pin_select_enc, pin_linear_e4m3, pin_backup_restore,
 ]

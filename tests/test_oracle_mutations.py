@@ -60,6 +60,12 @@ MUTATIONS = [
      "oracle_fp16_value(unnest_word(0, hi[i], p < 0 ? 0 : pool[p]))"),
     ("fp8_ignores_enc", "oracle_fast_value(enc, hi[c * k + kk]);",
      "oracle_e5m2_value(hi[c * k + kk]);"),
+    # backup and restore
+    ("restore_whole_stream", "for (int64_t i = c0 * chunk_bytes; i < c1 * chunk_bytes && i < numel; ++i) {",
+     "for (int64_t i = 0; i < numel; ++i) {"),
+    ("restore_shifted", "        pool[p] = backup[i];", "        pool[p] = backup[i > 0 ? i - 1 : 0];"),
+    ("backup_identity_table", "        backup[i] = pool[p];", "        backup[i] = pool[i];"),
+    ("restore_range_unchecked", "    if (c0 < 0 || c1 < c0 || c1 > used)", "    if (c0 < 0 || c1 < c0)"),
 ]
 
 
