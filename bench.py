@@ -17,7 +17,9 @@ and not from the 256 MB Infinity Cache.
 Also printed on the same JSON line: the roofline of the dominant call
 (HIP events around back-to-back launches of that call on its stream), the
 CPU oracle timed on a bounded sample on the host cores, a per-call
-breakdown, and secondary figures (prefill TFLOPS on FP8/FP16 matrix cores).
+breakdown, and secondary figures (prefill TFLOPS on FP8/FP16 matrix cores;
+residual restore from a pinned host backup, alone and under fast-mode
+decode of the hidden-8192 set).
 """
 import argparse
 import json
@@ -223,7 +225,10 @@ def main():
     secondary = {}
     if not args.no_secondary:
         secondary = prefill_secondary(torch, dps, workloads, copies[0], layers, stream)
-    del graphs, g_dom
+    del graphs, g_dom, copies
+    torch.cuda.synchronize()
+    if not args.no_secondary:
+        secondary["restore"] = restore_secondary(torch, dps, workloads, stream, enc)
     torch.cuda.synchronize()
 
     # ---- CPU oracle baseline --------------------------------------------------------
@@ -357,6 +362,121 @@ def prefill_secondary(torch, dps, workloads, nws, layers, stream):
             res[label] = {"M": m, "ms": round(t * 1e3, 3), "TFLOPs": round(flops / t / 1e12, 1),
                           "frac_of_peak": round(flops / t / 1e12 / peak, 3)}
     return res
+
+
+def restore_secondary(torch, dps, workloads, stream, enc):
+    """Residual restore (host -> pool chunks, 4 MiB copies on a copy stream of
+    its own) for the hidden-8192 layer set with 2 MiB residual chunks at
+    seeded random slots of a pool twice the residual's size (the other slots
+    stand for KV blocks), alone and while fast-mode decode (64 tokens, the
+    four layers) runs on the compute stream."""
+    dev = torch.device("cuda:0")
+    log2c = 21
+    m = 64
+    layers = workloads.H8192_SET
+    copy = torch.cuda.Stream()
+    nws, backups, total = [], [], 0
+    with torch.cuda.stream(stream):
+        for li, (name, n, k) in enumerate(layers):
+            n_chunks = workloads.n_chunks_for(n * k, log2c)
+            slots = workloads.chunk_slots(n_chunks, 2 * n_chunks, seed=500 + li)
+            pool = torch.empty(2 * n_chunks << log2c, dtype=torch.uint8, device=dev)
+            res = dps.Residual(pool, slots.to(dev), log2c)
+            w = workloads.weight_fp16(n, k, seed=600 + li, device=dev)
+            nws.append(dps.split(w, res, enc=enc))
+            del w
+            backups.append((dps.backup(res, n * k, slots_host=slots), slots, n * k))
+            total += n * k
+        xs = {k: workloads.activations_fp16(m, k, seed=k, device=dev)
+              for k in sorted({k for _, _, k in layers})}
+        ys = {n: torch.empty((m, n), dtype=torch.float16, device=dev)
+              for n in sorted({n for _, n, _ in layers})}
+    torch.cuda.synchronize()
+
+    def restore_all():
+        for nw, (bk, slots, numel) in zip(nws, backups):
+            dps.restore(bk, nw.residual, numel=numel, slots_host=slots)
+
+    def decode_step():
+        for li, (name, n, k) in enumerate(layers):
+            dps.linear(xs[k], nws[li], dps.MODE_FAST, out=ys[n])
+
+    def ev():
+        return torch.cuda.Event(enable_timing=True)
+
+    # restore alone (after one warm-up pass)
+    with torch.cuda.stream(copy):
+        restore_all()
+    copy.synchronize()
+    reps = 3
+    e0, e1 = ev(), ev()
+    with torch.cuda.stream(copy):
+        e0.record(copy)
+        for _ in range(reps):
+            restore_all()
+        e1.record(copy)
+    copy.synchronize()
+    t_restore = e0.elapsed_time(e1) * 1e-3 / reps
+
+    # a plain pinned host -> device copy of 256 MiB (the copy engines' rate)
+    src = torch.empty(256 << 20, dtype=torch.uint8, pin_memory=True)
+    dst = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+    with torch.cuda.stream(copy):
+        dst.copy_(src, non_blocking=True)
+        e0.record(copy)
+        for _ in range(reps):
+            dst.copy_(src, non_blocking=True)
+        e1.record(copy)
+    copy.synchronize()
+    t_plain = e0.elapsed_time(e1) * 1e-3 / reps
+    del src, dst
+
+    # fast-mode decode alone
+    steps = 40
+    with torch.cuda.stream(stream):
+        decode_step()
+        stream.synchronize()
+        e0.record(stream)
+        for _ in range(steps):
+            decode_step()
+        e1.record(stream)
+    stream.synchronize()
+    t_step = e0.elapsed_time(e1) * 1e-3 / steps
+
+    # both at once: the restore on the copy stream, decode steps (each between
+    # events) on the compute stream; steps that end before the restore does
+    # count as overlapped
+    start = ev()
+    r_end = ev()
+    step_ev = [(ev(), ev()) for _ in range(int(2 * t_restore / t_step) + 8)]
+    with torch.cuda.stream(stream):
+        start.record(stream)
+    copy.wait_stream(stream)
+    with torch.cuda.stream(copy):
+        restore_all()
+        r_end.record(copy)
+    with torch.cuda.stream(stream):
+        for a, b in step_ev:
+            a.record(stream)
+            decode_step()
+            b.record(stream)
+    torch.cuda.synchronize()
+    t_r_conc = start.elapsed_time(r_end) * 1e-3
+    inside = [a.elapsed_time(b) * 1e-3 for a, b in step_ev
+              if start.elapsed_time(b) * 1e-3 <= t_r_conc]
+    t_step_conc = sum(inside) / len(inside) if inside else None
+    return {"workload": "decode_h8192_scattered, fast mode, M=%d" % m,
+            "encoding": "e4m3" if enc == dps.ENC_E4M3 else "e5m2",
+            "residual_bytes": total, "chunk_bytes": 1 << log2c, "copy_bytes": dps.COPY_BYTES,
+            "restore_ms": round(t_restore * 1e3, 3),
+            "restore_GBs": round(total / t_restore / 1e9, 1),
+            "plain_h2d_GBs": round((256 << 20) / t_plain / 1e9, 1),
+            "decode_step_ms": round(t_step * 1e3, 4),
+            "decode_step_ms_during_restore": (round(t_step_conc * 1e3, 4)
+                                              if t_step_conc else None),
+            "decode_steps_overlapped": len(inside),
+            "restore_ms_during_decode": round(t_r_conc * 1e3, 3),
+            "restore_GBs_during_decode": round(total / t_r_conc / 1e9, 1)}
 
 
 def cpu_baseline(workloads):

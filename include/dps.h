@@ -149,6 +149,40 @@ dps_status dps_split(int enc, const uint16_t *w, int64_t numel, uint8_t *hi,
 dps_status dps_merge(int enc, const uint8_t *hi, const dps_residual *res, int64_t numel,
                      uint16_t *w_out, void *stream);
 
+/* Residual restore (Sec. IV-B "Residual Backup": a pinned host copy of every
+ * residual, the source for reloading residuals whose pool units KV blocks
+ * have overwritten; Sec. IV-C, restoration paragraph: host-to-device copies
+ * in fixed-size pieces on a copy stream of their own, overlapped with the
+ * passes that run in fast mode meanwhile).  Copies logical chunks
+ * [chunk_begin, chunk_end) of a residual's byte stream from `backup` into the
+ * pool slots the table names, as hipMemcpyAsync host-to-device copies of at
+ * most copy_bytes each (4 MiB in the paper), enqueued in order on `stream`.
+ * Chunks in consecutive slots are joined before the stream is cut into
+ * copies.  Other pool bytes are not touched.
+ *   backup       host memory, the logical stream (numel bytes).  Allocate it
+ *                pinned (hipHostMalloc) for the copies to be asynchronous.
+ *   numel        bytes in the stream (elements of the weight).
+ *   res          host pointer to the residual descriptor; res->slots is not
+ *                read (the copies need the table on the host).
+ *   slots_host   host int32[>= chunk_end], the same entries as res->slots;
+ *                every entry in [chunk_begin, chunk_end) must lie in
+ *                [0, pool_bytes / C) (checked; DPS_ERR_INVALID_ARG).
+ *   0 <= chunk_begin <= chunk_end <= ceil(numel / C); an empty range is a
+ *   no-op.  copy_bytes > 0.
+ * Completion is the stream's: record an event on it for the compute stream
+ * to wait on before a full-mode pass.  Bit-exact. */
+dps_status dps_restore(const uint8_t *backup, int64_t numel, const dps_residual *res,
+                       const int32_t *slots_host, int64_t chunk_begin, int64_t chunk_end,
+                       int64_t copy_bytes, void *stream);
+
+/* Residual backup (Sec. IV-B "Residual Backup", built once at start-up): the
+ * whole logical stream (numel bytes) copied from the pool into `backup`
+ * (host, pinned for asynchronous copies) with device-to-host copies of at
+ * most copy_bytes on `stream`.  Arguments as dps_restore; every table entry
+ * of the tensor's chunks must lie in the pool.  Bit-exact. */
+dps_status dps_backup(const dps_residual *res, const int32_t *slots_host, int64_t numel,
+                      uint8_t *backup, int64_t copy_bytes, void *stream);
+
 /* Per-row FP8 quantization of activations for fast-mode prefill (this
  * reading taken here of the dynamic per-token activations of Sec. V-A
  * "Baselines"): for row r, a = max_k |x[r][k]|, scale[r] = the smallest power

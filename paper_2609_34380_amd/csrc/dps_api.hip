@@ -56,14 +56,12 @@ int current_cu_count()
     return cus;
 }
 
-// Residual descriptor checks shared by split, merge and full-mode linears.
-dps_status check_residual(const dps_residual *r, int64_t numel)
+// Pool geometry checks shared by every call that touches a residual.
+dps_status check_pool(const dps_residual *r, int64_t numel)
 {
     REQUIRE(r != nullptr, DPS_ERR_INVALID_ARG, "residual descriptor is NULL");
     REQUIRE(r->pool != nullptr, DPS_ERR_INVALID_ARG, "residual pool is NULL");
-    REQUIRE(r->slots != nullptr, DPS_ERR_INVALID_ARG, "residual slot table is NULL");
     REQUIRE(aligned(r->pool, 16), DPS_ERR_ALIGNMENT, "residual pool is not 16-byte aligned");
-    REQUIRE(aligned(r->slots, 4), DPS_ERR_ALIGNMENT, "residual slot table is not 4-byte aligned");
     REQUIRE(r->log2_chunk >= 4 && r->log2_chunk <= 30, DPS_ERR_INVALID_ARG,
             "log2_chunk must be in 4..30");
     const int64_t c = int64_t(1) << r->log2_chunk;
@@ -71,6 +69,29 @@ dps_status check_residual(const dps_residual *r, int64_t numel)
     REQUIRE(r->n_chunks >= 0, DPS_ERR_INVALID_ARG, "n_chunks is negative");
     REQUIRE(r->n_chunks >= cdiv(numel, c), DPS_ERR_INVALID_ARG,
             "n_chunks does not cover the tensor");
+    return DPS_OK;
+}
+
+// Residual descriptor checks shared by split, merge and full-mode linears.
+dps_status check_residual(const dps_residual *r, int64_t numel)
+{
+    const dps_status s = check_pool(r, numel);
+    if (s != DPS_OK)
+        return s;
+    REQUIRE(r->slots != nullptr, DPS_ERR_INVALID_ARG, "residual slot table is NULL");
+    REQUIRE(aligned(r->slots, 4), DPS_ERR_ALIGNMENT, "residual slot table is not 4-byte aligned");
+    return DPS_OK;
+}
+
+// Host slot-table entries of chunks [c0, c1) must address whole pool slots.
+dps_status check_host_slots(const dps_residual *r, const int32_t *slots_host, int64_t c0,
+                            int64_t c1)
+{
+    REQUIRE(slots_host != nullptr, DPS_ERR_INVALID_ARG, "host slot table is NULL");
+    const int64_t n_slots = r->pool_bytes >> r->log2_chunk;
+    for (int64_t c = c0; c < c1; ++c)
+        REQUIRE(slots_host[c] >= 0 && slots_host[c] < n_slots, DPS_ERR_INVALID_ARG,
+                "host slot table entry outside the pool");
     return DPS_OK;
 }
 
@@ -252,6 +273,49 @@ DPS_EXPORT dps_status dps_merge(int enc, const uint8_t *hi, const dps_residual *
     if (s != DPS_OK)
         return s;
     return launched(dps::launch_merge(enc, hi, view_of(res), numel, w_out, (hipStream_t)stream));
+}
+
+DPS_EXPORT dps_status dps_restore(const uint8_t *backup, int64_t numel, const dps_residual *res,
+                                  const int32_t *slots_host, int64_t chunk_begin,
+                                  int64_t chunk_end, int64_t copy_bytes, void *stream)
+{
+    g_err[0] = 0;
+    REQUIRE(numel >= 0, DPS_ERR_INVALID_ARG, "numel is negative");
+    REQUIRE(copy_bytes > 0, DPS_ERR_INVALID_ARG, "copy_bytes must be positive");
+    dps_status s = check_pool(res, numel);
+    if (s != DPS_OK)
+        return s;
+    const int64_t used = cdiv(numel, int64_t(1) << res->log2_chunk);
+    REQUIRE(chunk_begin >= 0 && chunk_begin <= chunk_end && chunk_end <= used,
+            DPS_ERR_INVALID_ARG, "chunk range outside the tensor");
+    if (chunk_begin == chunk_end)
+        return DPS_OK;
+    REQUIRE(backup != nullptr, DPS_ERR_INVALID_ARG, "backup is NULL");
+    s = check_host_slots(res, slots_host, chunk_begin, chunk_end);
+    if (s != DPS_OK)
+        return s;
+    return launched(dps::launch_restore(backup, numel, view_of(res), slots_host, chunk_begin,
+                                        chunk_end, copy_bytes, (hipStream_t)stream));
+}
+
+DPS_EXPORT dps_status dps_backup(const dps_residual *res, const int32_t *slots_host,
+                                 int64_t numel, uint8_t *backup, int64_t copy_bytes,
+                                 void *stream)
+{
+    g_err[0] = 0;
+    REQUIRE(numel >= 0, DPS_ERR_INVALID_ARG, "numel is negative");
+    REQUIRE(copy_bytes > 0, DPS_ERR_INVALID_ARG, "copy_bytes must be positive");
+    dps_status s = check_pool(res, numel);
+    if (s != DPS_OK)
+        return s;
+    if (numel == 0)
+        return DPS_OK;
+    REQUIRE(backup != nullptr, DPS_ERR_INVALID_ARG, "backup is NULL");
+    s = check_host_slots(res, slots_host, 0, cdiv(numel, int64_t(1) << res->log2_chunk));
+    if (s != DPS_OK)
+        return s;
+    return launched(dps::launch_backup(view_of(res), slots_host, numel, backup, copy_bytes,
+                                       (hipStream_t)stream));
 }
 
 DPS_EXPORT dps_status dps_quant_rows_e4m3(const uint16_t *x, int64_t m, int64_t k, uint8_t *xq,

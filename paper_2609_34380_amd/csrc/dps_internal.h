@@ -25,6 +25,16 @@ hipError_t launch_quant_rows(const uint16_t *x, int64_t m, int64_t k, uint8_t *x
 hipError_t launch_splitk_reduce(const float *partial, int splits, int64_t rows, int64_t n,
                                 uint16_t *y, hipStream_t stream);
 
+// ---- residual backup / restore (host-issued DMA copies) ----------------------
+// Logical chunks [c0, c1) of the stream `backup` (numel bytes, host) into the
+// pool slots slots_host names, as copies of at most copy_bytes on `stream`.
+hipError_t launch_restore(const uint8_t *backup, int64_t numel, const ResidualView &r,
+                          const int32_t *slots_host, int64_t c0, int64_t c1,
+                          int64_t copy_bytes, hipStream_t stream);
+// The whole logical stream from the pool into `backup` (host).
+hipError_t launch_backup(const ResidualView &r, const int32_t *slots_host, int64_t numel,
+                         uint8_t *backup, int64_t copy_bytes, hipStream_t stream);
+
 // ---- linear -------------------------------------------------------------------
 // A linear problem: rows of x grouped by expert (offsets == nullptr: one
 // expert owning rows [0, rows)), weights [experts][n][k].

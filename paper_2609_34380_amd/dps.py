@@ -23,7 +23,7 @@ ACT_FP8_ROWSCALE = 1
 _STATUS = {0: "DPS_OK", 1: "DPS_ERR_INVALID_ARG", 2: "DPS_ERR_ALIGNMENT",
            3: "DPS_ERR_UNSUPPORTED", 4: "DPS_ERR_WORKSPACE", 5: "DPS_ERR_HIP"}
 
-EXPORTED = ("dps_select_enc", "dps_split", "dps_merge", "dps_quant_rows_e4m3", "dps_workspace_bytes",
+EXPORTED = ("dps_select_enc", "dps_split", "dps_merge", "dps_restore", "dps_backup", "dps_quant_rows_e4m3", "dps_workspace_bytes",
             "dps_linear", "dps_linear_grouped", "dps_status_str", "dps_last_error")
 
 
@@ -65,6 +65,10 @@ def load_library(path=LIB_PATH):
     lib.dps_split.restype = ST
     lib.dps_merge.argtypes = [ctypes.c_int, P, ctypes.POINTER(CResidual), I64, P, P]
     lib.dps_merge.restype = ST
+    lib.dps_restore.argtypes = [P, I64, ctypes.POINTER(CResidual), P, I64, I64, I64, P]
+    lib.dps_restore.restype = ST
+    lib.dps_backup.argtypes = [ctypes.POINTER(CResidual), P, I64, P, I64, P]
+    lib.dps_backup.restype = ST
     lib.dps_quant_rows_e4m3.argtypes = [P, I64, I64, P, P, P]
     lib.dps_quant_rows_e4m3.restype = ST
     lib.dps_workspace_bytes.argtypes = [ctypes.c_int, U32, I64, I64, I64, I64]
@@ -184,6 +188,46 @@ def merge(nw, out=None):
     _check(lib.dps_merge(nw.enc, _ptr(nw.hi), ctypes.byref(res), nw.hi.numel(), _ptr(out),
                          _stream()))
     return out
+
+
+COPY_BYTES = 4 << 20   # restore copy size used in the paper
+
+
+def _host_slots(residual, slots_host):
+    if slots_host is None:
+        slots_host = residual.slots.cpu()
+    assert slots_host.dtype == torch.int32 and not slots_host.is_cuda
+    return slots_host.contiguous()
+
+
+def backup(residual, numel, out=None, slots_host=None, copy_bytes=COPY_BYTES):
+    """The residual's logical byte stream copied into host memory (dps_backup).
+    out: a uint8 CPU tensor of numel bytes, pinned for asynchronous copies
+    (a new pinned tensor by default).  Completion follows the current stream."""
+    lib = load_library()
+    slots_host = _host_slots(residual, slots_host)
+    if out is None:
+        out = torch.empty(numel, dtype=torch.uint8, pin_memory=True)
+    assert out.dtype == torch.uint8 and not out.is_cuda and out.numel() >= numel
+    res = residual.c()
+    _check(lib.dps_backup(ctypes.byref(res), _ptr(slots_host), numel, _ptr(out), copy_bytes,
+                          _stream()))
+    return out
+
+
+def restore(backup_host, residual, numel=None, chunk_begin=0, chunk_end=None, slots_host=None,
+            copy_bytes=COPY_BYTES):
+    """Copy logical chunks [chunk_begin, chunk_end) of the residual stream from
+    the host backup into the pool (dps_restore), on the current stream."""
+    lib = load_library()
+    assert backup_host.dtype == torch.uint8 and not backup_host.is_cuda
+    numel = backup_host.numel() if numel is None else numel
+    slots_host = _host_slots(residual, slots_host)
+    if chunk_end is None:
+        chunk_end = -(-numel // (1 << residual.log2_chunk))
+    res = residual.c()
+    _check(lib.dps_restore(_ptr(backup_host), numel, ctypes.byref(res), _ptr(slots_host),
+                           chunk_begin, chunk_end, copy_bytes, _stream()))
 
 
 def quant_rows_e4m3(x):

@@ -29,7 +29,8 @@ def lib():
 
 def test_header_declares_the_boundary():
     names = _declared()
-    for expected in ("dps_select_enc", "dps_split", "dps_merge", "dps_linear",
+    for expected in ("dps_select_enc", "dps_split", "dps_merge", "dps_restore", "dps_backup",
+                     "dps_linear",
                      "dps_linear_grouped", "dps_quant_rows_e4m3", "dps_workspace_bytes",
                      "dps_status_str", "dps_last_error"):
         assert expected in names
@@ -124,6 +125,38 @@ def test_split_merge_reject_bad_arguments(lib):
     assert lib.dps_select_enc(0, 64, 0x2000, None) == 1
     assert lib.dps_quant_rows_e4m3(0x1000, 4, 24, 0x2000, 0x3000, None) == 1
     assert lib.dps_quant_rows_e4m3(0x1000, 0, 32, 0x2000, 0x3000, None) == 0
+
+
+def test_restore_backup_reject_bad_arguments(lib):
+    # every call here fails validation (or is empty) before any copy is enqueued
+    res = dps.CResidual(0x2000, 4 << 8, 0x3000, 4, 8)   # 4 pool slots of 256 bytes
+    good = (ctypes.c_int32 * 4)(3, 0, 2, 1)
+    outside = (ctypes.c_int32 * 4)(3, 0, 4, 1)          # slot 4 is past the pool
+    negative = (ctypes.c_int32 * 4)(3, -1, 2, 1)
+    bk = 0x10000
+    P = ctypes.c_void_p
+    def restore(backup=bk, numel=1000, r=res, slots=good, c0=0, c1=4, copy=4096):
+        return lib.dps_restore(backup, numel, ctypes.byref(r) if r is not None else None,
+                               ctypes.cast(slots, P) if slots is not None else None,
+                               c0, c1, copy, None)
+    assert restore(numel=-1) == 1
+    assert restore(copy=0) == 1
+    assert restore(r=None) == 1
+    assert restore(c0=-1) == 1
+    assert restore(c0=3, c1=2) == 1
+    assert restore(c1=5) == 1                           # ceil(1000 / 256) = 4 chunks
+    assert restore(backup=0) == 1
+    assert restore(slots=None) == 1
+    assert restore(slots=outside) == 1
+    assert restore(slots=negative, c0=0, c1=4) == 1
+    assert restore(c0=2, c1=2) == 0                     # empty range: nothing to do
+    assert restore(numel=2000) == 1                     # 8 chunks > n_chunks 4
+    assert lib.dps_backup(ctypes.byref(res), ctypes.cast(good, P), -1, bk, 4096, None) == 1
+    assert lib.dps_backup(ctypes.byref(res), ctypes.cast(good, P), 1000, bk, 0, None) == 1
+    assert lib.dps_backup(ctypes.byref(res), ctypes.cast(outside, P), 1000, bk, 4096, None) == 1
+    assert lib.dps_backup(ctypes.byref(res), None, 1000, bk, 4096, None) == 1
+    assert lib.dps_backup(ctypes.byref(res), ctypes.cast(good, P), 1000, None, 4096, None) == 1
+    assert lib.dps_backup(ctypes.byref(res), ctypes.cast(good, P), 0, None, 4096, None) == 0
 
 
 def test_workspace_query(lib):
