@@ -229,6 +229,7 @@ def main():
     torch.cuda.synchronize()
     if not args.no_secondary:
         secondary["restore"] = restore_secondary(torch, dps, workloads, stream, enc)
+        secondary["sum_manager"] = sum_secondary(dps)
     torch.cuda.synchronize()
 
     # ---- CPU oracle baseline --------------------------------------------------------
@@ -477,6 +478,37 @@ def restore_secondary(torch, dps, workloads, stream, enc):
             "decode_steps_overlapped": len(inside),
             "restore_ms_during_decode": round(t_r_conc * 1e3, 3),
             "restore_GBs_during_decode": round(total / t_r_conc / 1e9, 1)}
+
+
+def sum_secondary(dps):
+    """Host cost of the SUM manager's KV block calls, through the Python
+    binding: 96 units of 13056 blocks (one hidden-8192 layer's residual, 855
+    MB, per unit in 64 KiB KV blocks), 80 residuals; requests of 64 blocks
+    allocated and freed in a seeded random order that fills the pool far
+    enough to evict residuals."""
+    import random
+
+    rng = random.Random(7)
+    s = dps.SumManager(96, 13056, 80)
+    held = []
+    ops = 20000
+    t0 = time.perf_counter()
+    for i in range(ops):
+        # mostly allocate for the first 60% of the run (the pool fills up and
+        # evicts residuals), then mostly free
+        p_alloc = 0.8 if i < 0.6 * ops else 0.2
+        if held and rng.random() >= p_alloc:
+            s.free(held.pop(rng.randrange(len(held))))
+        else:
+            blocks = s.alloc(64)
+            if blocks is not None:
+                held.append(blocks)
+    t = time.perf_counter() - t0
+    evicted = s.counts()["evicted"]
+    s.close()
+    return {"units": 96, "blocks_per_unit": 13056, "residuals": 80, "ops": ops,
+            "request_blocks": 64, "us_per_op": round(t / ops * 1e6, 2),
+            "residuals_evicted": evicted, "binding": "python ctypes"}
 
 
 def cpu_baseline(workloads):

@@ -47,7 +47,8 @@ typedef enum {
     DPS_ERR_ALIGNMENT = 2,   /* a tensor pointer is not 16-byte aligned      */
     DPS_ERR_UNSUPPORTED = 3, /* valid request this build does not implement  */
     DPS_ERR_WORKSPACE = 4,   /* workspace missing or smaller than required   */
-    DPS_ERR_HIP = 5          /* the HIP runtime reported an error on launch  */
+    DPS_ERR_HIP = 5,         /* the HIP runtime reported an error on launch  */
+    DPS_ERR_NO_SPACE = 6     /* SUM manager: not enough room for the request */
 } dps_status;
 
 /* Precision mode of one call; a whole forward pass runs in one mode
@@ -232,6 +233,71 @@ dps_status dps_linear(int mode, uint32_t flags, const uint16_t *x, int64_t m,
 dps_status dps_linear_grouped(int mode, uint32_t flags, const uint16_t *x_sorted,
                               const int32_t *offsets, int64_t rows, const dps_weight *w,
                               uint16_t *y, void *ws, size_t ws_bytes, void *stream);
+
+/* ------------------------------------------------------------------------
+ * SUM manager (Sec. IV-B "SUM manager"; Sec. IV-D, Algorithm 1): host-side
+ * bookkeeping of the shared region's physical units.  A unit holds either
+ * one residual tensor (BACKED) or KV blocks (AVAIL: some free, FULL: none
+ * free), or nothing (FREE); RESTORING units are held for a residual being
+ * copied back.  Residual r starts bound to unit r.  Taking a BACKED unit for
+ * KV evicts its residual: the mapping goes stale, the data lives only in the
+ * host backup, and the mode is fast until every evicted residual is back.
+ * Sets are ordered by unit id; a pop takes the lowest id and a unit hands out
+ * its lowest free block indices first.  Block id = unit * blocks_per_unit +
+ * index.  Not thread-safe: one caller (the serving loop) drives it.
+ * ------------------------------------------------------------------------ */
+enum { DPS_UNIT_FREE = 0, DPS_UNIT_BACKED = 1, DPS_UNIT_AVAIL = 2, DPS_UNIT_FULL = 3,
+       DPS_UNIT_RESTORING = 4 };
+
+typedef struct dps_sum dps_sum;
+
+/* n_units >= 1 units of blocks_per_unit >= 1 KV blocks; n_res (0..n_units)
+ * residuals bound to units 0 .. n_res-1, the other units FREE, mode full.
+ * *out receives the manager (free it with dps_sum_destroy). */
+dps_status dps_sum_create(int64_t n_units, int64_t blocks_per_unit, int64_t n_res,
+                          dps_sum **out);
+void dps_sum_destroy(dps_sum *s);
+
+/* AllocKVBlock(n) of Algorithm 1: blocks from AVAIL units first, then a FREE
+ * unit, then a BACKED unit (evicting its residual, switching to fast mode).
+ * The n block ids go to blocks[0..n).  A request larger than the room left
+ * in AVAIL, FREE and BACKED units takes nothing and returns
+ * DPS_ERR_NO_SPACE. */
+dps_status dps_sum_alloc(dps_sum *s, int64_t n, int64_t *blocks);
+
+/* FreeKVBlock(blocks) of Algorithm 1: FULL units with a freed block become
+ * AVAIL, units with no block left become FREE, and *wake (may be NULL) is
+ * set to 1 if that happened while residuals wait for restoration.  Blocks
+ * that are not allocated, or listed twice, fail the whole call with
+ * DPS_ERR_INVALID_ARG and change nothing. */
+dps_status dps_sum_free(dps_sum *s, const int64_t *blocks, int64_t n, int32_t *wake);
+
+/* Restore worker, first step: the lowest stale residual is bound to the
+ * lowest FREE unit, which turns RESTORING.  *residual and *unit receive them,
+ * or -1 when nothing is stale or no unit is free.  The caller then copies
+ * the residual's bytes into that unit (dps_sum_slots, dps_restore) and calls
+ * dps_sum_restore_done once the copy has completed. */
+dps_status dps_sum_restore_begin(dps_sum *s, int64_t *residual, int64_t *unit);
+
+/* The copy of `residual` has completed: its unit becomes BACKED; when no
+ * residual is left evicted the mode returns to full. */
+dps_status dps_sum_restore_done(dps_sum *s, int64_t residual);
+
+/* DPS_MODE_FULL or DPS_MODE_FAST (-1 for NULL). */
+int32_t dps_sum_mode(const dps_sum *s);
+/* DPS_UNIT_* state of a unit (-1 if out of range). */
+int32_t dps_sum_unit_state(const dps_sum *s, int64_t unit);
+/* Unit a residual is bound to or being restored into; -1 while evicted. */
+int64_t dps_sum_unit_of(const dps_sum *s, int64_t residual);
+/* counts[0..8): |FREE|, |BACKED|, |AVAIL|, |FULL|, |RESTORING|, |STALE|,
+ * |EVICTED|, free blocks in AVAIL units. */
+dps_status dps_sum_counts(const dps_sum *s, int64_t *counts);
+/* Host slot table of a residual of n_chunks <= chunks_per_unit chunks in
+ * its unit u, where unit u spans pool slots [u * chunks_per_unit,
+ * (u + 1) * chunks_per_unit): slots_host[c] = u * chunks_per_unit + c.  The
+ * residual must be bound or being restored (else DPS_ERR_INVALID_ARG). */
+dps_status dps_sum_slots(const dps_sum *s, int64_t residual, int64_t chunks_per_unit,
+                         int64_t n_chunks, int32_t *slots_host);
 
 /* Static description of a status code. */
 const char *dps_status_str(dps_status s);

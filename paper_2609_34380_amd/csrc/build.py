@@ -16,7 +16,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libdps.so")
 SOURCES = ["dps_elementwise.hip", "dps_skinny.hip", "dps_gemm.hip", "dps_restore.hip",
-           "dps_api.hip"]
+           "dps_api.hip", "dps_sum.cpp"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

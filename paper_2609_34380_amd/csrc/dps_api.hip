@@ -222,6 +222,7 @@ DPS_EXPORT const char *dps_status_str(dps_status s)
     case DPS_ERR_UNSUPPORTED: return "unsupported";
     case DPS_ERR_WORKSPACE: return "workspace too small";
     case DPS_ERR_HIP: return "HIP error";
+    case DPS_ERR_NO_SPACE: return "no space";
     }
     return "unknown status";
 }

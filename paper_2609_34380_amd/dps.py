@@ -21,10 +21,16 @@ ACT_FP16 = 0
 ACT_FP8_ROWSCALE = 1
 
 _STATUS = {0: "DPS_OK", 1: "DPS_ERR_INVALID_ARG", 2: "DPS_ERR_ALIGNMENT",
-           3: "DPS_ERR_UNSUPPORTED", 4: "DPS_ERR_WORKSPACE", 5: "DPS_ERR_HIP"}
+           3: "DPS_ERR_UNSUPPORTED", 4: "DPS_ERR_WORKSPACE", 5: "DPS_ERR_HIP",
+           6: "DPS_ERR_NO_SPACE"}
+ERR_NO_SPACE = 6
+UNIT_FREE, UNIT_BACKED, UNIT_AVAIL, UNIT_FULL, UNIT_RESTORING = 0, 1, 2, 3, 4
 
 EXPORTED = ("dps_select_enc", "dps_split", "dps_merge", "dps_restore", "dps_backup", "dps_quant_rows_e4m3", "dps_workspace_bytes",
-            "dps_linear", "dps_linear_grouped", "dps_status_str", "dps_last_error")
+            "dps_linear", "dps_linear_grouped", "dps_status_str", "dps_last_error",
+            "dps_sum_create", "dps_sum_destroy", "dps_sum_alloc", "dps_sum_free",
+            "dps_sum_restore_begin", "dps_sum_restore_done", "dps_sum_mode",
+            "dps_sum_unit_state", "dps_sum_unit_of", "dps_sum_counts", "dps_sum_slots")
 
 
 class DpsError(RuntimeError):
@@ -79,6 +85,29 @@ def load_library(path=LIB_PATH):
     lib.dps_linear_grouped.argtypes = [ctypes.c_int, U32, P, P, I64, ctypes.POINTER(CWeight),
                                        P, P, ctypes.c_size_t, P]
     lib.dps_linear_grouped.restype = ST
+    PI64 = ctypes.POINTER(I64)
+    lib.dps_sum_create.argtypes = [I64, I64, I64, ctypes.POINTER(P)]
+    lib.dps_sum_create.restype = ST
+    lib.dps_sum_destroy.argtypes = [P]
+    lib.dps_sum_destroy.restype = None
+    lib.dps_sum_alloc.argtypes = [P, I64, P]
+    lib.dps_sum_alloc.restype = ST
+    lib.dps_sum_free.argtypes = [P, P, I64, ctypes.POINTER(I32)]
+    lib.dps_sum_free.restype = ST
+    lib.dps_sum_restore_begin.argtypes = [P, PI64, PI64]
+    lib.dps_sum_restore_begin.restype = ST
+    lib.dps_sum_restore_done.argtypes = [P, I64]
+    lib.dps_sum_restore_done.restype = ST
+    lib.dps_sum_mode.argtypes = [P]
+    lib.dps_sum_mode.restype = I32
+    lib.dps_sum_unit_state.argtypes = [P, I64]
+    lib.dps_sum_unit_state.restype = I32
+    lib.dps_sum_unit_of.argtypes = [P, I64]
+    lib.dps_sum_unit_of.restype = I64
+    lib.dps_sum_counts.argtypes = [P, P]
+    lib.dps_sum_counts.restype = ST
+    lib.dps_sum_slots.argtypes = [P, I64, I64, I64, P]
+    lib.dps_sum_slots.restype = ST
     lib.dps_status_str.argtypes = [ST]
     lib.dps_status_str.restype = ctypes.c_char_p
     lib.dps_last_error.argtypes = []
@@ -307,3 +336,76 @@ def make_residual(numel, log2_chunk, device, slots=None, pool=None):
         pool = torch.zeros(max(n_chunks, int(slots.max().item()) + 1) * c, dtype=torch.uint8,
                            device=device)
     return Residual(pool, slots, log2_chunk)
+
+
+class SumManager:
+    """The SUM manager's unit bookkeeping (dps_sum_*): n_units units of
+    blocks_per_unit KV blocks, residual r initially bound to unit r."""
+
+    COUNT_NAMES = ("free", "backed", "avail", "full", "restoring", "stale", "evicted",
+                   "free_blocks")
+
+    def __init__(self, n_units, blocks_per_unit, n_res):
+        lib = load_library()
+        h = ctypes.c_void_p()
+        _check(lib.dps_sum_create(n_units, blocks_per_unit, n_res, ctypes.byref(h)))
+        self._h = h
+        self.n_units, self.blocks_per_unit, self.n_res = n_units, blocks_per_unit, n_res
+
+    def close(self):
+        if self._h:
+            _lib.dps_sum_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def alloc(self, n):
+        """n block ids (a list), or None when the request does not fit."""
+        out = (ctypes.c_int64 * max(n, 1))()
+        st = _lib.dps_sum_alloc(self._h, n, out)
+        if st == ERR_NO_SPACE:
+            return None
+        _check(st)
+        return list(out[:n])
+
+    def free(self, blocks):
+        """Free the listed blocks; returns True when restoration should wake."""
+        arr = (ctypes.c_int64 * max(len(blocks), 1))(*blocks)
+        wake = ctypes.c_int32(0)
+        _check(_lib.dps_sum_free(self._h, arr, len(blocks), ctypes.byref(wake)))
+        return bool(wake.value)
+
+    def restore_begin(self):
+        """(residual, unit) now held for a restore, or None."""
+        r, u = ctypes.c_int64(), ctypes.c_int64()
+        _check(_lib.dps_sum_restore_begin(self._h, ctypes.byref(r), ctypes.byref(u)))
+        return None if r.value < 0 else (r.value, u.value)
+
+    def restore_done(self, residual):
+        _check(_lib.dps_sum_restore_done(self._h, residual))
+
+    @property
+    def mode(self):
+        return _lib.dps_sum_mode(self._h)
+
+    def unit_state(self, unit):
+        return _lib.dps_sum_unit_state(self._h, unit)
+
+    def unit_of(self, residual):
+        return _lib.dps_sum_unit_of(self._h, residual)
+
+    def counts(self):
+        c = (ctypes.c_int64 * 8)()
+        _check(_lib.dps_sum_counts(self._h, c))
+        return dict(zip(self.COUNT_NAMES, c[:]))
+
+    def slots(self, residual, chunks_per_unit, n_chunks):
+        """Host int32 slot table of the residual in its unit."""
+        out = torch.empty(max(n_chunks, 1), dtype=torch.int32)
+        _check(_lib.dps_sum_slots(self._h, residual, chunks_per_unit, n_chunks,
+                                  ctypes.c_void_p(out.data_ptr())))
+        return out[:n_chunks]

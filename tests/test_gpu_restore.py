@@ -115,3 +115,70 @@ def test_evict_serve_fast_restore_full(enc):
     for y in fast_outs:
         assert torch.equal(y.view(torch.int16), y_fast.view(torch.int16))
     assert torch.equal(y_full_back.view(torch.int16), y_full.view(torch.int16))
+
+
+def test_sum_managed_eviction_and_restore():
+    """Three 4096x4096 layers whose residuals (8 chunks of 2 MiB) each fill one
+    16 MiB unit of a 6-unit shared pool that KV blocks of 64 KiB also use.
+    The native SUM manager hands out KV blocks (their bytes are then written
+    with KV data) until two residuals are evicted; fast mode keeps every
+    output bit for bit.  Freeing the blocks wakes the restore: each evicted
+    residual is bound to a free unit (possibly not its old one), its device
+    slot table is rewritten and its bytes copied back from the pinned backup
+    on a copy stream.  Full mode is then bit-identical to the start."""
+    n = k = 4096
+    log2c = 21
+    chunks_per_unit = 8
+    unit_bytes = chunks_per_unit << log2c
+    kv_bytes = 64 << 10
+    n_units, n_res = 6, 3
+    sum_mgr = dps.SumManager(n_units, unit_bytes // kv_bytes, n_res)
+    pool = torch.zeros(n_units * unit_bytes, dtype=torch.uint8, device=DEV)
+    x = workloads.activations_fp16(64, k, seed=20).to(DEV)
+    layers, y_full, y_fast, backups = [], [], [], []
+    for r in range(n_res):
+        slots = sum_mgr.slots(r, chunks_per_unit, chunks_per_unit)
+        res = dps.Residual(pool, slots.to(DEV), log2c)
+        nw = dps.split(workloads.weight_fp16(n, k, seed=21 + r).to(DEV), res)
+        layers.append(nw)
+        y_full.append(dps.linear(x, nw, FULL))
+        y_fast.append(dps.linear(x, nw, FAST))
+        backups.append(dps.backup(res, n * k, slots_host=slots))
+    torch.cuda.synchronize()
+
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(22)
+    held = []
+    while sum_mgr.counts()["evicted"] < 2:
+        blocks = sum_mgr.alloc(100)
+        for b in blocks:          # the serving system writes KV into the new blocks
+            pool[b * kv_bytes:(b + 1) * kv_bytes] = torch.randint(
+                0, 256, (kv_bytes,), dtype=torch.uint8, device=DEV, generator=gen)
+        held += blocks
+    assert sum_mgr.mode == dps.MODE_FAST
+    for nw, want in zip(layers, y_fast):
+        assert torch.equal(dps.linear(x, nw, FAST).view(torch.int16), want.view(torch.int16))
+
+    # unit 0 (the first evicted) keeps its KV blocks, so both residuals move
+    bpu = unit_bytes // kv_bytes
+    assert sum_mgr.free([b for b in held if b // bpu != 0])
+    compute = torch.cuda.current_stream()
+    copy = torch.cuda.Stream()
+    copy.wait_stream(compute)
+    moved = []
+    while True:
+        step = sum_mgr.restore_begin()
+        if step is None:
+            break
+        r, u = step
+        slots = sum_mgr.slots(r, chunks_per_unit, chunks_per_unit)
+        moved.append((r, u))
+        with torch.cuda.stream(copy):
+            layers[r].residual.slots.copy_(slots, non_blocking=True)
+            dps.restore(backups[r], layers[r].residual, slots_host=slots)
+        copy.synchronize()
+        sum_mgr.restore_done(r)
+    assert moved == [(0, 1), (1, 3)] and sum_mgr.mode == dps.MODE_FULL
+    compute.wait_stream(copy)
+    for nw, want in zip(layers, y_full):
+        assert torch.equal(dps.linear(x, nw, FULL).view(torch.int16), want.view(torch.int16))
