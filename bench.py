@@ -225,6 +225,8 @@ def main():
     secondary = {}
     if not args.no_secondary:
         secondary = prefill_secondary(torch, dps, workloads, copies[0], layers, stream)
+        secondary["graph_pair"] = graph_pair_secondary(torch, dps, run_call, layers, ms, stream,
+                                                       ms_per_step)
     del graphs, g_dom, copies
     torch.cuda.synchronize()
     if not args.no_secondary:
@@ -363,6 +365,38 @@ def prefill_secondary(torch, dps, workloads, nws, layers, stream):
             res[label] = {"M": m, "ms": round(t * 1e3, 3), "TFLOPs": round(flops / t / 1e12, 1),
                           "frac_of_peak": round(flops / t / 1e12 / peak, 3)}
     return res
+
+
+def graph_pair_secondary(torch, dps, run_call, layers, ms, stream, ms_per_step):
+    """The decode set as the paper's dispatcher runs it: one captured graph
+    per (batch size, mode) per weight copy, a forward pass = one replay.
+    Reports each pass's time and the sum over all ten passes against the
+    single-graph step above."""
+    from paper_2609_34380_amd import graphs
+
+    pairs = []
+    for c in range(COPIES):
+        def step(m, mode, c=c):
+            for li in range(len(layers)):
+                run_call(c, m, mode, li)
+        pairs.append(graphs.ModeGraphs(step, ms, stream).capture())
+    reps = 8
+    per_pass = {}
+    for m in ms:
+        for mname, mode in (("fast", dps.MODE_FAST), ("full", dps.MODE_FULL)):
+            evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                   for _ in range(reps)]
+            for r in range(reps):
+                evs[r][0].record(stream)
+                pairs[r % COPIES].replay(m, mode)
+                evs[r][1].record(stream)
+            stream.synchronize()
+            ts = sorted(a.elapsed_time(b) for a, b in evs)
+            per_pass["M%d_%s" % (m, mname)] = round(ts[len(ts) // 2] * 1e3, 2)
+    total_us = sum(per_pass.values())
+    del pairs
+    return {"pass_us": per_pass, "sum_of_passes_ms": round(total_us / 1e3, 4),
+            "single_graph_step_ms": round(ms_per_step, 4)}
 
 
 def restore_secondary(torch, dps, workloads, stream, enc):

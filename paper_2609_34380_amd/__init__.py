@@ -1,7 +1,7 @@
 """MI355X (gfx950) implementation of the nested-precision linear layer of
-Dual-Mode Precision Serving: FP16 weights held as an FP8 E5M2 upper-byte plane
-plus a chunked low-byte residual plane, contracted in fast mode (upper plane
-only) or full mode (exact FP16 rebuilt in registers).
+Dual-Mode Precision Serving: FP16 weights held as an FP8 upper-byte plane (E5M2,
+or E4M3 for small-range layers) plus a chunked residual plane, contracted in
+fast mode (upper plane only) or full mode (exact FP16 rebuilt in registers).
 
 The compute lives in libdps.so (HIP kernels behind a C ABI, include/dps.h);
 ``paper_2609_34380_amd.dps`` is its thin Python binding.  Importing this
@@ -9,7 +9,7 @@ package does not load the library; the first call into ``dps`` does, and
 fails loudly if it is not built.
 """
 
-__all__ = ["dps", "workloads"]
+__all__ = ["dps", "graphs", "workloads"]
 
 
 def __getattr__(name):
