@@ -133,6 +133,10 @@ LINEAR_CASES = [
     (4, 1024, 1024, 16, False),     # the single-layer workload
     (1, 1024, 1024, 16, False),
     (3, 1000, 1040, 12, True),
+    (2, 8200, 2064, 10, True),      # 1-2 token kernel: two rows per wave, ragged K chunk,
+                                    # residual rows over several chunks (table lookups)
+    (4, 1024, 8192, 21, False),     # activations exactly fill the 64 KiB staging limit
+    (2, 300, 14336, 16, True),      # long rows (the down projection's K)
     (16, 64, 2048, 8, True),        # chunks smaller than a K range: table lookups
     (17, 520, 4096, 21, True),
     (32, 768, 2048, 14, True),      # one full 32-token tile
