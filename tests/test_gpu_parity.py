@@ -146,6 +146,9 @@ LINEAR_CASES = [
     (130, 260, 2048, 8, True),
     (300, 512, 512, 16, True),
     (256, 640, 4096, 21, True),
+    # layers above 2^24 weights take the 64- and 128-token tiles
+    (65, 4100, 4112, 21, True),
+    (130, 4100, 4112, 12, True),
 ]
 
 
