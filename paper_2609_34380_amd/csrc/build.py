@@ -15,7 +15,7 @@ ROOT = os.path.dirname(PKG)
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libdps.so")
-SOURCES = ["dps_elementwise.hip", "dps_skinny.hip", "dps_gemv.hip", "dps_gemm.hip",
+SOURCES = ["dps_elementwise.hip", "dps_skinny.hip", "dps_gemv.hip", "dps_rows.hip", "dps_gemm.hip",
            "dps_restore.hip", "dps_api.hip", "dps_sum.cpp"]
 ARCH = "gfx950"
 

@@ -50,7 +50,7 @@ struct LinearProblem {
     uint16_t *y;
 };
 
-enum KernelKind { KIND_SKINNY = 0, KIND_GEMM_F16 = 1, KIND_GEMM_FP8 = 2, KIND_GEMV = 3 };
+enum KernelKind { KIND_SKINNY = 0, KIND_GEMM_F16 = 1, KIND_GEMM_FP8 = 2, KIND_GEMV = 3, KIND_ROWS = 4 };
 // GEMM tile variants (weight rows x tokens per block).
 enum GemmVariant {
     // FP8 activations: eight-wave LDS-DMA kernel
@@ -89,6 +89,9 @@ hipError_t launch_skinny(const LinearProblem &p, const LinearPlan &plan, float *
                          hipStream_t stream);
 // Dense 1-4 token calls on the vector ALUs, whole rows per wave (no K split).
 hipError_t launch_gemv(const LinearProblem &p, const LinearPlan &plan, hipStream_t stream);
+// Dense calls of up to 16 tokens on the matrix cores, plan.variant = 16-row
+// groups per block (1-8), whole K per block (no K split).
+hipError_t launch_rows(const LinearProblem &p, const LinearPlan &plan, hipStream_t stream);
 hipError_t launch_gemm_f16(const LinearProblem &p, const LinearPlan &plan, float *partial,
                            hipStream_t stream);
 hipError_t launch_gemm_fp8(int enc, const uint8_t *xq, const float *scale, int64_t m, int64_t n,

@@ -135,8 +135,9 @@ def test_split_e4m3_large(numel, log2c, n_slots):
 # linear: tolerance against the fp64 oracle
 # -----------------------------------------------------------------------------
 
-# (m, n, k, log2c, scattered, wide): decode kernel (1-4 tokens), wide-row GEMM
-# (32/64/128-token tiles); wide = weights over most of the E4M3 range
+# (m, n, k, log2c, scattered, wide): decode kernel (1-4 tokens), dense
+# kernel for up to 16 tokens, wide-row GEMM (32/64/128-token tiles); wide =
+# weights over most of the E4M3 range
 E4M3_CASES = [
     (4, 1024, 1024, 16, False, False),
     (1, 1000, 1040, 12, True, True),
@@ -146,6 +147,8 @@ E4M3_CASES = [
     (65, 384, 1024, 12, True, True),
     (130, 260, 2048, 8, True, False),
     (300, 512, 512, 16, True, True),
+    (8, 28672, 1024, 21, True, True),
+    (15, 4100, 2064, 9, True, False),
 ]
 
 
@@ -224,13 +227,14 @@ def test_e4m3_one_hot_rows_select_weights_exactly(m):
         assert torch.equal(y.cpu().float(), want), mode
 
 
-@pytest.mark.parametrize("m", [1, 4, 64])
+@pytest.mark.parametrize("m", [1, 4, 8, 64])
 def test_e4m3_fast_weight_every_code(m):
     """Row r of the weight holds FP16 words whose E4M3 part is code r (all 254
     codes that are numbers; the two NaN codes give rows of zeros) with random
     residual bits.  One-hot activations read back E4M3(r) * 2^-8 exactly in
     fast mode, and the FP16 words exactly in full mode, on the decode kernel
-    (1 and 4 tokens) and the GEMM (64 tokens)."""
+    (1 and 4 tokens), the dense kernel for up to 16 tokens (8) and the GEMM
+    (64)."""
     n, k = 256, 256
     rng = np.random.default_rng(90 + m)
     codes = np.arange(256, dtype=np.uint16)

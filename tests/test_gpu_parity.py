@@ -149,6 +149,17 @@ LINEAR_CASES = [
     # layers above 2^24 weights take the 64- and 128-token tiles
     (65, 4100, 4112, 21, True),
     (130, 4100, 4112, 12, True),
+    # dense kernel for up to 16 tokens (whole K per block, 16-row groups):
+    # ragged row groups and K chunks, 1 KiB residual chunks that row pieces
+    # straddle, chunks below 1 KiB (per-vector lookups), 1-8 groups per block
+    (3, 8200, 4112, 10, True),       # 3 groups per block
+    (5, 4100, 2064, 9, True),        # 2 groups, chunks of 512 bytes
+    (8, 28672, 1024, 21, False),     # 7 groups (the gate+up rows at 8 tokens)
+    (12, 6144, 4096, 21, True),      # 2 groups (the QKV rows)
+    (16, 33000, 1040, 12, True),     # 8 groups, 258 blocks, 16-element K tail
+    (9, 4096, 4096, 21, True),       # 1 group (the O rows)
+    (1, 64, 33024, 12, True),        # one token whose activations exceed 64 KiB
+    (32, 4096, 4096, 21, True),      # 32 tokens: the wide-row GEMM's 32-token tile
 ]
 
 
@@ -333,7 +344,7 @@ def test_grouped_single_expert_equals_dense():
 # -----------------------------------------------------------------------------
 
 def test_workspace_too_small_is_rejected():
-    n, k, m = 4096, 4096, 32
+    n, k, m = 4096, 4096, 64    # 32 weight tiles: K is split, partials need room
     w = workloads.weight_fp16(n, k, seed=81)
     nst = Nested(w, 21)
     need = dps.workspace_bytes(FULL, 0, m, n, k)
