@@ -48,6 +48,7 @@ struct RowsArgs {
     uint64_t slots_const;  // res.slots, read through the scalar cache
     int64_t n, k;
     uint16_t *y;  // FP16 [m][n]
+    int rotate;   // walk the K chunks starting at (block / 4) mod chunks
 };
 
 __device__ __attribute__((aligned(16))) const uint8_t g_rows_zero16[16] = {0};
@@ -127,7 +128,14 @@ __global__ __launch_bounds__(512) void rows_kernel(RowsArgs a)
     const int lg = lane >> 4;
     const int64_t r0 = (int64_t)blockIdx.x * (16 * G);
     const int64_t nkc = (a.k + kRowsKC - 1) / kRowsKC;
-    const int64_t nst = nkc * G;  // stage t: K chunk t / G, row group t % G
+    const int64_t nst = nkc * G;  // stage t: chunk step t / G, row group t % G
+    // Chunk step c reads K chunk kc(c).  When rows are a multiple of 4 KiB
+    // apart, all blocks reading the same chunk at once would hit the same
+    // address bits 10-11; starting each group of four blocks at another chunk
+    // spreads the stream (MI355X, hidden-4096 set at 8 tokens: gate+up and O
+    // 0.81-0.91x the time, QKV 1.03x in full mode; 14 KiB rows lose with it).
+    const int64_t rot = a.rotate ? (int64_t)(blockIdx.x >> 2) % nkc : 0;
+    auto kc = [&](int64_t c) { return c + rot < nkc ? c + rot : c + rot - nkc; };
 
     // ---- DMA: wave w fills rows 2w and 2w+1 of the stage's row group, upper
     // bytes then (full mode) residual bytes: NI = 2 or 4 instructions.  Stages
@@ -135,7 +143,7 @@ __global__ __launch_bounds__(512) void rows_kernel(RowsArgs a)
     auto issue = [&](int64_t t) {
         uint8_t *slot = smem + (int)(t % WS) * SLOT;
         const bool live = t < nst;
-        const int64_t c = live ? t / G : 0;
+        const int64_t c = live ? kc(t / G) : 0;
         const int g = live ? (int)(t % G) : 0;
         int64_t L0[2];
         int64_t sl0[2] = {-1, -1}, sl1[2] = {-1, -1};
@@ -185,9 +193,9 @@ __global__ __launch_bounds__(512) void rows_kernel(RowsArgs a)
             }
     };
 
-    // ---- activations of this wave's K slice for chunk c: step pair s2, half
-    // h, token tile nt -> lane (j, g) holds X[16 nt + j][c KC + 16 (8w + 4 s2
-    // + g) + 8 h .. +7] (token rows past m repeat row m-1).  Always XL load
+    // ---- activations of this wave's K slice for chunk step c: step pair s2,
+    // half h, token tile nt -> lane (j, g) holds X[16 nt + j][kc(c) KC + 16
+    // (8w + 4 s2 + g) + 8 h .. +7] (token rows past m repeat row m-1).  Always XL load
     // instructions (past K: a valid address; the value is cleared at use).
     constexpr int XL = 4 * NT;
     u32x4 xa[2][2][NT], xb[2][2][NT];
@@ -198,7 +206,7 @@ __global__ __launch_bounds__(512) void rows_kernel(RowsArgs a)
             tok = tok < a.m ? tok : a.m - 1;
 #pragma unroll
             for (int s2 = 0; s2 < 2; ++s2) {
-                const int64_t kk = c * kRowsKC + 16 * (8 * wave + 4 * s2 + lg);
+                const int64_t kk = kc(c) * kRowsKC + 16 * (8 * wave + 4 * s2 + lg);
                 const int64_t kv = kk < a.k ? kk : 0;
 #pragma unroll
                 for (int h = 0; h < 2; ++h)
@@ -211,7 +219,7 @@ __global__ __launch_bounds__(512) void rows_kernel(RowsArgs a)
     auto ready_x = [&](int64_t c, u32x4 (&xr)[2][2][NT]) {
 #pragma unroll
         for (int s2 = 0; s2 < 2; ++s2) {
-            const int64_t kk = c * kRowsKC + 16 * (8 * wave + 4 * s2 + lg);
+            const int64_t kk = kc(c) * kRowsKC + 16 * (8 * wave + 4 * s2 + lg);
             const uint32_t msk = 0u - (uint32_t)(kk < a.k);
 #pragma unroll
             for (int h = 0; h < 2; ++h)
@@ -391,6 +399,7 @@ hipError_t launch_rows(const LinearProblem &p, const LinearPlan &plan, hipStream
     a.n = p.n;
     a.k = p.k;
     a.y = p.y;
+    a.rotate = p.k % 4096 == 0;
     const bool range = p.mode == MODE_FULL && p.res.log2c >= 10;
     if (p.enc == ENC_E4M3)
         return p.mode == MODE_FULL
