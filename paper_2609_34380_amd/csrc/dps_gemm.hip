@@ -136,7 +136,10 @@ __device__ __forceinline__ void stage_barrier()
 // slot chunk ^ swz(row), swz(row) = (row / 2) % 8 for the 128-byte rows, so
 // the 16 rows a fragment read touches land in 16 distinct 16-byte bank
 // groups.  Lane (i, g): A = weight row i and B = token row i, bytes
-// 32g .. 32g+31 of the stage.
+// 16g .. 16g+15 and 64+16g .. 64+16g+15 of the stage (the MFMA's 32-byte K
+// slice of lane group g, permuted alike in both operands).  Reading chunks
+// 2g and 2g+1 instead cost ~4 LDS bank-conflict cycles per read (rocprofv3
+// SQ_LDS_BANK_CONFLICT) and 3-5% of the prefill time on MI355X.
 template <int BN_, int BM_, int WN, int WM, int NSTAGE>
 struct G3 {
     static constexpr int BK = 128;
@@ -262,8 +265,8 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
             const int r = wn * C::TN + nt * 16 + li;
             const uint8_t *row = st + r * C::ROW;
             const int sw = g3_swz(r);
-            const u32x4 p = *reinterpret_cast<const u32x4 *>(row + (((2 * lg) ^ sw) << 4));
-            const u32x4 q = *reinterpret_cast<const u32x4 *>(row + (((2 * lg + 1) ^ sw) << 4));
+            const u32x4 p = *reinterpret_cast<const u32x4 *>(row + ((lg ^ sw) << 4));
+            const u32x4 q = *reinterpret_cast<const u32x4 *>(row + (((4 + lg) ^ sw) << 4));
             av[nt] = i32x8{(int)p.x, (int)p.y, (int)p.z, (int)p.w,
                            (int)q.x, (int)q.y, (int)q.z, (int)q.w};
         }
@@ -272,8 +275,8 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
             const int r = wm * C::TM + mt * 16 + li;
             const uint8_t *row = xs + r * C::ROW;
             const int sw = g3_swz(r);
-            const u32x4 p = *reinterpret_cast<const u32x4 *>(row + (((2 * lg) ^ sw) << 4));
-            const u32x4 q = *reinterpret_cast<const u32x4 *>(row + (((2 * lg + 1) ^ sw) << 4));
+            const u32x4 p = *reinterpret_cast<const u32x4 *>(row + ((lg ^ sw) << 4));
+            const u32x4 q = *reinterpret_cast<const u32x4 *>(row + (((4 + lg) ^ sw) << 4));
             const i32x8 bv = {(int)p.x, (int)p.y, (int)p.z, (int)p.w,
                               (int)q.x, (int)q.y, (int)q.z, (int)q.w};
 #pragma unroll
