@@ -18,8 +18,9 @@ Also printed on the same JSON line: the roofline of the dominant call
 (HIP events around back-to-back launches of that call on its stream), the
 CPU oracle timed on a bounded sample on the host cores, a per-call
 breakdown, and secondary figures (prefill TFLOPS on FP8/FP16 matrix cores;
-residual restore from a pinned host backup, alone and under fast-mode
-decode of the hidden-8192 set).
+each (batch size, mode) pass replayed as its own graph; the grouped MoE
+linear; residual restore from a pinned host backup, alone and under
+fast-mode decode of the hidden-8192 set; the SUM manager's cost per call).
 """
 import argparse
 import json
@@ -230,6 +231,7 @@ def main():
     del graphs, g_dom, copies
     torch.cuda.synchronize()
     if not args.no_secondary:
+        secondary["moe_grouped"] = moe_secondary(torch, dps, workloads, stream, enc)
         secondary["restore"] = restore_secondary(torch, dps, workloads, stream, enc)
         secondary["sum_manager"] = sum_secondary(dps)
     torch.cuda.synchronize()
@@ -364,6 +366,60 @@ def prefill_secondary(torch, dps, workloads, nws, layers, stream):
             flops = sum(2.0 * m * n * k for _, n, k in layers)
             res[label] = {"M": m, "ms": round(t * 1e3, 3), "TFLOPs": round(flops / t / 1e12, 1),
                           "frac_of_peak": round(flops / t / 1e12 / peak, 3)}
+    return res
+
+
+def moe_secondary(torch, dps, workloads, stream, enc):
+    """Grouped MoE linear (8 experts, hidden 4096, ffn 14336; 512 tokens routed
+    top-2 by uniform random choice, so 1024 rows grouped by expert): the
+    stacked gate+up and down weights through dps_linear_grouped in both
+    modes.  One weight copy per layer (1.41 GB of upper bytes, as much again
+    of residual) is far beyond the 256 MB Infinity Cache, so reads come from
+    HBM.  GB/s counts the weight-plane bytes each mode must read."""
+    dev = torch.device("cuda:0")
+    experts, tokens, topk = 8, 512, 2
+    rows = tokens * topk
+    token_of_row, offsets = workloads.moe_routing(tokens, experts, topk, seed=901)
+    res = {"workload": "moe_8x4096x14336, 512 tokens top-2 (%d routed rows)" % rows,
+           "encoding": "e4m3" if enc == dps.ENC_E4M3 else "e5m2"}
+    with torch.cuda.stream(stream):
+        off_dev = offsets.to(torch.int32).to(dev)
+        tok_dev = token_of_row.to(dev)
+        layers = []
+        for li, (name, n, k) in enumerate(workloads.MOE_SHAPES):
+            w = workloads.weight_fp16(n, k, seed=910 + li, experts=experts, device=dev)
+            nw = dps.split(w, dps.make_residual(w.numel(), 21, dev), enc=enc)
+            del w
+            x = workloads.activations_fp16(tokens, k, seed=920 + li, device=dev)
+            layers.append((nw, x[tok_dev].contiguous(),
+                           torch.empty((rows, n), dtype=torch.float16, device=dev), n, k))
+        need = max(dps.workspace_bytes(mode, 0, rows, n, k, experts)
+                   for _, _, _, n, k in layers for mode in (dps.MODE_FAST, dps.MODE_FULL))
+        ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+        for label, mode in (("fast", dps.MODE_FAST), ("full", dps.MODE_FULL)):
+            def one():
+                for nw, x, y, _, _ in layers:
+                    dps.linear_grouped(x, off_dev, nw, mode, out=y, workspace=ws)
+            one()
+            stream.synchronize()
+            reps = 10
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                one()
+            e1.record(stream)
+            stream.synchronize()
+            t = e0.elapsed_time(e1) * 1e-3 / reps
+            wbytes = sum(experts * n * k for _, _, _, n, k in layers) * (
+                1 if mode == dps.MODE_FAST else 2)
+            flops = sum(2.0 * rows * n * k for _, _, _, n, k in layers)
+            res[label] = {"ms": round(t * 1e3, 3), "GBs": round(wbytes / t / 1e9, 1),
+                          "TFLOPs": round(flops / t / 1e12, 1),
+                          "frac_of_mfma_peak": round(flops / t / 1e12 / MFMA_F16_TFLOPS, 3)}
+        del layers, ws
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
     return res
 
 
