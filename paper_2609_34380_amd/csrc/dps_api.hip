@@ -147,8 +147,11 @@ LinearPlan plan_linear(int mode, uint32_t flags, int64_t rows, int64_t n, int64_
     const int64_t rows_per_expert = grouped ? cdiv(rows, experts) : rows;
     if (flags & DPS_ACT_FP8_ROWSCALE) {
         p.kind = KIND_GEMM_FP8;
-        // measured on MI355X: 256 x 256 tiles for wide layers, 256 x 128 otherwise
-        p.variant = (n > 4096 && rows > 128) ? GEMM_G3_256x256 : GEMM_G3_256x128;
+        // 256 x 256 tiles once their grid holds at least two blocks per CU,
+        // else 256 x 128 (MI355X, 2048 tokens: gate+up 280 against 310 us on
+        // 256 x 128; QKV, 192 blocks of 256 x 256, 114 against 132 us)
+        p.variant = cdiv(n, 256) * cdiv(rows, 256) >= 2 * (int64_t)cu_count ? GEMM_G3_256x256
+                                                                           : GEMM_G3_256x128;
         const int64_t tiles =
             cdiv(n, gemm_rows_per_block(p.variant)) * cdiv(rows, gemm_tokens_per_block(p.variant));
         int64_t s = cdiv(target, tiles);

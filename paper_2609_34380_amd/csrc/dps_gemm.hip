@@ -131,8 +131,10 @@ __device__ __forceinline__ void stage_barrier()
 // ------------------------------------------------------------------------------
 // Block tile BN weight rows x BM tokens, waves in a WN x WM grid, each wave
 // (BN/WN) x (BM/WM).  A stage covers 128 K elements (one 16x16x128 MFMA
-// step).  Stages stream global -> LDS by direct-to-LDS loads through a ring
-// of NSTAGE slots, one barrier per stage.  LDS rows hold 16-byte chunks at
+// step).  Stages stream global -> LDS by direct-to-LDS loads, weights and
+// tokens through separate rings of WS and XS slots (the 256 x 256 tile keeps
+// two weight stages in flight within 160 KiB), one barrier per stage.  LDS
+// rows hold 16-byte chunks at
 // slot chunk ^ swz(row), swz(row) = (row / 2) % 8 for the 128-byte rows, so
 // the 16 rows a fragment read touches land in 16 distinct 16-byte bank
 // groups.  Lane (i, g): A = weight row i and B = token row i, bytes
@@ -140,18 +142,23 @@ __device__ __forceinline__ void stage_barrier()
 // slice of lane group g, permuted alike in both operands).  Reading chunks
 // 2g and 2g+1 instead cost ~4 LDS bank-conflict cycles per read (rocprofv3
 // SQ_LDS_BANK_CONFLICT) and 3-5% of the prefill time on MI355X.
-template <int BN_, int BM_, int WN, int WM, int NSTAGE>
+template <int BN_, int BM_, int WN, int WM, int WS, int XS>
 struct G3 {
     static constexpr int BK = 128;
     static constexpr int ROW = BK;                   // bytes per row, both operands
     static constexpr int W_BYTES = BN_ * ROW;
     static constexpr int X_BYTES = BM_ * ROW;
-    static constexpr int STAGE = W_BYTES + X_BYTES;
-    static constexpr int LDS = STAGE * NSTAGE;
+    static constexpr int X_BASE = W_BYTES * WS;      // weight ring, then token ring
+    static constexpr int LDS = X_BASE + X_BYTES * XS;
     static constexpr int NWAVES = WN * WM;
     static constexpr int W_INSTR = W_BYTES / 1024 / NWAVES;
     static constexpr int X_INSTR = X_BYTES / 1024 / NWAVES;
-    static constexpr int NI = W_INSTR + X_INSTR;
+    // Iteration t issues tokens of stage t+XS-1, then weights of stage
+    // t+WS-1 (XS <= WS).  At the wait for stage t the instructions issued
+    // after the later of tokens t and weights t may stay outstanding.
+    static constexpr int OUTSTANDING =
+        (XS < WS ? W_INSTR : 0) + (XS - 2) * (W_INSTR + X_INSTR);
+    static_assert(WS >= 2 && XS >= 2 && XS <= WS, "ring depths");
     static constexpr int TN = BN_ / WN, TM = BM_ / WM;
     static constexpr int NT = TN / 16, MT = TM / 16;
     static_assert(W_BYTES % (1024 * NWAVES) == 0 && X_BYTES % (1024 * NWAVES) == 0, "tiling");
@@ -160,10 +167,10 @@ struct G3 {
 
 __device__ __forceinline__ int g3_swz(int r) { return (r >> 1) & 7; }
 
-template <int ENC, int BN_, int BM_, int WN, int WM, int NSTAGE>
+template <int ENC, int BN_, int BM_, int WN, int WM, int WS, int XS>
 __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
 {
-    using C = G3<BN_, BM_, WN, WM, NSTAGE>;
+    using C = G3<BN_, BM_, WN, WM, WS, XS>;
     __shared__ __attribute__((aligned(16))) uint8_t smem[C::LDS];
 
     const int tid = threadIdx.x;
@@ -220,8 +227,8 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
         xel[jj] = ((lane & 7) ^ g3_swz(r)) * 16;
     }
 
-    auto issue = [&](int64_t t) {
-        uint8_t *st = smem + (int)(t % NSTAGE) * C::STAGE;
+    auto issue_w = [&](int64_t t) {
+        uint8_t *st = smem + (int)(t % WS) * C::W_BYTES;
         const bool live = t < ntk;
         const int64_t kt = kb0 + t * C::BK;
 #pragma unroll
@@ -231,13 +238,17 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
             const bool ok = live && kk < ke;
             dma16(ok ? (const void *)(wsrc[jj] + kk) : (const void *)g_zero16, st + j * 1024);
         }
+    };
+    auto issue_x = [&](int64_t t) {
+        uint8_t *st = smem + C::X_BASE + (int)(t % XS) * C::X_BYTES;
+        const bool live = t < ntk;
+        const int64_t kt = kb0 + t * C::BK;
 #pragma unroll
         for (int jj = 0; jj < C::X_INSTR; ++jj) {
             const int j = wave * C::X_INSTR + jj;
             const int64_t kk = kt + xel[jj];
             const bool ok = live && kk < ke;
-            dma16(ok ? (const void *)(xsrc[jj] + kk) : (const void *)g_zero16,
-                  st + C::W_BYTES + j * 1024);
+            dma16(ok ? (const void *)(xsrc[jj] + kk) : (const void *)g_zero16, st + j * 1024);
         }
     };
 
@@ -250,15 +261,22 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
         for (int j = 0; j < C::MT; ++j)
             acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+    // prologue: the steady-state issue of iterations -(WS-1) .. -1, keeping
+    // only stages >= 0
 #pragma unroll
-    for (int t = 0; t < NSTAGE - 1; ++t)
-        issue(t);
+    for (int u = -(WS - 1); u < 0; ++u) {
+        if (u + XS - 1 >= 0)
+            issue_x(u + XS - 1);
+        if (u + WS - 1 >= 0)
+            issue_w(u + WS - 1);
+    }
     for (int64_t t = 0; t < ntk; ++t) {
-        DPS_WAIT_VMCNT(C::NI * (NSTAGE - 2));
+        DPS_WAIT_VMCNT(C::OUTSTANDING);  // tokens t and weights t have landed
         stage_barrier();
-        issue(t + NSTAGE - 1);
-        const uint8_t *st = smem + (int)(t % NSTAGE) * C::STAGE;
-        const uint8_t *xs = st + C::W_BYTES;
+        issue_x(t + XS - 1);
+        issue_w(t + WS - 1);
+        const uint8_t *st = smem + (int)(t % WS) * C::W_BYTES;
+        const uint8_t *xs = smem + C::X_BASE + (int)(t % XS) * C::X_BYTES;
         i32x8 av[C::NT];
 #pragma unroll
         for (int nt = 0; nt < C::NT; ++nt) {
@@ -676,12 +694,12 @@ dim3 dense_grid(int64_t tiles)
     return dim3((unsigned)((tiles + 7) / 8 * 8), 1, 1);
 }
 
-template <int ENC, int BN_, int BM_, int WN, int WM, int NS>
+template <int ENC, int BN_, int BM_, int WN, int WM, int WS, int XS>
 hipError_t launch_g3(const GemmArgs &a, const LinearPlan &plan, hipStream_t stream)
 {
     const int64_t nt = (a.n + BN_ - 1) / BN_;
     const dim3 grid = dense_grid(nt * plan.splits * ((a.rows + BM_ - 1) / BM_));
-    hipLaunchKernelGGL((gemm3_kernel<ENC, BN_, BM_, WN, WM, NS>), grid, dim3(WN * WM * 64), 0,
+    hipLaunchKernelGGL((gemm3_kernel<ENC, BN_, BM_, WN, WM, WS, XS>), grid, dim3(WN * WM * 64), 0,
                        stream, a);
     return hipGetLastError();
 }
@@ -690,8 +708,8 @@ template <int ENC>
 hipError_t launch_g3_variant(const GemmArgs &a, const LinearPlan &plan, hipStream_t stream)
 {
     switch (plan.variant) {
-    case GEMM_G3_256x256: return launch_g3<ENC, 256, 256, 2, 4, 2>(a, plan, stream);
-    case GEMM_G3_256x128: return launch_g3<ENC, 256, 128, 4, 2, 3>(a, plan, stream);
+    case GEMM_G3_256x256: return launch_g3<ENC, 256, 256, 2, 4, 3, 2>(a, plan, stream);
+    case GEMM_G3_256x128: return launch_g3<ENC, 256, 128, 4, 2, 3, 3>(a, plan, stream);
     default: return hipErrorInvalidValue;
     }
 }
