@@ -163,3 +163,25 @@ def test_workspace_query(lib):
     assert lib.dps_workspace_bytes(0, 0, 0, 64, 64, 1) == 0
     # FP8 activations always need room for the quantized copy
     assert lib.dps_workspace_bytes(1, 1, 2048, 4096, 4096, 1) >= 2048 * 4096
+
+
+@pytest.mark.parametrize("mode", [0, 1], ids=["full", "fast"])
+def test_planner_whole_rows_up_to_16_tokens(lib, mode):
+    """Dense calls of up to 16 tokens run on whole-row kernels (row GEMV or
+    the 16-row-group MFMA kernel): K is never split, so no workspace.  The
+    hidden-4096 layers and awkward shapes alike."""
+    for m, n, k in ((1, 4096, 4096), (2, 28672, 4096), (3, 28672, 4096), (4, 4096, 14336),
+                    (8, 6144, 4096), (8, 28672, 4096), (16, 4096, 14336), (16, 33000, 1040),
+                    (1, 64, 33024)):
+        assert lib.dps_workspace_bytes(mode, 0, m, n, k, 1) == 0, (m, n, k)
+
+
+@pytest.mark.parametrize("mode", [0, 1], ids=["full", "fast"])
+def test_planner_splits_k_for_narrow_layers_beyond_16_tokens(lib, mode):
+    """From 17 tokens on, the 4096 x 4096 layer has too few 128-row weight
+    tiles to fill the chip, so K is split and the fp32 partials [splits][m][n]
+    need workspace; the plan does not depend on the mode."""
+    for m in (17, 32, 128):
+        ws = lib.dps_workspace_bytes(mode, 0, m, 4096, 4096, 1)
+        assert ws >= 2 * m * 4096 * 4, (m, ws)
+        assert ws == lib.dps_workspace_bytes(1 - mode, 0, m, 4096, 4096, 1)
