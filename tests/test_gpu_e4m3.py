@@ -149,6 +149,7 @@ E4M3_CASES = [
     (300, 512, 512, 16, True, True),
     (8, 28672, 1024, 21, True, True),
     (15, 4100, 2064, 9, True, False),
+    (6, 24, 1024, 9, True, True),
 ]
 
 

@@ -159,6 +159,9 @@ LINEAR_CASES = [
     (16, 33000, 1040, 12, True),     # 8 groups, 258 blocks, 16-element K tail
     (9, 4096, 4096, 21, True),       # 1 group (the O rows)
     (1, 64, 33024, 12, True),        # one token whose activations exceed 64 KiB
+    (7, 5, 2048, 12, True),          # fewer rows than one group
+    (16, 17, 1024, 10, False),       # one row past a group
+    (13, 4112, 4096, 21, True),      # 257 groups: two per block, the last block half empty
     (32, 4096, 4096, 21, True),      # 32 tokens: the wide-row GEMM's 32-token tile
 ]
 
