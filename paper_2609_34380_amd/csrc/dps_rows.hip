@@ -76,7 +76,8 @@ __device__ __forceinline__ int rows_swz(int i) { return (i & 15) << 2; }
 // compiler's own wait analysis loses count across the chunk loop and would
 // wait for every load in flight (draining the DMA ring) before each use.
 // The value may only be read after a vmcnt wait that retires it, followed
-// by rows_tie on it.
+// by rows_tie on it; nor may the compiler spill or copy it before then, so
+// the build rejects any kernel of this file that uses scratch.
 __device__ __forceinline__ u32x4 rows_gload16(const void *p)
 {
     u32x4 v;

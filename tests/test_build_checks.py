@@ -1,0 +1,22 @@
+"""Host checks of the build driver (no GPU): the scratch report parser that
+guards the kernels whose loads the compiler does not track."""
+from paper_2609_34380_amd.csrc import build
+
+
+REPORT = """\
+a.hip:10:0: remark: Function Name: _Zk1 [-Rpass-analysis=kernel-resource-usage]
+a.hip:10:0: remark:     VGPRs: 90 [-Rpass-analysis=kernel-resource-usage]
+a.hip:10:0: remark:     ScratchSize [bytes/lane]: 0 [-Rpass-analysis=kernel-resource-usage]
+a.hip:20:0: remark: Function Name: _Zk2 [-Rpass-analysis=kernel-resource-usage]
+a.hip:20:0: remark:     ScratchSize [bytes/lane]: 44 [-Rpass-analysis=kernel-resource-usage]
+"""
+
+
+def test_scratch_users_names_only_spilling_kernels():
+    assert build._scratch_users(REPORT) == [("_Zk2", 44)]
+    assert build._scratch_users("") == []
+
+
+def test_untracked_load_sources_are_checked():
+    assert "dps_rows.hip" in build.NO_SCRATCH
+    assert build.NO_SCRATCH <= set(build.SOURCES)
