@@ -333,39 +333,43 @@ def probe(args, torch, dps, workloads, layers, dev, stream, enc):
 
 
 def prefill_secondary(torch, dps, workloads, nws, layers, stream):
-    """Prefill (M = 2048) over the layer set: fast mode on FP8 matrix cores
-    (row-quantized activations), full mode on FP16 matrix cores."""
+    """Prefill (M = 2048 and 8192) over the layer set: fast mode on FP8 matrix
+    cores (row-quantized activations), full mode on FP16 matrix cores."""
     dev = torch.device("cuda:0")
-    m = 2048
     res = {}
-    with torch.cuda.stream(stream):
-        xs = {k: workloads.activations_fp16(m, k, seed=k + 5, outlier_frac=0.01,
-                                            outlier_scale=20.0, device=dev)
-              for k in sorted({k for _, _, k in layers})}
-        ys = {n: torch.empty((m, n), dtype=torch.float16, device=dev)
-              for n in sorted({n for _, n, _ in layers})}
-        need = max(dps.workspace_bytes(mode, act, m, n, k) for _, n, k in layers
-                   for mode, act in ((dps.MODE_FAST, 1), (dps.MODE_FULL, 0)))
-        ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
-        for label, mode, act, peak in (("fast_fp8", dps.MODE_FAST, "fp8", MFMA_FP8_TFLOPS),
-                                       ("full_f16", dps.MODE_FULL, "fp16", MFMA_F16_TFLOPS)):
-            def one():
-                for li, (name, n, k) in enumerate(layers):
-                    dps.linear(xs[k], nws[li], mode, act=act, out=ys[n], workspace=ws)
-            one()
-            stream.synchronize()
-            reps = 5
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            for _ in range(reps):
+    for m in (2048, 8192):
+        with torch.cuda.stream(stream):
+            xs = {k: workloads.activations_fp16(m, k, seed=k + 5, outlier_frac=0.01,
+                                                outlier_scale=20.0, device=dev)
+                  for k in sorted({k for _, _, k in layers})}
+            ys = {n: torch.empty((m, n), dtype=torch.float16, device=dev)
+                  for n in sorted({n for _, n, _ in layers})}
+            need = max(dps.workspace_bytes(mode, act, m, n, k) for _, n, k in layers
+                       for mode, act in ((dps.MODE_FAST, 1), (dps.MODE_FULL, 0)))
+            ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+            for label, mode, act, peak in (("fast_fp8", dps.MODE_FAST, "fp8", MFMA_FP8_TFLOPS),
+                                           ("full_f16", dps.MODE_FULL, "fp16",
+                                            MFMA_F16_TFLOPS)):
+                def one():
+                    for li, (name, n, k) in enumerate(layers):
+                        dps.linear(xs[k], nws[li], mode, act=act, out=ys[n], workspace=ws)
                 one()
-            e1.record(stream)
-            stream.synchronize()
-            t = e0.elapsed_time(e1) * 1e-3 / reps
-            flops = sum(2.0 * m * n * k for _, n, k in layers)
-            res[label] = {"M": m, "ms": round(t * 1e3, 3), "TFLOPs": round(flops / t / 1e12, 1),
-                          "frac_of_peak": round(flops / t / 1e12 / peak, 3)}
+                stream.synchronize()
+                reps = 5 if m <= 2048 else 2
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                for _ in range(reps):
+                    one()
+                e1.record(stream)
+                stream.synchronize()
+                t = e0.elapsed_time(e1) * 1e-3 / reps
+                flops = sum(2.0 * m * n * k for _, n, k in layers)
+                res[label if m == 2048 else "%s_M%d" % (label, m)] = {
+                    "M": m, "ms": round(t * 1e3, 3), "TFLOPs": round(flops / t / 1e12, 1),
+                    "frac_of_peak": round(flops / t / 1e12 / peak, 3)}
+            del xs, ys, ws
+    torch.cuda.empty_cache()
     return res
 
 
@@ -460,7 +464,8 @@ def restore_secondary(torch, dps, workloads, stream, enc):
     its own) for the hidden-8192 layer set with 2 MiB residual chunks at
     seeded random slots of a pool twice the residual's size (the other slots
     stand for KV blocks), alone and while fast-mode decode (64 tokens, the
-    four layers) runs on the compute stream."""
+    four layers) runs on the compute stream; and the decode steps of that set
+    with the mode alternating step by step (per-mode medians)."""
     dev = torch.device("cuda:0")
     log2c = 21
     m = 64
@@ -522,6 +527,34 @@ def restore_secondary(torch, dps, workloads, stream, enc):
     t_plain = e0.elapsed_time(e1) * 1e-3 / reps
     del src, dst
 
+    # modes alternating step by step (fast, full, fast, ...), each step between
+    # events: per-mode medians over the sequence
+    wbytes = sum(n * k for _, n, k in layers)
+    per_mode = {dps.MODE_FAST: [], dps.MODE_FULL: []}
+    with torch.cuda.stream(stream):
+        seq = [(ev(), ev(), dps.MODE_FAST if i % 2 == 0 else dps.MODE_FULL) for i in range(40)]
+        for mode in (dps.MODE_FAST, dps.MODE_FULL):
+            for li, (name, n, k) in enumerate(layers):
+                dps.linear(xs[k], nws[li], mode, out=ys[n])
+        for a, b, mode in seq:
+            a.record(stream)
+            for li, (name, n, k) in enumerate(layers):
+                dps.linear(xs[k], nws[li], mode, out=ys[n])
+            b.record(stream)
+    stream.synchronize()
+    for a, b, mode in seq:
+        per_mode[mode].append(a.elapsed_time(b) * 1e-3)
+
+    def med(v):
+        v = sorted(v)
+        return v[len(v) // 2]
+    alternating = {
+        "fast_ms_median": round(med(per_mode[dps.MODE_FAST]) * 1e3, 4),
+        "full_ms_median": round(med(per_mode[dps.MODE_FULL]) * 1e3, 4),
+        "fast_GBs": round(wbytes / med(per_mode[dps.MODE_FAST]) / 1e9, 1),
+        "full_GBs": round(2 * wbytes / med(per_mode[dps.MODE_FULL]) / 1e9, 1),
+        "steps": len(seq)}
+
     # fast-mode decode alone
     steps = 40
     with torch.cuda.stream(stream):
@@ -566,6 +599,7 @@ def restore_secondary(torch, dps, workloads, stream, enc):
             "decode_step_ms_during_restore": (round(t_step_conc * 1e3, 4)
                                               if t_step_conc else None),
             "decode_steps_overlapped": len(inside),
+            "alternating_modes": alternating,
             "restore_ms_during_decode": round(t_r_conc * 1e3, 3),
             "restore_GBs_during_decode": round(total / t_r_conc / 1e9, 1)}
 
