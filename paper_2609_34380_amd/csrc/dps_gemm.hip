@@ -678,10 +678,8 @@ int gemm_tokens_per_block(int variant)
 {
     switch (variant) {
     case GEMM_G3_256x256: return 256;
-    case GEMM_G4_128x64:
     case GEMM_G4S_128x64: return 64;
-    case GEMM_G4_128x32:
-    case GEMM_G4S_128x32: return 32;
+    case GEMM_G4_128x32: return 32;
     default: return 128;
     }
 }
@@ -739,22 +737,16 @@ hipError_t launch_g4_variant(const GemmArgs &a, const LinearPlan &plan, bool gro
 {
     if constexpr (MODE == MODE_FULL) {
         switch (plan.variant) {
-        case GEMM_G4_128x128: return launch_g4<MODE, ENC, 128, 3, 2, false>(a, plan, grouped, stream);
-        case GEMM_G4_128x64: return launch_g4<MODE, ENC, 64, 4, 2, false>(a, plan, grouped, stream);
         case GEMM_G4_128x32: return launch_g4<MODE, ENC, 32, 4, 4, false>(a, plan, grouped, stream);
         case GEMM_G4S_128x128: return launch_g4<MODE, ENC, 128, 3, 2, true>(a, plan, grouped, stream);
         case GEMM_G4S_128x64: return launch_g4<MODE, ENC, 64, 4, 2, true>(a, plan, grouped, stream);
-        case GEMM_G4S_128x32: return launch_g4<MODE, ENC, 32, 4, 4, true>(a, plan, grouped, stream);
         default: return hipErrorInvalidValue;
         }
     } else {
         switch (plan.variant) {
-        case GEMM_G4_128x128: return launch_g4<MODE, ENC, 128, 4, 3, false>(a, plan, grouped, stream);
-        case GEMM_G4_128x64: return launch_g4<MODE, ENC, 64, 6, 4, false>(a, plan, grouped, stream);
         case GEMM_G4_128x32: return launch_g4<MODE, ENC, 32, 8, 4, false>(a, plan, grouped, stream);
         case GEMM_G4S_128x128: return launch_g4<MODE, ENC, 128, 4, 3, true>(a, plan, grouped, stream);
         case GEMM_G4S_128x64: return launch_g4<MODE, ENC, 64, 6, 4, true>(a, plan, grouped, stream);
-        case GEMM_G4S_128x32: return launch_g4<MODE, ENC, 32, 8, 4, true>(a, plan, grouped, stream);
         default: return hipErrorInvalidValue;
         }
     }

@@ -57,14 +57,11 @@ enum GemmVariant {
     GEMM_G3_256x256 = 0,
     GEMM_G3_256x128 = 1,
     // FP16 activations: 128-element stages with wide-row loads, K split over
-    // waves
-    GEMM_G4_128x128 = 2,
-    GEMM_G4_128x64 = 3,
-    GEMM_G4_128x32 = 4,
-    // the same with four dedicated DMA waves
-    GEMM_G4S_128x128 = 5,
-    GEMM_G4S_128x64 = 6,
-    GEMM_G4S_128x32 = 7
+    // waves; up to 32 tokens the eight compute waves issue the DMA, from 64
+    // tokens on four dedicated DMA waves do (the planner's three tiles)
+    GEMM_G4_128x32 = 2,
+    GEMM_G4S_128x64 = 3,
+    GEMM_G4S_128x128 = 4
 };
 // Decode-kernel variants 0 and 1 keep the weight stream in registers (16 or
 // 32 weight rows per wave); SKINNY_RING streams it through per-wave LDS rings.
