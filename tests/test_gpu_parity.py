@@ -108,18 +108,29 @@ def test_quant_rows_bit_exact():
     assert np.array_equal(xq.cpu().numpy(), xq_ref)
 
 
-def test_quant_rows_every_fp16_value():
-    """Every finite FP16 value with |x| <= 448 in one row (scale 1)."""
+@pytest.mark.parametrize("k", [1024, 8192, 16384, 0])
+def test_quant_rows_every_fp16_value(k):
+    """Every finite FP16 value with |x| <= 448, at scale 1: in rows of k
+    elements (each row ends with 448, so its scale is 1; rows of up to 16384
+    elements take the wave-per-row kernel), or all in one row (k = 0, the
+    block-per-row kernel)."""
     bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
     v = bits.view(np.float16).astype(np.float64)
     keep = bits[np.isfinite(v) & (np.abs(v) <= 448)]
-    pad = (-keep.size) % 16
-    row = np.concatenate([keep, np.zeros(pad, np.uint16)])
-    x = torch.from_numpy(row.view(np.int16).copy()).view(torch.float16).reshape(1, -1)
+    if k == 0:
+        pad = (-keep.size) % 16
+        mat = np.concatenate([keep, np.zeros(pad, np.uint16)]).reshape(1, -1)
+    else:
+        per = k - 1
+        rows = -(-keep.size // per)
+        body = np.concatenate([keep, np.zeros(rows * per - keep.size, np.uint16)])
+        top = np.full((rows, 1), np.float16(448.0).view(np.uint16), np.uint16)
+        mat = np.concatenate([body.reshape(rows, per), top], axis=1)
+    x = torch.from_numpy(mat.view(np.int16).copy()).view(torch.float16)
     xq, s = dps.quant_rows_e4m3(x.to(DEV))
     torch.cuda.synchronize()
-    xq_ref, s_ref = oracle.act_quant(row.reshape(1, -1))
-    assert s_ref[0] == 1.0 and s.item() == 1.0
+    xq_ref, s_ref = oracle.act_quant(mat)
+    assert np.all(s_ref == 1.0) and np.all(s.cpu().numpy() == 1.0)
     assert np.array_equal(xq.cpu().numpy(), xq_ref)
 
 
