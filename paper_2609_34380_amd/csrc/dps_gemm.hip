@@ -142,7 +142,7 @@ __device__ __forceinline__ void stage_barrier()
 // slice of lane group g, permuted alike in both operands).  Reading chunks
 // 2g and 2g+1 instead cost ~4 LDS bank-conflict cycles per read (rocprofv3
 // SQ_LDS_BANK_CONFLICT) and 3-5% of the prefill time on MI355X.
-template <int BN_, int BM_, int WN, int WM, int WS, int XS>
+template <int BN_, int BM_, int WN, int WM, int WS, int XS, bool DW>
 struct G3 {
     static constexpr int BK = 128;
     static constexpr int ROW = BK;                   // bytes per row, both operands
@@ -150,9 +150,10 @@ struct G3 {
     static constexpr int X_BYTES = BM_ * ROW;
     static constexpr int X_BASE = W_BYTES * WS;      // weight ring, then token ring
     static constexpr int LDS = X_BASE + X_BYTES * XS;
-    static constexpr int NWAVES = WN * WM;
-    static constexpr int W_INSTR = W_BYTES / 1024 / NWAVES;
-    static constexpr int X_INSTR = X_BYTES / 1024 / NWAVES;
+    static constexpr int NWAVES = WN * WM;                  // compute waves
+    static constexpr int NISS = DW ? 4 : NWAVES;            // waves that issue the DMA
+    static constexpr int W_INSTR = W_BYTES / 1024 / NISS;
+    static constexpr int X_INSTR = X_BYTES / 1024 / NISS;
     // Iteration t issues tokens of stage t+XS-1, then weights of stage
     // t+WS-1 (XS <= WS).  At the wait for stage t the instructions issued
     // after the later of tokens t and weights t may stay outstanding.
@@ -161,16 +162,16 @@ struct G3 {
     static_assert(WS >= 2 && XS >= 2 && XS <= WS, "ring depths");
     static constexpr int TN = BN_ / WN, TM = BM_ / WM;
     static constexpr int NT = TN / 16, MT = TM / 16;
-    static_assert(W_BYTES % (1024 * NWAVES) == 0 && X_BYTES % (1024 * NWAVES) == 0, "tiling");
+    static_assert(W_BYTES % (1024 * NISS) == 0 && X_BYTES % (1024 * NISS) == 0, "tiling");
     static_assert(LDS <= 160 * 1024, "LDS");
 };
 
 __device__ __forceinline__ int g3_swz(int r) { return (r >> 1) & 7; }
 
-template <int ENC, int BN_, int BM_, int WN, int WM, int WS, int XS>
-__global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
+template <int ENC, int BN_, int BM_, int WN, int WM, int WS, int XS, bool DW>
+__global__ __launch_bounds__(WN * WM * 64 + (DW ? 256 : 0)) void gemm3_kernel(GemmArgs a)
 {
-    using C = G3<BN_, BM_, WN, WM, WS, XS>;
+    using C = G3<BN_, BM_, WN, WM, WS, XS, DW>;
     __shared__ __attribute__((aligned(16))) uint8_t smem[C::LDS];
 
     const int tid = threadIdx.x;
@@ -178,6 +179,12 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
     const int wave = tid >> 6;
     const int li = lane & 15;
     const int lg = lane >> 4;
+    // DW: four more waves (one per SIMD) only issue the direct-to-LDS loads
+    // and wait for them; a wave that issues vector-memory instructions stalls
+    // on them, and the compute waves then keep the matrix cores busy instead
+    const bool dma_wave = DW && wave >= C::NWAVES;
+    const int iss = DW ? wave - C::NWAVES : wave;  // index among the issuing waves
+    const bool issues = !DW || dma_wave;
 
     // 1-D grid remapped for the 8 XCDs: block L runs on XCD L % 8, so XCD x
     // is given the contiguous tile range [x * per_xcd, (x+1) * per_xcd),
@@ -207,8 +214,8 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
     const uint8_t *wsrc[C::W_INSTR];
     int wel[C::W_INSTR];  // K offset of this lane's chunk within the stage
 #pragma unroll
-    for (int jj = 0; jj < C::W_INSTR; ++jj) {
-        const int j = wave * C::W_INSTR + jj;
+    for (int jj = 0; jj < C::W_INSTR && issues; ++jj) {
+        const int j = iss * C::W_INSTR + jj;
         const int r = 8 * j + (lane >> 3);
         int64_t nr = n0 + r;
         nr = nr < a.n ? nr : a.n - 1;
@@ -218,8 +225,8 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
     const uint8_t *xsrc[C::X_INSTR];
     int xel[C::X_INSTR];
 #pragma unroll
-    for (int jj = 0; jj < C::X_INSTR; ++jj) {
-        const int j = wave * C::X_INSTR + jj;
+    for (int jj = 0; jj < C::X_INSTR && issues; ++jj) {
+        const int j = iss * C::X_INSTR + jj;
         const int r = 8 * j + (lane >> 3);
         int64_t m = mrow0 + r;
         m = m < mrow1 ? m : mrow1 - 1;
@@ -233,7 +240,7 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
         const int64_t kt = kb0 + t * C::BK;
 #pragma unroll
         for (int jj = 0; jj < C::W_INSTR; ++jj) {
-            const int j = wave * C::W_INSTR + jj;
+            const int j = iss * C::W_INSTR + jj;
             const int64_t kk = kt + wel[jj];
             const bool ok = live && kk < ke;
             dma16(ok ? (const void *)(wsrc[jj] + kk) : (const void *)g_zero16, st + j * 1024);
@@ -245,7 +252,7 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
         const int64_t kt = kb0 + t * C::BK;
 #pragma unroll
         for (int jj = 0; jj < C::X_INSTR; ++jj) {
-            const int j = wave * C::X_INSTR + jj;
+            const int j = iss * C::X_INSTR + jj;
             const int64_t kk = kt + xel[jj];
             const bool ok = live && kk < ke;
             dma16(ok ? (const void *)(xsrc[jj] + kk) : (const void *)g_zero16, st + j * 1024);
@@ -264,17 +271,22 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
     // prologue: the steady-state issue of iterations -(WS-1) .. -1, keeping
     // only stages >= 0
 #pragma unroll
-    for (int u = -(WS - 1); u < 0; ++u) {
+    for (int u = -(WS - 1); u < 0 && issues; ++u) {
         if (u + XS - 1 >= 0)
             issue_x(u + XS - 1);
         if (u + WS - 1 >= 0)
             issue_w(u + WS - 1);
     }
     for (int64_t t = 0; t < ntk; ++t) {
-        DPS_WAIT_VMCNT(C::OUTSTANDING);  // tokens t and weights t have landed
+        if (issues)
+            DPS_WAIT_VMCNT(C::OUTSTANDING);  // tokens t and weights t have landed
         stage_barrier();
-        issue_x(t + XS - 1);
-        issue_w(t + WS - 1);
+        if (issues) {
+            issue_x(t + XS - 1);
+            issue_w(t + WS - 1);
+        }
+        if (dma_wave)
+            continue;
         const uint8_t *st = smem + (int)(t % WS) * C::W_BYTES;
         const uint8_t *xs = smem + C::X_BASE + (int)(t % XS) * C::X_BYTES;
         i32x8 av[C::NT];
@@ -303,6 +315,8 @@ __global__ __launch_bounds__(WN * WM * 64) void gemm3_kernel(GemmArgs a)
         }
     }
     DPS_WAIT_VMCNT(0);  // no DMA may still target this block's LDS when it exits
+    if (dma_wave)
+        return;
 
     // E4M3 weights carry the fast-mode factor 2^-8 (exact in fp32)
     constexpr float wscale = ENC == ENC_E4M3 ? 0.00390625f : 1.f;
@@ -692,12 +706,13 @@ dim3 dense_grid(int64_t tiles)
     return dim3((unsigned)((tiles + 7) / 8 * 8), 1, 1);
 }
 
-template <int ENC, int BN_, int BM_, int WN, int WM, int WS, int XS>
+template <int ENC, int BN_, int BM_, int WN, int WM, int WS, int XS, bool DW>
 hipError_t launch_g3(const GemmArgs &a, const LinearPlan &plan, hipStream_t stream)
 {
     const int64_t nt = (a.n + BN_ - 1) / BN_;
     const dim3 grid = dense_grid(nt * plan.splits * ((a.rows + BM_ - 1) / BM_));
-    hipLaunchKernelGGL((gemm3_kernel<ENC, BN_, BM_, WN, WM, WS, XS>), grid, dim3(WN * WM * 64), 0,
+    hipLaunchKernelGGL((gemm3_kernel<ENC, BN_, BM_, WN, WM, WS, XS, DW>), grid,
+                       dim3(WN * WM * 64 + (DW ? 256 : 0)), 0,
                        stream, a);
     return hipGetLastError();
 }
@@ -706,8 +721,8 @@ template <int ENC>
 hipError_t launch_g3_variant(const GemmArgs &a, const LinearPlan &plan, hipStream_t stream)
 {
     switch (plan.variant) {
-    case GEMM_G3_256x256: return launch_g3<ENC, 256, 256, 2, 4, 3, 2>(a, plan, stream);
-    case GEMM_G3_256x128: return launch_g3<ENC, 256, 128, 4, 2, 3, 3>(a, plan, stream);
+    case GEMM_G3_256x256: return launch_g3<ENC, 256, 256, 2, 4, 3, 2, false>(a, plan, stream);
+    case GEMM_G3_256x128: return launch_g3<ENC, 256, 128, 4, 2, 3, 3, true>(a, plan, stream);
     default: return hipErrorInvalidValue;
     }
 }
