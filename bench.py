@@ -18,7 +18,8 @@ Also printed on the same JSON line: the roofline of the dominant call
 (HIP events around back-to-back launches of that call on its stream), the
 CPU oracle timed on a bounded sample on the host cores, a per-call
 breakdown, and secondary figures (prefill TFLOPS on FP8/FP16 matrix cores;
-each (batch size, mode) pass replayed as its own graph; the grouped MoE
+each (batch size, mode) pass replayed as its own graph; the same layers as
+plain FP16 weights through torch's GEMM, for context; the grouped MoE
 linear; residual restore from a pinned host backup, alone and under
 fast-mode decode of the hidden-8192 set; the SUM manager's cost per call).
 """
@@ -231,6 +232,7 @@ def main():
     del graphs, g_dom, copies
     torch.cuda.synchronize()
     if not args.no_secondary:
+        secondary["library_fp16"] = library_fp16_secondary(torch, workloads, layers, ms, stream)
         secondary["moe_grouped"] = moe_secondary(torch, dps, workloads, stream, enc)
         secondary["restore"] = restore_secondary(torch, dps, workloads, stream, enc)
         secondary["sum_manager"] = sum_secondary(dps)
@@ -457,6 +459,88 @@ def graph_pair_secondary(torch, dps, run_call, layers, ms, stream, ms_per_step):
     del pairs
     return {"pass_us": per_pass, "sum_of_passes_ms": round(total_us / 1e3, 4),
             "single_graph_step_ms": round(ms_per_step, 4)}
+
+
+def library_fp16_secondary(torch, workloads, layers, ms, stream):
+    """Context, not a target: the same layers as plain FP16 weights through
+    torch's GEMM (the ROCm BLAS libraries), the dense FP16 model the paper
+    measures full mode against.  Decode passes (4 layers at one M, weight
+    copies rotated, each pass a graph) and the prefill set at M = 2048.  Full
+    mode reads the same 2 bytes per weight, so its pass times show the cost of
+    the nesting itself."""
+    import torch.nn.functional as F
+
+    dev = torch.device("cuda:0")
+    with torch.cuda.stream(stream):
+        ws = [[workloads.weight_fp16(n, k, seed=1000 * c + li, device=dev)
+               for li, (_, n, k) in enumerate(layers)] for c in range(COPIES)]
+        xs = {m: {k: workloads.activations_fp16(m, k, seed=m * 7 + k, device=dev)
+                  for k in sorted({k for _, _, k in layers})} for m in ms}
+        ys = {m: {n: torch.empty((m, n), dtype=torch.float16, device=dev)
+                  for n in sorted({n for _, n, _ in layers})} for m in ms}
+
+        def one_pass(c, m):
+            for li, (_, n, k) in enumerate(layers):
+                torch.matmul(xs[m][k], ws[c][li].t(), out=ys[m][n])
+
+        for c in range(COPIES):
+            for m in ms:
+                one_pass(c, m)
+    stream.synchronize()
+    graphs = {}
+    for c in range(COPIES):
+        for m in ms:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=stream):
+                one_pass(c, m)
+            graphs[c, m] = g
+    torch.cuda.synchronize()
+    reps = 8
+    per_pass = {}
+    with torch.cuda.stream(stream):
+        for m in ms:
+            evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                   for _ in range(reps)]
+            for r in range(reps):
+                evs[r][0].record(stream)
+                graphs[r % COPIES, m].replay()
+                evs[r][1].record(stream)
+            stream.synchronize()
+            ts = sorted(a.elapsed_time(b) for a, b in evs)
+            per_pass["M%d" % m] = round(ts[len(ts) // 2] * 1e3, 2)
+    del graphs, xs, ys
+    torch.cuda.synchronize()
+
+    m = 2048
+    with torch.cuda.stream(stream):
+        xp = {k: workloads.activations_fp16(m, k, seed=k + 5, outlier_frac=0.01,
+                                            outlier_scale=20.0, device=dev)
+              for k in sorted({k for _, _, k in layers})}
+        yp = {n: torch.empty((m, n), dtype=torch.float16, device=dev)
+              for n in sorted({n for _, n, _ in layers})}
+
+        def prefill():
+            for li, (_, n, k) in enumerate(layers):
+                torch.matmul(xp[k], ws[0][li].t(), out=yp[n])
+
+        prefill()
+        stream.synchronize()
+        reps = 5
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            prefill()
+        e1.record(stream)
+    stream.synchronize()
+    t = e0.elapsed_time(e1) * 1e-3 / reps
+    flops = sum(2.0 * m * n * k for _, n, k in layers)
+    del ws, xp, yp
+    torch.cuda.empty_cache()
+    return {"what": "plain FP16 weights through torch.matmul (ROCm BLAS), same layers",
+            "decode_pass_us": per_pass,
+            "decode_sum_of_passes_ms": round(sum(per_pass.values()) / 1e3, 4),
+            "prefill_M2048": {"ms": round(t * 1e3, 3), "TFLOPs": round(flops / t / 1e12, 1)}}
 
 
 def restore_secondary(torch, dps, workloads, stream, enc):
