@@ -45,7 +45,7 @@ typedef enum {
     DPS_OK = 0,
     DPS_ERR_INVALID_ARG = 1, /* null/negative/inconsistent argument         */
     DPS_ERR_ALIGNMENT = 2,   /* a tensor pointer is not 16-byte aligned      */
-    DPS_ERR_UNSUPPORTED = 3, /* valid request this build does not implement  */
+    DPS_ERR_UNSUPPORTED = 3, /* valid request the library does not implement */
     DPS_ERR_WORKSPACE = 4,   /* workspace missing or smaller than required   */
     DPS_ERR_HIP = 5,         /* the HIP runtime reported an error on launch  */
     DPS_ERR_NO_SPACE = 6     /* SUM manager: not enough room for the request */

@@ -10,7 +10,7 @@ import torch
 import oracle
 from paper_2609_34380_amd import dps, workloads
 
-# spec acceptance: relative Frobenius error and per-element max abs
+# acceptance bounds for linear outputs: relative Frobenius error and per-element max abs
 REL_FRO = 1e-3
 MAX_ABS = 2e-2
 
