@@ -1,0 +1,128 @@
+"""Seeded random sweep: shapes drawn across every kernel the planner picks
+(row GEMV, the 16-row-group kernel, the wide-row GEMM at every token tile,
+split and unsplit K, the grouped MoE path, FP8 activations), random chunk
+sizes from 256 B to 2 MiB, identity and scattered slot tables, both nested
+encodings.  Every case checks the planes bit-exact and each output against
+the fp64 oracle within the acceptance bounds.
+
+Weight scales stay small enough (std <= 0.06 against N(0, 1) activations)
+that |y| stays below ~64, where half an FP16 ulp of the output is below the
+2e-2 max-abs bound; the bound is a statement about outputs of that size.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_helpers import DEV, Nested, assert_close, u16
+from paper_2609_34380_amd import dps, workloads
+
+pytestmark = pytest.mark.gpu
+
+FAST, FULL = dps.MODE_FAST, dps.MODE_FULL
+KINDS = ("gemv", "rows", "gemm_small", "gemm", "grouped", "fp8")
+N_CASES = 36
+MAX_MACS = 2e8  # per output, so the fp64 oracle stays within about a second
+
+
+def _draw(i):
+    rng = np.random.default_rng(9100 + i)
+    kind = KINDS[i % len(KINDS)]
+    k = 16 * int(rng.integers(1, 6000 // 16))
+    n = int(rng.integers(1, 4300))
+    counts = None
+    if kind == "gemv":
+        m = int(rng.integers(1, 5))
+    elif kind == "rows":
+        m = int(rng.integers(1, 17))
+    elif kind == "gemm_small":
+        m = int(rng.integers(17, 130))
+    elif kind == "gemm":
+        m = int(rng.integers(130, 600))
+    elif kind == "grouped":
+        e = int(rng.integers(1, 7))
+        counts = [int(c) if rng.random() > 0.2 else 0 for c in rng.integers(1, 120, e)]
+        m = max(1, sum(counts))
+    else:
+        m = int(rng.integers(1, 600))
+    experts = len(counts) if counts is not None else 1
+    n = max(1, min(n, int(MAX_MACS // (m * k * experts))))
+    log2c = int(rng.integers(8, 22))
+    scattered = bool(rng.integers(0, 2))
+    std = float(rng.choice([0.005, 0.02, 0.06]))
+    want_e4m3 = bool(rng.integers(0, 2))
+    outliers = kind == "fp8" and std <= 0.02
+    return dict(kind=kind, m=m, n=n, k=k, counts=counts, log2c=log2c, scattered=scattered,
+                std=std, want_e4m3=want_e4m3, outliers=outliers, seed=9100 + i)
+
+
+CASES = [_draw(i) for i in range(N_CASES)]
+
+
+def _id(c):
+    return "%s_m%d_n%d_k%d_c%d%s_s%g%s" % (c["kind"], c["m"], c["n"], c["k"], c["log2c"],
+                                          "_scat" if c["scattered"] else "", c["std"],
+                                          "_e4m3" if c["want_e4m3"] else "")
+
+
+def _omode(mode):
+    return oracle.FAST if mode == FAST else oracle.FULL
+
+
+@pytest.mark.parametrize("case", CASES, ids=[_id(c) for c in CASES])
+def test_sweep_case(case):
+    kind, m, n, k, seed = case["kind"], case["m"], case["n"], case["k"], case["seed"]
+    counts = case["counts"]
+    experts = len(counts) if counts is not None else None
+    w = workloads.weight_fp16(n, k, seed=seed, std=case["std"], experts=experts)
+    x = workloads.activations_fp16(m, k, seed=seed + 1,
+                                   outlier_frac=0.01 if case["outliers"] else 0.0)
+    enc = dps.ENC_E5M2
+    if case["want_e4m3"] and oracle.select_enc(u16(w)) == oracle.E4M3:
+        enc = dps.ENC_E4M3
+    oenc = oracle.E4M3 if enc == dps.ENC_E4M3 else oracle.E5M2
+    numel = w.numel()
+    n_chunks = -(-numel // (1 << case["log2c"]))
+    if case["scattered"]:
+        nst = Nested(w, case["log2c"], n_slots=2 * n_chunks + 3, slot_seed=seed + 2,
+                     filler_seed=seed + 3, enc=enc)
+    else:
+        nst = Nested(w, case["log2c"], enc=enc)
+    nst.check_planes()
+    xd = x.to(DEV)
+    xh = u16(x)
+
+    if kind == "fp8":
+        y = dps.linear(xd, nst.nw, FAST, act="fp8")
+        torch.cuda.synchronize()
+        xq, s = oracle.act_quant(xh)
+        assert_close(y, oracle.linear_fp8(xq, s, nst.hi_ref, enc=oenc), "fp8")
+        return
+
+    for mode in (FAST, FULL):
+        res_ref = nst.res_ref if mode == FULL else None
+        if kind == "grouped":
+            offsets = np.zeros(len(counts) + 1, dtype=np.int64)
+            offsets[1:] = np.cumsum(counts)
+            if offsets[-1] != m:          # every expert empty: one row for the last
+                offsets[-1] = m
+            off_dev = torch.from_numpy(offsets.astype(np.int32)).to(DEV)
+            y = dps.linear_grouped(xd, off_dev, nst.nw, mode)
+            torch.cuda.synchronize()
+            ref = oracle.linear_grouped(_omode(mode), xh, offsets, nst.hi_ref, res_ref, enc=oenc)
+        else:
+            y = dps.linear(xd, nst.nw, mode)
+            torch.cuda.synchronize()
+            ref = oracle.linear(_omode(mode), xh, nst.hi_ref, res_ref, enc=oenc)
+        assert_close(y, ref, "mode=%d enc=%d" % (mode, enc))
+
+
+def test_sweep_reaches_every_kernel_kind():
+    """The drawn cases cover every kernel family, both encodings' requests,
+    chunks below and above 1 KiB and both table layouts (host-side check of
+    the draw itself)."""
+    assert {c["kind"] for c in CASES} == set(KINDS)
+    assert {c["want_e4m3"] for c in CASES} == {False, True}
+    assert min(c["log2c"] for c in CASES) < 10 < max(c["log2c"] for c in CASES)
+    assert {c["scattered"] for c in CASES} == {False, True}
+    assert any(c["counts"] is not None and 0 in c["counts"] for c in CASES)
