@@ -51,8 +51,9 @@ def parse():
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--roofline-reps", type=int, default=40)
     ap.add_argument("--probe-call", default=None,
-                    help="LAYER:M:MODE -- run only that call (for rocprofv3) and a copy "
-                         "kernel of known size, then exit")
+                    help="LAYER:M:MODE[:fp8] -- run only that call (for rocprofv3) and a "
+                         "copy kernel of known size, then exit; ':fp8' = fast mode on FP8 "
+                         "activations (prefill)")
     ap.add_argument("--probe-reps", type=int, default=20)
     ap.add_argument("--enc", choices=("e5m2", "e4m3"), default="e5m2",
                     help="nested encoding of every layer")
@@ -298,9 +299,13 @@ def probe(args, torch, dps, workloads, layers, dev, stream, enc):
     """One call of the decode set, launched back to back on rotating weight
     copies, then a device-to-device copy of 256 MiB (a kernel of known HBM
     traffic, to calibrate rocprofv3's FETCH_SIZE / WRITE_SIZE)."""
-    name, m, mode_name = args.probe_call.split(":")
+    parts = args.probe_call.split(":")
+    name, m, mode_name = parts[:3]
+    act = parts[3] if len(parts) > 3 else "fp16"
     m = int(m)
     mode = dps.MODE_FAST if mode_name == "fast" else dps.MODE_FULL
+    if act not in ("fp16", "fp8") or (act == "fp8" and mode != dps.MODE_FAST):
+        raise SystemExit("--probe-call: FP8 activations need fast mode")
     li = [l[0] for l in layers].index(name)
     _, n, k = layers[li]
     with torch.cuda.stream(stream):
@@ -309,18 +314,19 @@ def probe(args, torch, dps, workloads, layers, dev, stream, enc):
             w = workloads.weight_fp16(n, k, seed=1000 * c + li, device=dev)
             nws.append(dps.split(w, dps.make_residual(n * k, LOG2_CHUNK, dev), enc=enc))
             del w
-        x = workloads.activations_fp16(m, k, seed=m * 7 + k, device=dev)
+        x = workloads.activations_fp16(m, k, seed=m * 7 + k, device=dev,
+                                       outlier_frac=0.01 if act == "fp8" else 0.0)
         y = torch.empty((m, n), dtype=torch.float16, device=dev)
-        need = dps.workspace_bytes(mode, 0, m, n, k)
+        need = dps.workspace_bytes(mode, 1 if act == "fp8" else 0, m, n, k)
         ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
         for r in range(COPIES):
-            dps.linear(x, nws[r], mode, out=y, workspace=ws)
+            dps.linear(x, nws[r], mode, act=act, out=y, workspace=ws)
         stream.synchronize()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         for r in range(args.probe_reps):
-            dps.linear(x, nws[r % COPIES], mode, out=y, workspace=ws)
+            dps.linear(x, nws[r % COPIES], mode, act=act, out=y, workspace=ws)
         e1.record(stream)
         stream.synchronize()
         src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
@@ -331,6 +337,7 @@ def probe(args, torch, dps, workloads, layers, dev, stream, enc):
     t = e0.elapsed_time(e1) * 1e-3 / args.probe_reps
     print(json.dumps({"probe_call": args.probe_call, "us_per_call": round(t * 1e6, 2),
                       "kernels_per_call": 1 if need == 0 else 2,
+                      "flops_per_call": 2.0 * m * n * k,
                       "copy_bytes_each_way": 256 << 20}), flush=True)
 
 
