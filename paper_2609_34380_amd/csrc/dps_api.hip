@@ -225,12 +225,16 @@ LinearPlan plan_linear(int mode, uint32_t flags, int64_t rows, int64_t n, int64_
         // count rounds down); each range keeps >= 1024 elements.
         // four dedicated DMA waves pay off from 64-token tiles on (MI355X:
         // 3-10% at 128-2048 tokens; at 32 tokens the plain kernel is 2% ahead)
-        // Layers of at most 2^24 weights keep the 32-token tile at every
-        // token count: more tiles and shorter split-K chains win there
-        // (MI355X, hidden-4096 O layer, both modes: 34.5 against 40.3 us at
-        // 128 tokens, 42.4 against 47.2 at 256; the QKV, gate+up and down
-        // layers lose 1-30% with it).
-        p.variant = (rows_per_expert <= 32 || n * k <= (int64_t(1) << 24))
+        // Layers of at most 2^24 weights keep the 32-token tile up to 256
+        // tokens: more tiles and shorter split-K chains win there (MI355X,
+        // hidden-4096 O layer, both modes: 34.5 against 40.3 us at 128
+        // tokens, even at 256; the QKV, gate+up and down layers lose 1-30%
+        // with it).  From 512 tokens on the wider tiles read each weight
+        // tile for 4x as many tokens and win (O layer, full / fast mode:
+        // 33 / 28 against 51 / 39 us at 512 tokens, 94 / 77 against 185 /
+        // 150 us at 2048).
+        p.variant = (rows_per_expert <= 32 ||
+                     (n * k <= (int64_t(1) << 24) && rows_per_expert <= 256))
                         ? GEMM_G4_128x32
                         : (rows_per_expert <= 64 ? GEMM_G4S_128x64 : GEMM_G4S_128x128);
         const int64_t waves_per_block = 8;
