@@ -143,7 +143,6 @@ LinearPlan plan_linear(int mode, uint32_t flags, int64_t rows, int64_t n, int64_
 {
     LinearPlan p;
     memset(&p, 0, sizeof(p));
-    const int64_t target = 2 * (int64_t)cu_count;  // blocks we aim to have in flight
     const int64_t rows_per_expert = grouped ? cdiv(rows, experts) : rows;
     if (flags & DPS_ACT_FP8_ROWSCALE) {
         p.kind = KIND_GEMM_FP8;
@@ -152,9 +151,14 @@ LinearPlan plan_linear(int mode, uint32_t flags, int64_t rows, int64_t n, int64_
         // 256 x 128; QKV, 192 blocks of 256 x 256, 114 against 132 us)
         p.variant = cdiv(n, 256) * cdiv(rows, 256) >= 2 * (int64_t)cu_count ? GEMM_G3_256x256
                                                                            : GEMM_G3_256x128;
+        // K is split only while the tiles alone leave CUs idle: the fp32
+        // partials cost more than a half-filled last wave of blocks (MI355X,
+        // split to two blocks per CU against one: gate+up at 512 tokens 129
+        // against 95 us, O at 2048 tokens 71 against 51, down 167 against
+        // 148; QKV at 512 tokens 48 against 50)
         const int64_t tiles =
             cdiv(n, gemm_rows_per_block(p.variant)) * cdiv(rows, gemm_tokens_per_block(p.variant));
-        int64_t s = cdiv(target, tiles);
+        int64_t s = cdiv((int64_t)cu_count, tiles);
         const int64_t smax = k / 1024 > 1 ? k / 1024 : 1;
         s = s < 1 ? 1 : (s > smax ? smax : s);
         p.ksplit = round_up(cdiv(k, s), 128);
