@@ -146,11 +146,18 @@ LinearPlan plan_linear(int mode, uint32_t flags, int64_t rows, int64_t n, int64_
     const int64_t rows_per_expert = grouped ? cdiv(rows, experts) : rows;
     if (flags & DPS_ACT_FP8_ROWSCALE) {
         p.kind = KIND_GEMM_FP8;
-        // 256 x 256 tiles once their grid holds at least two blocks per CU,
-        // else 256 x 128 (MI355X, 2048 tokens: gate+up 280 against 310 us on
-        // 256 x 128; QKV, 192 blocks of 256 x 256, 114 against 132 us)
-        p.variant = cdiv(n, 256) * cdiv(rows, 256) >= 2 * (int64_t)cu_count ? GEMM_G3_256x256
-                                                                           : GEMM_G3_256x128;
+        // 256 x 256 tiles once their grid gives every CU a block and its last
+        // round of blocks is at least half full, else 256 x 128.  MI355X,
+        // hidden-4096 layers: gate+up at 1024 tokens (448 big tiles) 136
+        // against 165 us, down and O at 4096 tokens (256) 245 / 78 against
+        // 297 / 95; QKV at 2048 tokens (192) 94 against 110 and at 3072
+        // (288, a last round of 32) 129 against 139 on the smaller tile.
+        {
+            const int64_t cus = cu_count;
+            const int64_t big = cdiv(n, 256) * cdiv(rows, 256);
+            const bool fills = big >= cus && (big % cus == 0 || 2 * (big % cus) >= cus);
+            p.variant = fills ? GEMM_G3_256x256 : GEMM_G3_256x128;
+        }
         // K is split only while the tiles alone leave CUs idle: the fp32
         // partials cost more than a half-filled last wave of blocks (MI355X,
         // split to two blocks per CU against one: gate+up at 512 tokens 129
