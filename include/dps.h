@@ -108,7 +108,7 @@ typedef struct {
  * layer).  Element (e, r, c) is logical element (e * n + r) * k + c of both
  * the upper-byte plane `hi` and the residual stream.
  *   hi   device uint8[experts][n][k], 16-byte aligned.
- *   k    multiple of 16, > 0.   n > 0.   experts >= 1.
+ *   k    multiple of 16, 16..2^30.   n in 1..2^31-1.   experts in 1..65535.
  *   enc  DPS_ENC_E5M2 or DPS_ENC_E4M3: the encoding hi and the residual were
  *        split with. */
 typedef struct {
@@ -192,7 +192,7 @@ dps_status dps_backup(const dps_residual *res, const int32_t *slots_host, int64_
  *   x      device FP16 [m][k], 16-byte aligned, finite values.
  *   xq     device uint8 [m][k] (E4M3 codes), 16-byte aligned.
  *   scale  device float [m].
- * k must be a multiple of 16. */
+ * k must be a multiple of 16, at most 2^30. */
 dps_status dps_quant_rows_e4m3(const uint16_t *x, int64_t m, int64_t k,
                                uint8_t *xq, float *scale, void *stream);
 

@@ -122,8 +122,10 @@ dps_status check_weight(const dps_weight *w, int mode)
             "unknown nested encoding");
     REQUIRE(w->experts >= 1 && w->experts <= 65535, DPS_ERR_INVALID_ARG,
             "experts must be in 1..65535");
-    REQUIRE(w->n > 0, DPS_ERR_INVALID_ARG, "n must be positive");
+    REQUIRE(w->n > 0 && w->n <= 0x7fffffff, DPS_ERR_INVALID_ARG, "n must be in 1..2^31-1");
     REQUIRE(w->k > 0 && w->k % 16 == 0, DPS_ERR_INVALID_ARG, "k must be a positive multiple of 16");
+    // the kernels keep a block's K range in 32-bit lane registers
+    REQUIRE(w->k <= (int64_t(1) << 30), DPS_ERR_INVALID_ARG, "k must be at most 2^30");
     REQUIRE(w->hi != nullptr, DPS_ERR_INVALID_ARG, "upper-byte plane is NULL");
     REQUIRE(aligned(w->hi, 16), DPS_ERR_ALIGNMENT, "upper-byte plane is not 16-byte aligned");
     if (mode == DPS_MODE_FULL) {
@@ -375,7 +377,8 @@ DPS_EXPORT dps_status dps_quant_rows_e4m3(const uint16_t *x, int64_t m, int64_t 
 {
     g_err[0] = 0;
     REQUIRE(m >= 0 && m <= 0x7fffffff, DPS_ERR_INVALID_ARG, "m must be in 0..2^31-1");
-    REQUIRE(k > 0 && k % 16 == 0, DPS_ERR_INVALID_ARG, "k must be a positive multiple of 16");
+    REQUIRE(k > 0 && k % 16 == 0 && k <= (int64_t(1) << 30), DPS_ERR_INVALID_ARG,
+            "k must be a positive multiple of 16, at most 2^30");
     if (m == 0)
         return DPS_OK;
     REQUIRE(x != nullptr && xq != nullptr && scale != nullptr, DPS_ERR_INVALID_ARG,

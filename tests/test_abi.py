@@ -64,6 +64,8 @@ def _linear(lib, mode=0, flags=0, x=0x4000, m=4, w=None, y=0x5000, ws=None, ws_b
     (dict(flags=9), 1),
     (dict(mode=0, flags=1), 1),                      # FP8 activations need fast mode
     (dict(w=_weight(k=40)), 1),                      # k % 16 != 0
+    (dict(w=_weight(k=(1 << 30) + 16)), 1),          # k above 2^30
+    (dict(w=_weight(n=1 << 31)), 1),                 # n above 2^31-1
     (dict(w=_weight(n=0)), 1),
     (dict(w=_weight(enc=2)), 1),                     # unknown nested encoding
     (dict(w=_weight(experts=2)), 1),                 # dense call with stacked experts
@@ -125,6 +127,7 @@ def test_split_merge_reject_bad_arguments(lib):
     assert lib.dps_select_enc(0, 64, 0x2000, None) == 1
     assert lib.dps_quant_rows_e4m3(0x1000, 4, 24, 0x2000, 0x3000, None) == 1
     assert lib.dps_quant_rows_e4m3(0x1000, 0, 32, 0x2000, 0x3000, None) == 0
+    assert lib.dps_quant_rows_e4m3(0x1000, 4, (1 << 30) + 16, 0x2000, 0x3000, None) == 1
 
 
 def test_restore_backup_reject_bad_arguments(lib):
