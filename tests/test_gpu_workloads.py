@@ -84,6 +84,31 @@ def test_prefill_h4096(h4096_set, m, mode):
         assert_close(got, ref, "%s m=%d" % (name, m))
 
 
+@pytest.mark.parametrize("m", [512, 1024, 3072, 4096])
+@pytest.mark.parametrize("mode", [FAST, FULL], ids=["fast_fp8", "full_f16"])
+def test_prefill_h4096_tile_rule_sizes(h4096_set, m, mode):
+    """Token counts where the planner's tile and split rules change branch:
+    FP8 256 x 256 tiles with exactly one block per CU (down and O at 4096
+    tokens) and 256 x 128 tiles with a nearly empty last round of big tiles
+    (QKV at 3072), FP8 calls without a K split (512, 1024), and the O layer
+    on 128-token FP16 tiles from 512 tokens on."""
+    for name, n, k, nst in h4096_set:
+        x = workloads.activations_fp16(m, k, seed=730 + m + k, outlier_frac=0.01,
+                                       outlier_scale=20.0)
+        act = "fp8" if mode == FAST else "fp16"
+        y = dps.linear(x.to(DEV), nst.nw, mode, act=act)
+        rows = _sample_rows(m, seed=m * 5 + n)
+        got = y[torch.from_numpy(rows).to(DEV)].cpu()
+        xr = x[torch.from_numpy(rows)]
+        if mode == FAST:
+            xq, s = oracle.act_quant(u16(xr))
+            ref = oracle.linear_fp8(xq, s, nst.hi_ref)
+        else:
+            ref = oracle.linear_rows(oracle.FULL, u16(xr), np.arange(len(rows)), nst.hi_ref,
+                                     nst.res_ref)
+        assert_close(got, ref, "%s m=%d" % (name, m))
+
+
 def test_prefill_fp8_quantization_full_size():
     """The E4M3 row quantization at the prefill size, bit-exact on every row."""
     x = workloads.activations_fp16(2048, 14336, seed=710, outlier_frac=0.01, outlier_scale=20.0)
