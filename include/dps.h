@@ -228,6 +228,8 @@ dps_status dps_linear(int mode, uint32_t flags, const uint16_t *x, int64_t m,
  *             does not synchronize; rows outside [0, rows) are never touched
  *             even if the array breaks this contract.
  *   y         device FP16 [rows][w->n].
+ * With w->experts == 1 the call is the dense one (dps_linear on all rows,
+ * same kernels and results); offsets is then checked but not read.
  * Other arguments as dps_linear.  DPS_ACT_FP8_ROWSCALE is not supported
  * here (DPS_ERR_UNSUPPORTED). */
 dps_status dps_linear_grouped(int mode, uint32_t flags, const uint16_t *x_sorted,

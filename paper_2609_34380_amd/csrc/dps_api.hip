@@ -501,6 +501,11 @@ DPS_EXPORT dps_status dps_linear_grouped(int mode, uint32_t flags, const uint16_
     REQUIRE(x_sorted != nullptr && y != nullptr, DPS_ERR_INVALID_ARG, "x_sorted or y is NULL");
     REQUIRE(aligned(x_sorted, 16) && aligned(y, 16), DPS_ERR_ALIGNMENT,
             "x_sorted or y is not 16-byte aligned");
+    // One expert owns every row (offsets = {0, rows}): the dense call, with
+    // the dense plan that dps_workspace_bytes reports for experts == 1
+    if (w->experts == 1)
+        return run_linear(mode, flags, x_sorted, nullptr, rows, w, y, ws, ws_bytes,
+                          (hipStream_t)stream, false);
     return run_linear(mode, flags, x_sorted, offsets, rows, w, y, ws, ws_bytes,
                       (hipStream_t)stream, true);
 }

@@ -339,6 +339,25 @@ def test_grouped_matches_oracle(counts, n, k, log2c, mode):
     assert_close(y, ref)
 
 
+@pytest.mark.parametrize("m", [1, 2, 5, 16, 40])
+def test_grouped_single_expert_workspace_and_values(m):
+    """One expert through dps_linear_grouped, with the workspace sized by
+    dps_workspace_bytes (the grouped plan can split K where the dense plan
+    of the same call does not), against the oracle."""
+    n, k = 3459, 1504
+    w = workloads.weight_fp16(n, k, seed=75)
+    x = workloads.activations_fp16(m, k, seed=76)
+    nst = Nested(w, 16)
+    nw1 = dps.NestedWeight(nst.nw.hi.view(1, n, k), nst.res)
+    off = torch.tensor([0, m], dtype=torch.int32, device=DEV)
+    for mode in (FAST, FULL):
+        y = dps.linear_grouped(x.to(DEV), off, nw1, mode)
+        torch.cuda.synchronize()
+        ref = oracle.linear(_omode(mode), u16(x), nst.hi_ref,
+                            nst.res_ref if mode == FULL else None)
+        assert_close(y, ref, "m=%d mode=%d" % (m, mode))
+
+
 def test_grouped_single_expert_equals_dense():
     n, k, m = 300, 512, 90
     w = workloads.weight_fp16(n, k, seed=71)
