@@ -2,8 +2,10 @@
 (row GEMV, the 16-row-group kernel, the wide-row GEMM at every token tile,
 split and unsplit K, the grouped MoE path, FP8 activations), random chunk
 sizes from 256 B to 2 MiB, identity and scattered slot tables, both nested
-encodings.  Every case checks the planes bit-exact and each output against
-the fp64 oracle within the acceptance bounds.
+encodings; and a fixed set of edge cases (token counts on both sides of
+every planner threshold, tiny and odd shapes, chunks down to 16 bytes,
+skewed expert groups).  Every case checks the planes bit-exact and each
+output against the fp64 oracle within the acceptance bounds.
 
 Weight scales stay small enough (std <= 0.06 against N(0, 1) activations)
 that |y| stays below ~64, where half an FP16 ulp of the output is below the
@@ -59,6 +61,34 @@ def _draw(i):
 CASES = [_draw(i) for i in range(N_CASES)]
 
 
+def _edges():
+    """Token counts on both sides of every planner threshold (1-2 and 3-4
+    token row GEMV, 16-row groups up to 16, the 32- / 64- / 128-token tiles,
+    the small-layer rule at 256) over tiny, odd and wide shapes, chunks of
+    16 B to 2 KiB, and grouped calls with empty, single-row and over-full
+    experts."""
+    ms = [1, 2, 3, 4, 5, 15, 16, 17, 31, 32, 33, 63, 64, 65, 127, 128, 129, 255, 256, 257, 300]
+    shapes = [(1, 16), (7, 32), (17, 48), (130, 1040), (4100, 16), (256, 4112)]
+    chunks = [4, 5, 9, 10, 11]
+    out = []
+    i = 0
+    for m in ms:
+        for n, k in shapes:
+            i += 1
+            out.append(dict(kind="fp8" if i % 7 == 0 else "gemm", m=m, n=n, k=k, counts=None,
+                            log2c=chunks[i % len(chunks)], scattered=bool(i % 2), std=0.02,
+                            want_e4m3=i % 3 == 0, outliers=False, seed=20000 + i))
+    for j, counts in enumerate([[0, 0, 1], [1], [200, 0, 3], [129, 129], [1] * 8, [300],
+                                [0, 64, 0, 65]]):
+        out.append(dict(kind="grouped", m=sum(counts), n=137, k=528, counts=counts,
+                        log2c=[4, 9, 12][j % 3], scattered=True, std=0.02,
+                        want_e4m3=j % 2 == 1, outliers=False, seed=21000 + j))
+    return out
+
+
+EDGE_CASES = _edges()
+
+
 def _id(c):
     return "%s_m%d_n%d_k%d_c%d%s_s%g%s" % (c["kind"], c["m"], c["n"], c["k"], c["log2c"],
                                           "_scat" if c["scattered"] else "", c["std"],
@@ -71,6 +101,16 @@ def _omode(mode):
 
 @pytest.mark.parametrize("case", CASES, ids=[_id(c) for c in CASES])
 def test_sweep_case(case):
+    _check_case(case)
+
+
+@pytest.mark.parametrize("case", EDGE_CASES, ids=["edge%d_%s" % (i, _id(c))
+                                                  for i, c in enumerate(EDGE_CASES)])
+def test_sweep_edge_case(case):
+    _check_case(case)
+
+
+def _check_case(case):
     kind, m, n, k, seed = case["kind"], case["m"], case["n"], case["k"], case["seed"]
     counts = case["counts"]
     experts = len(counts) if counts is not None else None
