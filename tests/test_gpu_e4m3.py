@@ -297,3 +297,30 @@ def test_e4m3_grouped_matches_oracle(counts, n, k, log2c, mode):
     ref = oracle.linear_grouped(_omode(mode), u16(x), offsets, nst.hi_ref,
                                 nst.res_ref if mode == FULL else None, enc=oracle.E4M3)
     assert_close(y, ref)
+
+
+def test_e4m3_weights_near_the_bound_and_subnormal():
+    """A layer whose weights reach up to the E4M3 bound (1.75-1.87, truncated
+    to +-1.75 in fast mode) and down into FP16 subnormals: chosen as E4M3 on
+    both sides, both modes against the oracle, merge after split exact."""
+    n, k, m = 300, 1024, 40
+    rng = np.random.default_rng(7)
+    v = rng.uniform(-1.87, 1.87, (n, k)).astype(np.float32)
+    v[0] = rng.uniform(-2.0 ** -14, 2.0 ** -14, k)
+    v[1] = 1.75 + rng.uniform(0, 0.12, k)
+    w = torch.from_numpy(v.astype(np.float16))
+    assert oracle.select_enc(u16(w)) == oracle.E4M3
+    assert int(dps.select_enc(w.to(DEV)).cpu()[0]) == dps.ENC_E4M3
+    x = workloads.activations_fp16(m, k, seed=8) * 0.05
+    nst = Nested(w, 10, n_slots=2 * (n * k // 1024) + 3, slot_seed=9, filler_seed=10,
+                 enc=dps.ENC_E4M3)
+    nst.check_planes()
+    for mode, om in ((dps.MODE_FAST, oracle.FAST), (dps.MODE_FULL, oracle.FULL)):
+        y = dps.linear(x.to(DEV), nst.nw, mode)
+        torch.cuda.synchronize()
+        ref = oracle.linear(om, u16(x), nst.hi_ref,
+                            nst.res_ref if mode == dps.MODE_FULL else None, enc=oracle.E4M3)
+        assert_close(y, ref, "mode %d" % mode)
+    back = dps.merge(nst.nw)
+    torch.cuda.synchronize()
+    assert np.array_equal(u16(back.cpu()), u16(w))

@@ -308,6 +308,52 @@ def test_linear_fp8_matches_oracle(m, n, k):
     assert_close(y, ref)
 
 
+def test_linear_fp8_activation_extremes():
+    """FP8 activations with an all-zero row (scale 1), rows of tiny, 448-sized
+    and near-FP16-maximum values, a row with one nonzero element and a row
+    spanning many powers of two: the quantization bit-exact, each row's
+    output within the bounds against the oracle, and outputs past the FP16
+    range rounded to +-inf exactly where the exact value reaches 65520."""
+    m, n, k = 64, 520, 1040
+    w = workloads.weight_fp16(n, k, seed=5)
+    rng = np.random.default_rng(6)
+    x = rng.normal(0, 1, (m, k)).astype(np.float32)
+    x[0] = 0
+    x[1] = 1e-6 * x[1]
+    x[2] = 448.0
+    x[3] = np.where(x[3] >= 0, 60000.0, -60000.0)
+    x[4, :] = 0
+    x[4, 7] = 2.0 ** -20
+    x[5] = 448.0 * 2.0 ** np.round(rng.normal(0, 3, k))
+    xt = torch.from_numpy(np.clip(x, -65504, 65504).astype(np.float16))
+    nst = Nested(w, 12)
+    y = dps.linear(xt.to(DEV), nst.nw, FAST, act="fp8")
+    xq_d, s_d = dps.quant_rows_e4m3(xt.to(DEV))
+    torch.cuda.synchronize()
+    xq, s = oracle.act_quant(u16(xt))
+    assert np.array_equal(xq_d.cpu().numpy(), xq)
+    assert np.array_equal(s_d.cpu().numpy().astype(np.float64), s)
+    ref = oracle.linear_fp8(xq, s, nst.hi_ref)
+    got = y.cpu().double().numpy()
+    over = np.abs(ref) >= 65520.0
+    assert over.any()
+    assert np.array_equal(np.isinf(got), over)
+    assert np.array_equal(np.sign(got[over]), np.sign(ref[over]))
+    assert np.all(got[0] == 0)
+    # Outputs span many binades here, so instead of the fixed bounds (stated
+    # for outputs of moderate size) each one is held to its own error bound:
+    # FP16 rounding of the exact value (half an ulp, or half the subnormal
+    # step) plus fp32 accumulation over k terms, bounded by k * 2^-24 times
+    # the sum of the products' magnitudes (operands decoded by torch).
+    wv = torch.from_numpy(nst.hi_ref).view(torch.float8_e5m2).double().numpy()
+    xv = torch.from_numpy(xq).view(torch.float8_e4m3fn).double().numpy() * s[:, None]
+    sum_abs = np.abs(xv) @ np.abs(wv).T
+    bound = 2.0 ** -11 * np.abs(ref) + 2.0 ** -25 + k * 2.0 ** -24 * sum_abs
+    keep = ~over
+    assert np.all(np.abs(got[keep] - ref[keep]) <= bound[keep])
+    assert_close(torch.from_numpy(got[6:]), ref[6:], "rows of N(0, 1) activations")
+
+
 # -----------------------------------------------------------------------------
 # grouped (MoE)
 # -----------------------------------------------------------------------------
