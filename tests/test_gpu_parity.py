@@ -12,7 +12,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_helpers import DEV, Nested, assert_close, errors, u16
+from gpu_helpers import DEV, Nested, assert_close, errors, make_residual_host, u16
 from paper_2609_34380_amd import dps, workloads
 
 pytestmark = pytest.mark.gpu
@@ -63,6 +63,46 @@ def test_split_scattered_pool(numel, log2c, n_slots):
     back = dps.merge(nst.nw)
     torch.cuda.synchronize()
     assert np.array_equal(back.cpu().view(torch.int16).numpy().view(np.uint16), bits)
+
+
+@pytest.mark.parametrize("i", range(12))
+def test_split_merge_select_random(i):
+    """Seeded random sizes (1 to 3 M words), chunks of 16 B to 4 MiB, identity
+    or scattered tables over KV filler, random bit patterns or weights of
+    small or wide range: the encoding choice, both planes and the merge
+    bit-exact against the oracle (merge after split the identity for E5M2)."""
+    rng = np.random.default_rng(30000 + i)
+    numel = int(rng.integers(1, 3_000_000)) if i % 4 else int(rng.integers(1, 4000))
+    log2c = int(rng.integers(4, 23))
+    scattered = bool(rng.integers(0, 2))
+    kind = i % 3
+    if kind == 0:
+        bits = rng.integers(0, 65536, numel).astype(np.uint16)
+    else:
+        bits = rng.normal(0, 0.02 if kind == 1 else 0.5, numel).astype(np.float16).view(np.uint16)
+    want_e4m3 = bool(rng.integers(0, 2))
+    n_chunks = max(1, -(-numel // (1 << log2c)))
+    pool, slots = make_residual_host(numel, log2c, 2 * n_chunks + 3 if scattered else n_chunks,
+                                     slot_seed=i if scattered else None,
+                                     filler_seed=i + 1 if scattered else None)
+    wd = torch.from_numpy(bits.view(np.float16).copy()).to(DEV)
+    e_ref = oracle.select_enc(bits)
+    assert int(dps.select_enc(wd).cpu()[0]) == e_ref
+    enc = dps.ENC_E4M3 if (want_e4m3 and e_ref == oracle.E4M3) else dps.ENC_E5M2
+    oenc = oracle.E4M3 if enc == dps.ENC_E4M3 else oracle.E5M2
+    res_ref = oracle.Residual(pool.copy(), slots, log2c)
+    hi_ref = oracle.split(bits, res_ref, enc=oenc)
+    res = dps.Residual(torch.from_numpy(pool.copy()).to(DEV), torch.from_numpy(slots).to(DEV),
+                       log2c)
+    nw = dps.split(wd, res, enc=enc)
+    back = dps.merge(nw)
+    torch.cuda.synchronize()
+    assert np.array_equal(nw.hi.cpu().numpy(), hi_ref)
+    assert np.array_equal(res.pool.cpu().numpy(), res_ref.pool)
+    merged = u16(back.cpu())
+    assert np.array_equal(merged, oracle.merge(hi_ref, res_ref, enc=oenc).reshape(-1))
+    if enc == dps.ENC_E5M2:
+        assert np.array_equal(merged, bits)
 
 
 def test_out_of_range_slot_is_never_dereferenced():
