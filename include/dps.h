@@ -219,6 +219,25 @@ dps_status dps_linear(int mode, uint32_t flags, const uint16_t *x, int64_t m,
                       const dps_weight *w, uint16_t *y, void *ws, size_t ws_bytes,
                       void *stream);
 
+/* Upper bound of the scratch dps_linear_static may use: 64 MiB per device.
+ * dps_workspace_bytes() at or below it means the call fits. */
+#define DPS_STATIC_SCRATCH_BYTES (((size_t)64) << 20)
+
+/* dps_linear without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, serving loops, harnesses that
+ * forbid hipMalloc).  Same arguments, kernels and results as dps_linear; the
+ * split-K partials and FP8 activation staging go to a static device array of
+ * DPS_STATIC_SCRATCH_BYTES that every device the library runs on holds until
+ * the process ends.  The first call on a device looks the array's address up
+ * (hipGetSymbolAddress, no allocation); no call allocates or frees anything.
+ * A call whose dps_workspace_bytes() exceeds DPS_STATIC_SCRATCH_BYTES returns
+ * DPS_ERR_WORKSPACE with nothing enqueued.  Every call on one device shares
+ * that device's array: calls that may overlap on one device (different
+ * streams without ordering, several host threads) race on it and give wrong
+ * results; order them on one stream. */
+dps_status dps_linear_static(int mode, uint32_t flags, const uint16_t *x, int64_t m,
+                             const dps_weight *w, uint16_t *y, void *stream);
+
 /* Grouped nested linear for MoE experts (Sec. IV-C, GroupedGEMM paragraph,
  * MoE case): rows [offsets[e], offsets[e+1]) of x_sorted are multiplied by
  * expert e's weights; Y rows follow the same order.

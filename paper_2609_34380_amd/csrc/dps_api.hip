@@ -3,6 +3,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "dps.h"
 #include "dps_internal.h"
 
@@ -508,4 +510,86 @@ DPS_EXPORT dps_status dps_linear_grouped(int mode, uint32_t flags, const uint16_
                           (hipStream_t)stream, false);
     return run_linear(mode, flags, x_sorted, offsets, rows, w, y, ws, ws_bytes,
                       (hipStream_t)stream, true);
+}
+
+// ---- dps_linear_static: dps_linear with library-owned scratch ----------------
+// The split-K partials and the FP8 activation staging of a call live in one
+// file-scope device array instead of a caller workspace.  Each device that
+// loads the library holds its own copy until the process ends; host code
+// reaches it only through the address hipGetSymbolAddress returns for the
+// current device (the array's name is a host-side stand-in, not a device
+// address).  Nothing in it has to start at zero: every byte a kernel reads
+// there was written earlier in the same call.
+static __device__ __align__(256) uint8_t scratch[DPS_STATIC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {nullptr};
+
+// Device address of the current device's scratch array, looked up once per
+// device (with that device current) and kept.
+dps_status static_scratch(void **out)
+{
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return launched(e);
+    REQUIRE(dev >= 0 && dev < kMaxDevices, DPS_ERR_UNSUPPORTED,
+            "device index beyond the static scratch table");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || p == nullptr) {
+            snprintf(g_err, sizeof(g_err), "hipGetSymbolAddress(scratch) failed: %s",
+                     hipGetErrorString(e));
+            return DPS_ERR_HIP;
+        }
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return DPS_OK;
+}
+
+}  // namespace
+
+DPS_EXPORT dps_status dps_linear_static(int mode, uint32_t flags, const uint16_t *x, int64_t m,
+                                        const dps_weight *w, uint16_t *y, void *stream)
+{
+    g_err[0] = 0;
+    void *ws = nullptr;
+    dps_status s = static_scratch(&ws);
+    if (s != DPS_OK)
+        return s;
+    REQUIRE(mode == DPS_MODE_FULL || mode == DPS_MODE_FAST, DPS_ERR_INVALID_ARG, "unknown mode");
+    REQUIRE(flags == DPS_ACT_FP16 || flags == DPS_ACT_FP8_ROWSCALE, DPS_ERR_INVALID_ARG,
+            "unknown flags");
+    REQUIRE(!(flags == DPS_ACT_FP8_ROWSCALE && mode != DPS_MODE_FAST), DPS_ERR_INVALID_ARG,
+            "FP8 activations need fast mode");
+    s = check_weight(w, mode);
+    if (s != DPS_OK)
+        return s;
+    REQUIRE(w->experts == 1, DPS_ERR_INVALID_ARG,
+            "dps_linear_static takes a dense weight (experts == 1)");
+    REQUIRE(m >= 0, DPS_ERR_INVALID_ARG, "m is negative");
+    if (m == 0)
+        return DPS_OK;
+    REQUIRE(x != nullptr && y != nullptr, DPS_ERR_INVALID_ARG, "x or y is NULL");
+    REQUIRE(aligned(x, 16) && aligned(y, 16), DPS_ERR_ALIGNMENT, "x or y is not 16-byte aligned");
+    const dps::LinearPlan plan =
+        dps::plan_linear(mode, flags, m, w->n, w->k, 1,
+                         mode == DPS_MODE_FULL ? w->res.log2_chunk : 30, current_cu_count(),
+                         false);
+    const size_t need = plan.ws_partial + plan.ws_quant;
+    if (need > (size_t)DPS_STATIC_SCRATCH_BYTES) {
+        snprintf(g_err, sizeof(g_err),
+                 "call needs %zu bytes of scratch, above the static scratch of %zu bytes; "
+                 "use dps_linear with a workspace",
+                 need, (size_t)DPS_STATIC_SCRATCH_BYTES);
+        return DPS_ERR_WORKSPACE;
+    }
+    return run_linear(mode, flags, x, nullptr, m, w, y, ws, DPS_STATIC_SCRATCH_BYTES,
+                      (hipStream_t)stream, false);
 }

@@ -27,7 +27,7 @@ ERR_NO_SPACE = 6
 UNIT_FREE, UNIT_BACKED, UNIT_AVAIL, UNIT_FULL, UNIT_RESTORING = 0, 1, 2, 3, 4
 
 EXPORTED = ("dps_select_enc", "dps_split", "dps_merge", "dps_restore", "dps_backup", "dps_quant_rows_e4m3", "dps_workspace_bytes",
-            "dps_linear", "dps_linear_grouped", "dps_status_str", "dps_last_error",
+            "dps_linear", "dps_linear_static", "dps_linear_grouped", "dps_status_str", "dps_last_error",
             "dps_sum_create", "dps_sum_destroy", "dps_sum_alloc", "dps_sum_free",
             "dps_sum_restore_begin", "dps_sum_restore_done", "dps_sum_mode",
             "dps_sum_unit_state", "dps_sum_unit_of", "dps_sum_counts", "dps_sum_slots")
@@ -82,6 +82,8 @@ def load_library(path=LIB_PATH):
     lib.dps_linear.argtypes = [ctypes.c_int, U32, P, I64, ctypes.POINTER(CWeight), P, P,
                                ctypes.c_size_t, P]
     lib.dps_linear.restype = ST
+    lib.dps_linear_static.argtypes = [ctypes.c_int, U32, P, I64, ctypes.POINTER(CWeight), P, P]
+    lib.dps_linear_static.restype = ST
     lib.dps_linear_grouped.argtypes = [ctypes.c_int, U32, P, P, I64, ctypes.POINTER(CWeight),
                                        P, P, ctypes.c_size_t, P]
     lib.dps_linear_grouped.restype = ST
@@ -305,6 +307,25 @@ def linear(x, nw, mode, act="fp16", out=None, workspace=None):
     ws, ws_bytes = _workspace(mode, flag, m, nw, x.device, workspace)
     _check(lib.dps_linear(mode, flag, _ptr(x), m, ctypes.byref(nw.c()), _ptr(out), _ptr(ws),
                           ws_bytes, _stream()))
+    return out
+
+
+STATIC_SCRATCH_BYTES = 64 << 20   # DPS_STATIC_SCRATCH_BYTES
+
+
+def linear_static(x, nw, mode, act="fp16", out=None):
+    """Y = X . W^T through dps_linear_static: the library's static device
+    scratch instead of a workspace, so the call allocates nothing (beyond
+    `out` when it is not given)."""
+    lib = load_library()
+    _require_cuda(x)
+    assert x.dtype == torch.float16 and x.dim() == 2 and x.is_contiguous()
+    flag = _act_flag(act)
+    m = x.shape[0]
+    if out is None:
+        out = torch.empty((m, nw.n), dtype=torch.float16, device=x.device)
+    _check(lib.dps_linear_static(mode, flag, _ptr(x), m, ctypes.byref(nw.c()), _ptr(out),
+                                 _stream()))
     return out
 
 
