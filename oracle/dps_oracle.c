@@ -314,6 +314,28 @@ int oracle_backup(const uint8_t *pool, int64_t pool_bytes, const int32_t *slots,
 
 enum { ORACLE_FULL = 0, ORACLE_FAST = 1 };
 
+/* sum_{kk < k} a[kk] * b[kk] in fp64, in the natural k order.              */
+static double dot(const double *a, const double *b, int64_t k)
+{
+    double acc = 0.0;
+    for (int64_t kk = 0; kk < k; ++kk)
+        acc += a[kk] * b[kk];
+    return acc;
+}
+
+/* Rows [r0, r1) of the FP16 matrix x [.][k], decoded once into a new fp64
+ * array [r1 - r0][k] (NULL if it cannot be allocated).                    */
+static double *decode_fp16_rows(const uint16_t *x, int64_t r0, int64_t r1, int64_t k)
+{
+    int64_t cnt = (r1 - r0) * k;
+    double *v = (double *)malloc(sizeof(double) * (size_t)(cnt > 0 ? cnt : 1));
+    if (!v)
+        return NULL;
+    for (int64_t i = 0; i < cnt; ++i)
+        v[i] = oracle_fp16_value(x[r0 * k + i]);
+    return v;
+}
+
 /* Weight element (c, k) of the expert whose elements start at logical
  * offset w_base (e * n * k for expert e).  Fills row c of the decoded
  * weight into wrow[0..k).                                                  */
@@ -362,6 +384,9 @@ int oracle_linear_grouped(int mode, int enc, const uint16_t *x, const int64_t *o
         if (r1 == r0)
             continue;
         int64_t w_base = e * n * k;
+        double *xv = decode_fp16_rows(x, r0, r1, k);
+        if (!xv)
+            return -1;
 #pragma omp parallel
         {
             double *wrow = (double *)malloc(sizeof(double) * (size_t)(k > 0 ? k : 1));
@@ -373,16 +398,13 @@ int oracle_linear_grouped(int mode, int enc, const uint16_t *x, const int64_t *o
                 for (int64_t c = 0; c < n; ++c) {
                     decode_weight_row(mode, enc, hi, pool, pool_bytes, slots, n_chunks,
                                       log2_chunk, w_base, c, k, wrow);
-                    for (int64_t r = r0; r < r1; ++r) {
-                        double acc = 0.0;
-                        for (int64_t kk = 0; kk < k; ++kk)
-                            acc += oracle_fp16_value(x[r * k + kk]) * wrow[kk];
-                        y[r * n + c] = acc;
-                    }
+                    for (int64_t r = r0; r < r1; ++r)
+                        y[r * n + c] = dot(xv + (r - r0) * k, wrow, k);
                 }
                 free(wrow);
             }
         }
+        free(xv);
     }
     return bad ? -1 : 0;
 }
@@ -411,6 +433,13 @@ int oracle_linear_rows(int mode, int enc, const uint16_t *x, const int64_t *rows
     if (mode == ORACLE_FULL &&
         check_residual(n * k, slots, n_chunks, log2_chunk, pool_bytes))
         return -1;
+    /* the listed rows of x, decoded once */
+    double *xv = (double *)malloc(sizeof(double) * (size_t)(n_rows * k > 0 ? n_rows * k : 1));
+    if (!xv)
+        return -1;
+    for (int64_t j = 0; j < n_rows; ++j)
+        for (int64_t kk = 0; kk < k; ++kk)
+            xv[j * k + kk] = oracle_fp16_value(x[rows[j] * k + kk]);
     int bad = 0;
 #pragma omp parallel
     {
@@ -423,16 +452,13 @@ int oracle_linear_rows(int mode, int enc, const uint16_t *x, const int64_t *rows
             for (int64_t c = 0; c < n; ++c) {
                 decode_weight_row(mode, enc, hi, pool, pool_bytes, slots, n_chunks,
                                   log2_chunk, 0, c, k, wrow);
-                for (int64_t j = 0; j < n_rows; ++j) {
-                    double acc = 0.0;
-                    for (int64_t kk = 0; kk < k; ++kk)
-                        acc += oracle_fp16_value(x[rows[j] * k + kk]) * wrow[kk];
-                    y[j * n + c] = acc;
-                }
+                for (int64_t j = 0; j < n_rows; ++j)
+                    y[j * n + c] = dot(xv + j * k, wrow, k);
             }
             free(wrow);
         }
     }
+    free(xv);
     return bad ? -1 : 0;
 }
 
@@ -476,17 +502,32 @@ int oracle_linear_fp8(int enc, const uint8_t *xq, const double *scale, int64_t m
 {
     if (enc != ORACLE_ENC_E5M2 && enc != ORACLE_ENC_E4M3)
         return -1;
-#pragma omp parallel for schedule(static)
-    for (int64_t c = 0; c < n; ++c) {
-        for (int64_t r = 0; r < m; ++r) {
-            double acc = 0.0;
-            for (int64_t kk = 0; kk < k; ++kk)
-                acc += oracle_e4m3_value(xq[r * k + kk]) *
-                       oracle_fast_value(enc, hi[c * k + kk]);
-            y[r * n + c] = scale[r] * acc;
+    /* the E4M3 activation codes, decoded once */
+    double *xv = (double *)malloc(sizeof(double) * (size_t)(m * k > 0 ? m * k : 1));
+    if (!xv)
+        return -1;
+    for (int64_t i = 0; i < m * k; ++i)
+        xv[i] = oracle_e4m3_value(xq[i]);
+    int bad = 0;
+#pragma omp parallel
+    {
+        double *wrow = (double *)malloc(sizeof(double) * (size_t)(k > 0 ? k : 1));
+        if (!wrow) {
+#pragma omp atomic write
+            bad = 1;
+        } else {
+#pragma omp for schedule(static)
+            for (int64_t c = 0; c < n; ++c) {
+                for (int64_t kk = 0; kk < k; ++kk)
+                    wrow[kk] = oracle_fast_value(enc, hi[c * k + kk]);
+                for (int64_t r = 0; r < m; ++r)
+                    y[r * n + c] = scale[r] * dot(xv + r * k, wrow, k);
+            }
+            free(wrow);
         }
     }
-    return 0;
+    free(xv);
+    return bad ? -1 : 0;
 }
 
 /* Number of OpenMP threads the linear routines run on.                    */

@@ -37,11 +37,15 @@ MUTATIONS = [
     ("expert_base_dropped", "int64_t w_base = e * n * k;", "int64_t w_base = 0;"),
     ("fast_rounds_up", "wrow[kk] = oracle_fast_value(enc, hi[i]);",
      "wrow[kk] = oracle_fast_value(enc, (uint8_t)(hi[i] + 1));"),
-    ("x_reversed", "acc += oracle_fp16_value(x[r * k + kk]) * wrow[kk];",
-     "acc += oracle_fp16_value(x[r * k + (k - 1 - kk)]) * wrow[kk];"),
+    ("x_reversed", "v[i] = oracle_fp16_value(x[r0 * k + i]);",
+     "v[i] = oracle_fp16_value(x[r0 * k + (i / k) * k + (k - 1 - i % k)]);"),
+    ("rows_x_reversed", "xv[j * k + kk] = oracle_fp16_value(x[rows[j] * k + kk]);",
+     "xv[j * k + kk] = oracle_fp16_value(x[rows[j] * k + (k - 1 - kk)]);"),
+    ("dot_operand_reversed", "acc += a[kk] * b[kk];", "acc += a[kk] * b[k - 1 - kk];"),
     ("tie_to_odd", "(c & 1) == 0 && (best & 1) == 1", "(c & 1) == 1 && (best & 1) == 0"),
     ("scale_one_step_high", "while (a <= 448.0 * (s / 2.0))", "while (a <= 448.0 * (s / 4.0))"),
-    ("fp8_scale_dropped", "y[r * n + c] = scale[r] * acc;", "y[r * n + c] = acc;"),
+    ("fp8_scale_dropped", "y[r * n + c] = scale[r] * dot(xv + r * k, wrow, k);",
+     "y[r * n + c] = dot(xv + r * k, wrow, k);"),
     ("e4m3_bias", "return sign * ldexp(1.0 + (double)m / 8.0, e - 7);",
      "return sign * ldexp(1.0 + (double)m / 8.0, e - 8);"),
     # E4M3 nesting and the encoding choice
@@ -58,8 +62,8 @@ MUTATIONS = [
      "if (e >= 17 || isnan(oracle_e4m3_value(hi)))"),
     ("full_ignores_enc", "oracle_fp16_value(unnest_word(enc, hi[i], p < 0 ? 0 : pool[p]))",
      "oracle_fp16_value(unnest_word(0, hi[i], p < 0 ? 0 : pool[p]))"),
-    ("fp8_ignores_enc", "oracle_fast_value(enc, hi[c * k + kk]);",
-     "oracle_e5m2_value(hi[c * k + kk]);"),
+    ("fp8_ignores_enc", "wrow[kk] = oracle_fast_value(enc, hi[c * k + kk]);",
+     "wrow[kk] = oracle_e5m2_value(hi[c * k + kk]);"),
     # backup and restore
     ("restore_whole_stream", "for (int64_t i = c0 * chunk_bytes; i < c1 * chunk_bytes && i < numel; ++i) {",
      "for (int64_t i = 0; i < numel; ++i) {"),
