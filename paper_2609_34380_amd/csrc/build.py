@@ -29,10 +29,11 @@ CFLAGS = [
 ]
 
 
-# Sources whose kernels issue loads the compiler does not track (inline asm,
-# retired by the kernel's own counter waits): their registers must never be
-# spilled or copied before that wait, so any scratch use fails the build.
-NO_SCRATCH = {"dps_rows.hip"}
+# Kernel sources whose kernels must not use scratch: a spill or a stack array
+# in a streaming or matrix-core kernel adds memory traffic beside the weight
+# stream and costs time with no error, so the build fails on it instead.
+NO_SCRATCH = {"dps_elementwise.hip", "dps_skinny.hip", "dps_gemv.hip", "dps_rows.hip",
+              "dps_gemm.hip"}
 
 
 def _scratch_users(report):

@@ -14,10 +14,12 @@
 //     chosen so that the grid about fills the chip once;
 //   - the eight waves split each stage's K range: wave w multiplies the
 //     128-element slice [128w, 128w+128) of every stage, its activations
-//     held in registers for the whole 1024-element chunk (prefetched one
-//     chunk ahead), and keeps one fp32 accumulator tile per row group and
-//     16-token tile; the waits for the ring count the activation loads, so
-//     they retire exactly the stage about to be read;
+//     held in registers for the whole 1024-element chunk, and keeps one fp32
+//     accumulator tile per row group and 16-token tile.  The activation
+//     slice of the next chunk streams into a 4 KiB LDS area of the wave with
+//     direct-to-LDS loads, like the weights, so every load the kernel issues
+//     is counted by the same vector-memory counter and the ring's waits
+//     retire exactly what the stage about to be read needs;
 //   - at the end the eight slices are summed through LDS in wave order, so
 //     the result does not depend on timing, and written as FP16.
 // Weights are merged (full mode) or converted (fast mode) into FP16 words in
@@ -72,32 +74,16 @@ __device__ __forceinline__ void rows_barrier()
 
 __device__ __forceinline__ int rows_swz(int i) { return (i & 15) << 2; }
 
-// 16-byte activation load whose completion the kernel tracks itself: the
-// compiler's own wait analysis loses count across the chunk loop and would
-// wait for every load in flight (draining the DMA ring) before each use.
-// The value may only be read after a vmcnt wait that retires it, followed
-// by rows_tie on it; nor may the compiler spill or copy it before then, so
-// the build rejects any kernel of this file that uses scratch.
-__device__ __forceinline__ u32x4 rows_gload16(const void *p)
-{
-    u32x4 v;
-    asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v) : "v"(p) : "memory");
-    return v;
-}
-
-// Orders the reads of v after the preceding wait (both are volatile).
-__device__ __forceinline__ void rows_tie(u32x4 &v)
-{
-    asm volatile("" : "+v"(v));
-}
-
 typedef const __attribute__((address_space(4))) int32_t *const_i32p;
 
-// Ring depth.  The vector-memory counter retires in issue order, so the wait
-// for the activations of chunk c+1 (loaded at the start of chunk c, after the
-// DMA of stage cG + WS - 2) also waits for that DMA; with WS - 2 <= G it is
-// DMA the first stage of chunk c+1 needs anyway.  Deeper rings (up to 128
-// KiB) serve blocks with more row groups.
+// Ring depth: WS - 2 <= G keeps the activation load of the next chunk
+// (issued at the first stage of a chunk) behind the DMA the counter waits
+// for, so the waits retire no DMA a later stage could still have overlapped
+// (the counter arithmetic is derived at the main loop).  Deeper rings serve
+// blocks with more row groups.  Behind the ring, each wave has XB areas of
+// XA bytes for its activation slice of one chunk: two where LDS allows
+// (the next chunk's slice then streams in while this one is read), else
+// one, refilled right after it has been read.
 template <int MODE, int NT, int G>
 struct RowsConfig {
     static constexpr int PLANES = MODE == MODE_FULL ? 2 : 1;
@@ -106,9 +92,13 @@ struct RowsConfig {
     static constexpr int WS = G + 2 < WSMAX ? G + 2 : WSMAX;
     static constexpr int NI = 2 * PLANES;  // DMA instructions per wave per stage
     static constexpr int RED = 8 * G * NT * 1024;  // slice sums, reusing the ring
-    static constexpr int LDS = WS * SLOT > RED ? WS * SLOT : RED;
+    static constexpr int RING = WS * SLOT > RED ? WS * SLOT : RED;
+    static constexpr int XL = 4 * NT;              // activation instructions per wave per chunk
+    static constexpr int XA = XL * 1024;           // activation area of one wave
+    static constexpr int XB = RING + 2 * 8 * XA <= 160 * 1024 ? 2 : 1;
+    static constexpr int LDS = RING + XB * 8 * XA;
     static_assert(WS >= 3 && WS - 2 <= G, "ring depth");
-    static_assert(LDS <= 131072, "LDS");
+    static_assert(LDS <= 160 * 1024, "LDS");
 };
 
 // NT: 16-token tiles (tokens <= 16 NT); G: 16-row groups per block; RANGE:
@@ -194,13 +184,20 @@ __global__ __launch_bounds__(512) void rows_kernel(RowsArgs a)
             }
     };
 
-    // ---- activations of this wave's K slice for chunk step c: step pair s2,
-    // half h, token tile nt -> lane (j, g) holds X[16 nt + j][kc(c) KC + 16
-    // (8w + 4 s2 + g) + 8 h .. +7] (token rows past m repeat row m-1).  Always XL load
-    // instructions (past K: a valid address; the value is cleared at use).
-    constexpr int XL = 4 * NT;
-    u32x4 xa[2][2][NT], xb[2][2][NT];
-    auto load_x = [&](int64_t c, u32x4 (&xr)[2][2][NT]) {
+    // ---- activations of this wave's K slice for chunk step c: instruction q
+    // = (s2, h, nt) of lane (j, g) loads X[16 nt + j][kc(c) KC + 16 (8w + 4 s2
+    // + g) + 8 h .. +7] (token rows past m repeat row m-1; past K a valid
+    // address, the value is cleared when read) into 16-byte position `lane`
+    // of 1 KiB piece q of the wave's area, so each lane later reads back
+    // exactly its own 16 bytes.
+    constexpr int XL = C::XL;
+    constexpr int XB = C::XB;
+    // the wave's area for chunk c
+    auto xarea = [&](int64_t c) {
+        return smem + C::RING + ((XB == 2 ? (int)(c & 1) : 0) * 8 + wave) * C::XA;
+    };
+    auto issue_x = [&](int64_t c, int64_t cbuf) {
+        uint8_t *xa = xarea(cbuf);
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
             int64_t tok = 16 * nt + li;
@@ -211,13 +208,17 @@ __global__ __launch_bounds__(512) void rows_kernel(RowsArgs a)
                 const int64_t kv = kk < a.k ? kk : 0;
 #pragma unroll
                 for (int h = 0; h < 2; ++h)
-                    xr[s2][h][nt] = rows_gload16(a.x + tok * a.k + kv + 8 * h);
+                    __builtin_amdgcn_global_load_lds(
+                        a.x + tok * a.k + kv + 8 * h,
+                        DPS_ROWS_LDS(xa + ((s2 * 2 + h) * NT + nt) * 1024), 16, 0, 0);
             }
         }
     };
-    // after the wait that retires chunk c's loads: order the reads, clear
-    // what lies past K
-    auto ready_x = [&](int64_t c, u32x4 (&xr)[2][2][NT]) {
+    // after the wait that retires chunk c's activation loads: registers from
+    // the wave's area, with what lies past K cleared
+    u32x4 xr[2][2][NT];
+    auto read_x = [&](int64_t c) {
+        const uint8_t *xa = xarea(c);
 #pragma unroll
         for (int s2 = 0; s2 < 2; ++s2) {
             const int64_t kk = kc(c) * kRowsKC + 16 * (8 * wave + 4 * s2 + lg);
@@ -226,7 +227,8 @@ __global__ __launch_bounds__(512) void rows_kernel(RowsArgs a)
             for (int h = 0; h < 2; ++h)
 #pragma unroll
                 for (int nt = 0; nt < NT; ++nt) {
-                    rows_tie(xr[s2][h][nt]);
+                    xr[s2][h][nt] = *reinterpret_cast<const u32x4 *>(
+                        xa + ((s2 * 2 + h) * NT + nt) * 1024 + lane * 16);
                     xr[s2][h][nt] &= u32x4{msk, msk, msk, msk};
                 }
         }
@@ -245,29 +247,52 @@ __global__ __launch_bounds__(512) void rows_kernel(RowsArgs a)
     for (int s2 = 0; s2 < 2; ++s2)
         foff[s2] = li * kRowsKC + (((8 * wave + 4 * s2 + lg) ^ rows_swz(li)) << 4);
 
-    // Issue order: X(0); DMA of stages 0 .. WS-2; then per chunk c: X(c+1)
-    // (the last chunk loads its own again), and per stage t of the chunk:
-    // wait, barrier, DMA of stage t+WS-1 (always NI instructions).  X(c')
-    // follows the DMA of stage c'G - G + WS - 2.  The counter retires in
-    // issue order, and the wait for stage t = cG + g leaves outstanding what
-    // was issued after the DMA of stage t: the DMA of stages t+1 .. t+WS-2,
-    // and X(c+1) when g <= WS-2 (X(c) never, as WS - 2 <= G).  At g = 0 it
-    // also retires X(c): G NI + XL >= (WS-2) NI + XL instructions followed it.
+    // Issue order with one area per wave (XB == 1): X(0); DMA of stages
+    // 0 .. WS-2; then per stage t = cG + g: wait, barrier, at g = 0 the read
+    // of X(c) from the area followed by the load of X(c+1) into it (the last
+    // chunk loads its own again), then the DMA of stage t+WS-1 (always NI
+    // instructions).  The counter retires in issue order.  The wait for
+    // stage t may leave outstanding what was issued after the later of
+    // DMA(t) and, at g = 0, X(c):
+    //   - DMA(t+1) .. DMA(t+WS-2), issued in earlier iterations: BASE;
+    //   - at g = 0, X(c) went out in iteration (c-1)G, ahead of that
+    //     iteration's DMA, which is DMA(t+1) when WS = G+2 and DMA(t) or an
+    //     earlier one otherwise (WS - 2 <= G), so BASE retires X(c) too;
+    //   - at 1 <= g <= WS-2, X(c+1) (iteration cG) followed DMA(t)
+    //     (iteration t-WS+1 < cG): BASE + XL; from g = WS-1 on it precedes.
+    // With two areas (XB == 2), X(c+1) goes into the other area at the start
+    // of chunk c, before the wait of its first stage: X(c) then precedes
+    // DMA(t) at g = 0, and X(c+1) follows DMA(t) for g <= WS-2 (BASE + XL),
+    // not after.  (A model of both issue orders on the host shows every wait
+    // retires what its stage reads and nothing later, for G = 1..8 and both
+    // modes.)
     constexpr int BASE = (WS - 2) * NI;
     static_assert(BASE + XL <= 63, "vmcnt range");
 
-    // one chunk's G stages, with its activations in xr
-    auto chunk = [&](int64_t c, u32x4 (&xr)[2][2][NT]) {
+    issue_x(0, 0);
+#pragma unroll
+    for (int u = 0; u < WS - 1; ++u)
+        issue(u);
+    for (int64_t c = 0; c < nkc; ++c) {
+        if (XB == 2)
+            issue_x(c + 1 < nkc ? c + 1 : c, c + 1);
 #pragma unroll
         for (int g = 0; g < G; ++g) {
             const int64_t t = c * G + g;
-            if (g <= WS - 2)
+            const bool x_pending = XB == 2 ? g <= WS - 2 : (g >= 1 && g <= WS - 2);
+            if (x_pending)
                 DPS_ROWS_WAIT_VMCNT(BASE + XL);
             else
                 DPS_ROWS_WAIT_VMCNT(BASE);
             rows_barrier();
-            if (g == 0)
-                ready_x(c, xr);
+            if (g == 0) {
+                read_x(c);
+                if (XB == 1) {
+                    // the area is refilled only once this wave's reads of it are done
+                    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+                    issue_x(c + 1 < nkc ? c + 1 : c, 0);
+                }
+            }
             issue(t + WS - 1);
             const uint8_t *slot = smem + (int)(t % WS) * SLOT;
 #pragma unroll
@@ -285,35 +310,10 @@ __global__ __launch_bounds__(512) void rows_kernel(RowsArgs a)
                 }
             }
         }
-    };
-
-    // Two activation buffers in turn (no register copies, whose waits would
-    // retire the whole ring).
-    load_x(0, xa);
-#pragma unroll
-    for (int u = 0; u < WS - 1; ++u)
-        issue(u);
-    for (int64_t c = 0; c < nkc; c += 2) {
-        load_x(c + 1 < nkc ? c + 1 : c, xb);
-        chunk(c, xa);
-        if (c + 1 < nkc) {
-            load_x(c + 2 < nkc ? c + 2 : c + 1, xa);
-            chunk(c + 1, xb);
-        }
     }
 
-    DPS_ROWS_WAIT_VMCNT(0);  // no DMA may still target the ring
-    // the last activation loads (never read) keep their registers until here
-#pragma unroll
-    for (int s2 = 0; s2 < 2; ++s2)
-#pragma unroll
-        for (int h = 0; h < 2; ++h)
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) {
-                rows_tie(xa[s2][h][nt]);
-                rows_tie(xb[s2][h][nt]);
-            }
-    __syncthreads();         // every wave is done reading it
+    DPS_ROWS_WAIT_VMCNT(0);  // no DMA may still target the ring or the areas
+    __syncthreads();         // every wave is done reading the ring
 
     // ---- slice sums: wave w stores its tiles, then tile (g, nt) is summed
     // over w = 0..7 in order by wave (g NT + nt) % 8.
