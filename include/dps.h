@@ -219,6 +219,30 @@ dps_status dps_linear(int mode, uint32_t flags, const uint16_t *x, int64_t m,
                       const dps_weight *w, uint16_t *y, void *ws, size_t ws_bytes,
                       void *stream);
 
+/* Kernel families of the linear calls (dps_plan_info). */
+enum {
+    DPS_KERNEL_GEMV = 0,     /* 1-4 tokens: whole weight rows per wave, vector ALUs  */
+    DPS_KERNEL_ROWS = 1,     /* up to 16 tokens: 16-row groups, whole K per block    */
+    DPS_KERNEL_DECODE = 2,   /* a few tokens per expert: LDS-ring decode kernel      */
+    DPS_KERNEL_GEMM_F16 = 3, /* FP16 matrix cores, weight tile x token tile          */
+    DPS_KERNEL_GEMM_FP8 = 4  /* FP8 matrix cores (DPS_ACT_FP8_ROWSCALE)              */
+};
+
+/* The launch plan of a dps_linear (experts == 1) or dps_linear_grouped call
+ * with these arguments on the current device, for introspection (which
+ * kernel runs, how the work is tiled):
+ *   info[0]  DPS_KERNEL_* family;
+ *   info[1]  weight rows per block (0 for DPS_KERNEL_GEMV: whole rows per
+ *            wave);
+ *   info[2]  token rows per block tile (per pass for DPS_KERNEL_DECODE);
+ *   info[3]  K splits (> 1: fp32 partials in the workspace, summed in a
+ *            second launch);
+ *   info[4]  K elements per split.
+ * log2_chunk is the residual chunk size of a full-mode call (ignored in fast
+ * mode).  Host only; enqueues nothing.  info: host int64[5]. */
+dps_status dps_plan_info(int mode, uint32_t flags, int64_t rows, int64_t n, int64_t k,
+                         int64_t experts, int32_t log2_chunk, int64_t *info);
+
 /* Upper bound of the scratch dps_linear_static may use: 64 MiB per device.
  * dps_workspace_bytes() at or below it means the call fits. */
 #define DPS_STATIC_SCRATCH_BYTES (((size_t)64) << 20)

@@ -400,6 +400,49 @@ DPS_EXPORT size_t dps_workspace_bytes(int mode, uint32_t flags, int64_t rows, in
     return p.ws_partial + p.ws_quant;
 }
 
+DPS_EXPORT dps_status dps_plan_info(int mode, uint32_t flags, int64_t rows, int64_t n, int64_t k,
+                                    int64_t experts, int32_t log2_chunk, int64_t *info)
+{
+    g_err[0] = 0;
+    REQUIRE(mode == DPS_MODE_FULL || mode == DPS_MODE_FAST, DPS_ERR_INVALID_ARG, "unknown mode");
+    REQUIRE(flags == DPS_ACT_FP16 || flags == DPS_ACT_FP8_ROWSCALE, DPS_ERR_INVALID_ARG,
+            "unknown flags");
+    REQUIRE(rows > 0 && n > 0 && k > 0 && experts >= 1, DPS_ERR_INVALID_ARG,
+            "rows, n, k and experts must be positive");
+    REQUIRE(log2_chunk >= 4 && log2_chunk <= 30, DPS_ERR_INVALID_ARG,
+            "log2_chunk must be in 4..30");
+    REQUIRE(info != nullptr, DPS_ERR_INVALID_ARG, "info is NULL");
+    const bool grouped = experts > 1;
+    const dps::LinearPlan p =
+        dps::plan_linear(mode, flags, rows, n, k, experts,
+                         mode == DPS_MODE_FULL ? log2_chunk : 30, current_cu_count(), grouped);
+    switch (p.kind) {
+    case dps::KIND_GEMV:
+        info[0] = DPS_KERNEL_GEMV;
+        info[1] = 0;
+        info[2] = rows;
+        break;
+    case dps::KIND_ROWS:
+        info[0] = DPS_KERNEL_ROWS;
+        info[1] = 16 * p.variant;
+        info[2] = 16;
+        break;
+    case dps::KIND_SKINNY:
+        info[0] = DPS_KERNEL_DECODE;
+        info[1] = dps::skinny_rows_per_block(p.variant);
+        info[2] = dps::skinny_pass_rows(rows, grouped);
+        break;
+    default:
+        info[0] = p.kind == dps::KIND_GEMM_FP8 ? DPS_KERNEL_GEMM_FP8 : DPS_KERNEL_GEMM_F16;
+        info[1] = dps::gemm_rows_per_block(p.variant);
+        info[2] = dps::gemm_tokens_per_block(p.variant);
+        break;
+    }
+    info[3] = p.splits;
+    info[4] = p.ksplit;
+    return DPS_OK;
+}
+
 namespace {
 
 dps_status run_linear(int mode, uint32_t flags, const uint16_t *x, const int32_t *offsets,
@@ -416,7 +459,12 @@ dps_status run_linear(int mode, uint32_t flags, const uint16_t *x, const int32_t
                 "workspace is smaller than dps_workspace_bytes()");
         REQUIRE(aligned(ws, 256), DPS_ERR_ALIGNMENT, "workspace is not 256-byte aligned");
     }
-    const int64_t token_tiles = (rows + 127) / 128 + (grouped ? w->experts : 0);
+    // grouped GEMM grids run one row of blocks per token tile plus one per
+    // expert (grid.y); keep every call within that limit
+    const bool gemm = plan.kind == dps::KIND_GEMM_F16 || plan.kind == dps::KIND_GEMM_FP8;
+    const int64_t token_tiles =
+        cdiv(rows, gemm ? dps::gemm_tokens_per_block(plan.variant) : 128) +
+        (grouped ? w->experts : 0);
     REQUIRE(token_tiles <= 65535, DPS_ERR_UNSUPPORTED, "too many rows for one call");
     REQUIRE(plan.splits <= 65535, DPS_ERR_UNSUPPORTED, "k too large for one call");
 

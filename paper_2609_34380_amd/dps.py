@@ -27,7 +27,7 @@ ERR_NO_SPACE = 6
 UNIT_FREE, UNIT_BACKED, UNIT_AVAIL, UNIT_FULL, UNIT_RESTORING = 0, 1, 2, 3, 4
 
 EXPORTED = ("dps_select_enc", "dps_split", "dps_merge", "dps_restore", "dps_backup", "dps_quant_rows_e4m3", "dps_workspace_bytes",
-            "dps_linear", "dps_linear_static", "dps_linear_grouped", "dps_status_str", "dps_last_error",
+            "dps_plan_info", "dps_linear", "dps_linear_static", "dps_linear_grouped", "dps_status_str", "dps_last_error",
             "dps_sum_create", "dps_sum_destroy", "dps_sum_alloc", "dps_sum_free",
             "dps_sum_restore_begin", "dps_sum_restore_done", "dps_sum_mode",
             "dps_sum_unit_state", "dps_sum_unit_of", "dps_sum_counts", "dps_sum_slots")
@@ -79,6 +79,8 @@ def load_library(path=LIB_PATH):
     lib.dps_quant_rows_e4m3.restype = ST
     lib.dps_workspace_bytes.argtypes = [ctypes.c_int, U32, I64, I64, I64, I64]
     lib.dps_workspace_bytes.restype = ctypes.c_size_t
+    lib.dps_plan_info.argtypes = [ctypes.c_int, U32, I64, I64, I64, I64, I32, P]
+    lib.dps_plan_info.restype = ST
     lib.dps_linear.argtypes = [ctypes.c_int, U32, P, I64, ctypes.POINTER(CWeight), P, P,
                                ctypes.c_size_t, P]
     lib.dps_linear.restype = ST
@@ -276,6 +278,20 @@ def quant_rows_e4m3(x):
 def workspace_bytes(mode, act, rows, n, k, experts=1):
     lib = load_library()
     return lib.dps_workspace_bytes(mode, act, rows, n, k, experts)
+
+
+KERNEL_NAMES = {0: "gemv", 1: "rows", 2: "decode", 3: "gemm_f16", 4: "gemm_fp8"}
+
+
+def plan_info(mode, act, rows, n, k, experts=1, log2_chunk=21):
+    """The launch plan of a linear call (dps_plan_info): a dict with the
+    kernel family, weight rows and token rows per block tile, K splits and
+    K elements per split."""
+    lib = load_library()
+    info = (ctypes.c_int64 * 5)()
+    _check(lib.dps_plan_info(mode, _act_flag(act), rows, n, k, experts, log2_chunk, info))
+    return {"kernel": KERNEL_NAMES[info[0]], "tile_rows": info[1], "tile_tokens": info[2],
+            "splits": info[3], "ksplit": info[4]}
 
 
 def _act_flag(act):

@@ -188,3 +188,46 @@ def test_planner_splits_k_for_narrow_layers_beyond_16_tokens(lib, mode):
         ws = lib.dps_workspace_bytes(mode, 0, m, 4096, 4096, 1)
         assert ws >= 2 * m * 4096 * 4, (m, ws)
         assert ws == lib.dps_workspace_bytes(1 - mode, 0, m, 4096, 4096, 1)
+
+
+def test_plan_info_names_the_kernel_of_each_shape_class(lib):
+    """The planner's choice, read through dps_plan_info, for one shape of each
+    kernel family (on a 256-CU part, or when no device is visible)."""
+    from paper_2609_34380_amd import dps as d
+    assert d.plan_info(0, "fp16", 1, 4096, 4096)["kernel"] == "gemv"
+    assert d.plan_info(1, "fp16", 8, 6144, 4096)["kernel"] == "rows"
+    p = d.plan_info(1, "fp16", 8, 4096, 4096, experts=8)
+    assert p["kernel"] == "decode"
+    p = d.plan_info(0, "fp16", 2048, 28672, 4096)
+    assert (p["kernel"], p["tile_rows"], p["tile_tokens"], p["splits"]) == ("gemm_f16", 128, 128, 1)
+    p = d.plan_info(1, "fp8", 4096, 4096, 1024)
+    assert (p["kernel"], p["tile_rows"], p["tile_tokens"]) == ("gemm_fp8", 256, 256)
+    p = d.plan_info(1, "fp8", 2048, 6144, 4096)
+    assert (p["kernel"], p["tile_rows"], p["tile_tokens"]) == ("gemm_fp8", 256, 128)
+    # the workspace query follows the same plan
+    for mode, act, m, n, k in ((0, "fp16", 128, 4096, 4096), (1, "fp8", 512, 4096, 4096)):
+        p = d.plan_info(mode, act, m, n, k)
+        ws = d.workspace_bytes(mode, d._act_flag(act), m, n, k)
+        assert (p["splits"] > 1) == (ws >= p["splits"] * m * n * 4 > 0), (m, n, k, p, ws)
+
+
+def test_plan_info_rejects_bad_arguments(lib):
+    info = (ctypes.c_int64 * 5)()
+    assert lib.dps_plan_info(3, 0, 8, 64, 64, 1, 21, info) == 1
+    assert lib.dps_plan_info(0, 0, 0, 64, 64, 1, 21, info) == 1
+    assert lib.dps_plan_info(0, 0, 8, 64, 64, 1, 3, info) == 1
+    assert lib.dps_plan_info(0, 0, 8, 64, 64, 1, 21, None) == 1
+
+
+def test_grouped_grid_limit_uses_the_planned_token_tile(lib):
+    """60000 experts of 10 rows each plan 32-token tiles: 18750 token tiles
+    plus one per expert exceed the 65535 blocks of grid.y, so the call is
+    refused on the host (it fitted the old 128-token estimate and would have
+    failed at launch)."""
+    experts, rows = 60000, 600000
+    w = _weight(n=64, k=64, experts=experts, n_chunks=experts, log2=12,
+                pool_bytes=experts << 12)
+    st = lib.dps_linear_grouped(1, 0, 0x4000, 0x6000, rows, ctypes.byref(w), 0x5000, None, 0,
+                                None)
+    assert st == 3, st
+    assert b"too many rows" in lib.dps_last_error()
