@@ -55,6 +55,9 @@ def parse():
                          "copy kernel of known size, then exit; ':fp8' = fast mode on FP8 "
                          "activations (prefill)")
     ap.add_argument("--probe-reps", type=int, default=20)
+    ap.add_argument("--ceilings", action="store_true",
+                    help="measure only the HBM streaming-read and MFMA-loop ceilings "
+                         "(libdps_probe), print them as JSON and exit")
     ap.add_argument("--enc", choices=("e5m2", "e4m3"), default="e5m2",
                     help="nested encoding of every layer")
     return ap.parse_args()
@@ -83,6 +86,9 @@ def main():
 
     layers = workloads.H4096_SET
     enc = dps.ENC_E4M3 if args.enc == "e4m3" else dps.ENC_E5M2
+    if args.ceilings:
+        print(json.dumps({"ceilings": measured_ceilings(torch, stream)}), flush=True)
+        return
     if args.probe_call:
         probe(args, torch, dps, workloads, layers, dev, stream, enc)
         return
@@ -173,10 +179,12 @@ def main():
             t = ts[len(ts) // 2] * 1e-3
             name, n, k = layers[li]
             wb = weight_bytes(mode, li)
+            p10, p90 = pct(ts, 10), pct(ts, 90)
             alg = wb + 2 * m * k + 2 * m * n
             flops = 2.0 * m * n * k
             bound_t = max(alg / (HBM_PEAK_GBS * 1e9), flops / (MFMA_F16_TFLOPS * 1e12))
             breakdown.append({"layer": name, "M": m, "mode": mname, "us": round(t * 1e6, 2),
+                              "us_p10": round(p10 * 1e3, 2), "us_p90": round(p90 * 1e3, 2),
                               "eff_weight_GBs": round(wb / t / 1e9, 1),
                               "alg_GBs": round(alg / t / 1e9, 1),
                               "TFLOPs": round(flops / t / 1e12, 2),
@@ -218,7 +226,12 @@ def main():
         roof = {"bound": "mfma", "achieved": round(flops / t_launch / 1e12, 1),
                 "peak": MFMA_F16_TFLOPS, "unit": "TFLOP/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = measured_traffic("%s:%d:%s" % (dom["layer"], dm, dom["mode"]), args.enc)
+    traffic = measured_traffic("%s:%d:%s" % (dom["layer"], dm, dom["mode"]), args.enc)
+    roof["traffic"] = traffic[0] if traffic else None
+    roof["traffic_source"] = (
+        "replayed from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE record %s (taken on "
+        "these kernel sources: csrc sha256 matches); not measured in this run" % traffic[1]
+        if traffic else "no committed counter record for these kernel sources")
     roof["kernel"] = ("%s layer %dx%d, M=%d, %s mode" % (dom["layer"], dn, dk, dm, dom["mode"]))
     roof["probe_call"] = "%s:%d:%s" % (dom["layer"], dm, dom["mode"])
     roof["us_per_launch"] = round(t_launch * 1e6, 2)
@@ -227,7 +240,12 @@ def main():
     # ---- secondary: prefill TFLOPS (FP8 fast, FP16 full) ---------------------------
     secondary = {}
     if not args.no_secondary:
-        secondary = prefill_secondary(torch, dps, workloads, copies[0], layers, stream)
+        ceil = measured_ceilings(torch, stream)
+        ref = ceil["hbm_read_GBs_nontemporal"] if roof["bound"] == "hbm" else ceil["mfma_f16_TFLOPs"]
+        roof["measured_peak"] = ref
+        roof["frac_of_measured_peak"] = round(roof["achieved"] / ref, 4)
+        secondary = {"measured_ceilings": ceil}
+        secondary.update(prefill_secondary(torch, dps, workloads, copies[0], layers, stream))
         secondary["graph_pair"] = graph_pair_secondary(torch, dps, run_call, layers, ms, stream,
                                                        ms_per_step)
     del graphs, g_dom, copies
@@ -270,16 +288,69 @@ def main():
     print(json.dumps(out), flush=True)
 
 
+def pct(sorted_ms, q):
+    """Nearest-rank q-th percentile of an ascending list of times in ms, in s."""
+    i = min(len(sorted_ms) - 1, max(0, int(round(q / 100.0 * (len(sorted_ms) - 1)))))
+    return sorted_ms[i] * 1e-3
+
+
+def measured_ceilings(torch, stream):
+    """What the part delivers, from libdps_probe: a 512 MiB buffer read once
+    with 16-byte loads (plain and nontemporal; 2048 blocks of 256 threads,
+    grid-stride), and back-to-back FP16 16x16x32 / FP8 16x16x128 MFMAs on
+    register operands (2048 blocks of four waves, 8 x 512 MFMAs per wave).
+    Best of five launches each, HIP events on the launching stream."""
+    from paper_2609_34380_amd import probe
+
+    dev = torch.device("cuda:0")
+    res = {}
+    with torch.cuda.stream(stream):
+        buf = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+        buf.fill_(0x5A)
+        out = torch.empty(2048, dtype=torch.int32, device=dev)
+        facc = torch.empty(2048 * 256, dtype=torch.float32, device=dev)
+
+        def best(fn, reps=5):
+            fn()
+            ts = []
+            for _ in range(reps):
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                fn()
+                e1.record(stream)
+                e1.synchronize()
+                ts.append(e0.elapsed_time(e1) * 1e-3)
+            return min(ts)
+        for nt in (False, True):
+            t = best(lambda: probe.stream_read(buf, out, nontemporal=nt))
+            res["hbm_read_GBs_" + ("nontemporal" if nt else "plain")] = round(buf.numel() / t / 1e9, 1)
+        iters = 512
+        for fp8, key in ((0, "mfma_f16_TFLOPs"), (1, "mfma_fp8_TFLOPs")):
+            t = best(lambda: probe.mfma(fp8, iters, facc))
+            flops = 2048 * 4 * 8 * iters * probe.FLOPS_PER_MFMA[fp8]
+            res[key] = round(flops / t / 1e12, 1)
+        del buf, out, facc
+    torch.cuda.synchronize()
+    res["what"] = ("stream read: 512 MiB once, 16-byte loads, 2048 blocks x 256 threads, one "
+                   "contiguous chunk per block; MFMA loop: "
+                   "register operands, 2048 blocks x 4 waves x 4096 MFMAs; best of 5")
+    return res
+
+
 def measured_traffic(probe_call, enc):
-    """HBM bytes per launch of the dominant kernel from the committed rocprofv3
-    counter record (profiles/*_traffic.md), or None when no record matches this
-    call or the kernel sources changed since the counters were taken."""
+    """(HBM bytes per launch, record file) of the dominant kernel from the
+    committed rocprofv3 counter record (profiles/*_traffic.md), or None when no
+    record matches this call or the kernel sources changed since the counters
+    were taken."""
     import glob
     import hashlib
 
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2609_34380_amd", "csrc")
     for f in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.h"))):
+        if os.path.basename(f) == "dps_probe.hip":   # the ceiling probes, not a measured kernel
+            continue
         with open(f, "rb") as fh:
             h.update(fh.read())
     digest = h.hexdigest()
@@ -291,7 +362,7 @@ def measured_traffic(probe_call, enc):
                     rec = json.loads(line)
                     if (rec.get("probe_call") == probe_call and rec.get("csrc_sha256") == digest
                             and rec.get("encoding", "e5m2") == enc):
-                        return rec["traffic_bytes_per_launch"]
+                        return rec["traffic_bytes_per_launch"], os.path.relpath(path, ROOT)
     return None
 
 
@@ -343,7 +414,10 @@ def probe(args, torch, dps, workloads, layers, dev, stream, enc):
 
 def prefill_secondary(torch, dps, workloads, nws, layers, stream):
     """Prefill (M = 2048 and 8192) over the layer set: fast mode on FP8 matrix
-    cores (row-quantized activations), full mode on FP16 matrix cores."""
+    cores (row-quantized activations; the quantization kernel is part of each
+    call), full mode on FP16 matrix cores.  Per pass: the whole set between
+    events; per call: each call between events over the same passes
+    (median, p10, p90), with its fraction of its dtype's dense peak."""
     dev = torch.device("cuda:0")
     res = {}
     for m in (2048, 8192):
@@ -359,24 +433,43 @@ def prefill_secondary(torch, dps, workloads, nws, layers, stream):
             for label, mode, act, peak in (("fast_fp8", dps.MODE_FAST, "fp8", MFMA_FP8_TFLOPS),
                                            ("full_f16", dps.MODE_FULL, "fp16",
                                             MFMA_F16_TFLOPS)):
-                def one():
-                    for li, (name, n, k) in enumerate(layers):
-                        dps.linear(xs[k], nws[li], mode, act=act, out=ys[n], workspace=ws)
-                one()
+                def call(li):
+                    _, n, k = layers[li]
+                    dps.linear(xs[k], nws[li], mode, act=act, out=ys[n], workspace=ws)
+                for li in range(len(layers)):
+                    call(li)
                 stream.synchronize()
-                reps = 5 if m <= 2048 else 2
-                e0 = torch.cuda.Event(enable_timing=True)
-                e1 = torch.cuda.Event(enable_timing=True)
-                e0.record(stream)
-                for _ in range(reps):
-                    one()
-                e1.record(stream)
+                reps = 5 if m <= 2048 else 3
+                ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                       for _ in layers] for _ in range(reps)]
+                p0 = torch.cuda.Event(enable_timing=True)
+                p1 = torch.cuda.Event(enable_timing=True)
+                p0.record(stream)
+                for r in range(reps):
+                    for li in range(len(layers)):
+                        ev[r][li][0].record(stream)
+                        call(li)
+                        ev[r][li][1].record(stream)
+                p1.record(stream)
                 stream.synchronize()
-                t = e0.elapsed_time(e1) * 1e-3 / reps
+                t = p0.elapsed_time(p1) * 1e-3 / reps
                 flops = sum(2.0 * m * n * k for _, n, k in layers)
+                calls = []
+                for li, (name, n, k) in enumerate(layers):
+                    ts = sorted(ev[r][li][0].elapsed_time(ev[r][li][1]) for r in range(reps))
+                    tc = ts[len(ts) // 2] * 1e-3
+                    fl = 2.0 * m * n * k
+                    plan = dps.plan_info(mode, act, m, n, k)
+                    calls.append({"layer": name, "us": round(tc * 1e6, 1),
+                                  "us_p10": round(pct(ts, 10) * 1e6, 1),
+                                  "us_p90": round(pct(ts, 90) * 1e6, 1),
+                                  "TFLOPs": round(fl / tc / 1e12, 1),
+                                  "frac_of_peak": round(fl / tc / 1e12 / peak, 3),
+                                  "plan": plan})
                 res[label if m == 2048 else "%s_M%d" % (label, m)] = {
                     "M": m, "ms": round(t * 1e3, 3), "TFLOPs": round(flops / t / 1e12, 1),
-                    "frac_of_peak": round(flops / t / 1e12 / peak, 3)}
+                    "frac_of_peak": round(flops / t / 1e12 / peak, 3), "peak_TFLOPs": peak,
+                    "calls": calls}
             del xs, ys, ws
     torch.cuda.empty_cache()
     return res
@@ -410,26 +503,47 @@ def moe_secondary(torch, dps, workloads, stream, enc):
                    for _, _, _, n, k in layers for mode in (dps.MODE_FAST, dps.MODE_FULL))
         ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
         for label, mode in (("fast", dps.MODE_FAST), ("full", dps.MODE_FULL)):
-            def one():
-                for nw, x, y, _, _ in layers:
-                    dps.linear_grouped(x, off_dev, nw, mode, out=y, workspace=ws)
-            one()
+            wb = 1 if mode == dps.MODE_FAST else 2
+            for nw, x, y, _, _ in layers:
+                dps.linear_grouped(x, off_dev, nw, mode, out=y, workspace=ws)
             stream.synchronize()
             reps = 10
+            ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                   for _ in layers] for _ in range(reps)]
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
             e0.record(stream)
-            for _ in range(reps):
-                one()
+            for r in range(reps):
+                for li, (nw, x, y, _, _) in enumerate(layers):
+                    ev[r][li][0].record(stream)
+                    dps.linear_grouped(x, off_dev, nw, mode, out=y, workspace=ws)
+                    ev[r][li][1].record(stream)
             e1.record(stream)
             stream.synchronize()
             t = e0.elapsed_time(e1) * 1e-3 / reps
-            wbytes = sum(experts * n * k for _, _, _, n, k in layers) * (
-                1 if mode == dps.MODE_FAST else 2)
+            wbytes = sum(experts * n * k for _, _, _, n, k in layers) * wb
             flops = sum(2.0 * rows * n * k for _, _, _, n, k in layers)
+            calls = []
+            for li, (_, _, _, n, k) in enumerate(layers):
+                ts = sorted(ev[r][li][0].elapsed_time(ev[r][li][1]) for r in range(reps))
+                tc = ts[len(ts) // 2] * 1e-3
+                alg = wb * experts * n * k + 2 * rows * k + 2 * rows * n
+                fl = 2.0 * rows * n * k
+                bound = max(alg / (HBM_PEAK_GBS * 1e9), fl / (MFMA_F16_TFLOPS * 1e12))
+                calls.append({"layer": workloads.MOE_SHAPES[li][0], "us": round(tc * 1e6, 1),
+                              "us_p10": round(pct(ts, 10) * 1e6, 1),
+                              "us_p90": round(pct(ts, 90) * 1e6, 1),
+                              "weight_GBs": round(wb * experts * n * k / tc / 1e9, 1),
+                              "roofline_frac": round(bound / tc, 3),
+                              "bound": "hbm" if alg / (HBM_PEAK_GBS * 1e9) >= fl / (
+                                  MFMA_F16_TFLOPS * 1e12) else "mfma"})
+            ideal = sum(max((wb * experts * n * k + 2 * rows * (n + k)) / (HBM_PEAK_GBS * 1e9),
+                            2.0 * rows * n * k / (MFMA_F16_TFLOPS * 1e12))
+                        for _, _, _, n, k in layers)
             res[label] = {"ms": round(t * 1e3, 3), "GBs": round(wbytes / t / 1e9, 1),
                           "TFLOPs": round(flops / t / 1e12, 1),
-                          "frac_of_mfma_peak": round(flops / t / 1e12 / MFMA_F16_TFLOPS, 3)}
+                          "frac_of_mfma_peak": round(flops / t / 1e12 / MFMA_F16_TFLOPS, 3),
+                          "roofline_frac": round(ideal / t, 3), "calls": calls}
         del layers, ws
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
@@ -450,7 +564,7 @@ def graph_pair_secondary(torch, dps, run_call, layers, ms, stream, ms_per_step):
                 run_call(c, m, mode, li)
         pairs.append(graphs.ModeGraphs(step, ms, stream).capture())
     reps = 8
-    per_pass = {}
+    per_pass, spread = {}, {}
     for m in ms:
         for mname, mode in (("fast", dps.MODE_FAST), ("full", dps.MODE_FULL)):
             evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -462,9 +576,12 @@ def graph_pair_secondary(torch, dps, run_call, layers, ms, stream, ms_per_step):
             stream.synchronize()
             ts = sorted(a.elapsed_time(b) for a, b in evs)
             per_pass["M%d_%s" % (m, mname)] = round(ts[len(ts) // 2] * 1e3, 2)
+            spread["M%d_%s" % (m, mname)] = [round(pct(ts, 10) * 1e6, 2),
+                                             round(pct(ts, 90) * 1e6, 2)]
     total_us = sum(per_pass.values())
     del pairs
-    return {"pass_us": per_pass, "sum_of_passes_ms": round(total_us / 1e3, 4),
+    return {"pass_us": per_pass, "pass_us_p10_p90": spread,
+            "sum_of_passes_ms": round(total_us / 1e3, 4),
             "single_graph_step_ms": round(ms_per_step, 4)}
 
 
@@ -591,23 +708,32 @@ def restore_secondary(torch, dps, workloads, stream, enc):
     def ev():
         return torch.cuda.Event(enable_timing=True)
 
-    # restore alone (after one warm-up pass)
-    with torch.cuda.stream(copy):
-        restore_all()
-    copy.synchronize()
-    reps = 3
-    e0, e1 = ev(), ev()
-    with torch.cuda.stream(copy):
-        e0.record(copy)
-        for _ in range(reps):
+    # restore alone (after one warm-up pass): each pass between events on the
+    # copy stream, and the host time spent enqueueing its copies
+    def restore_alone(reps=3):
+        with torch.cuda.stream(copy):
             restore_all()
-        e1.record(copy)
-    copy.synchronize()
-    t_restore = e0.elapsed_time(e1) * 1e-3 / reps
+        copy.synchronize()
+        evs = [(ev(), ev()) for _ in range(reps)]
+        enq = []
+        with torch.cuda.stream(copy):
+            for a, b in evs:
+                a.record(copy)
+                h0 = time.perf_counter()
+                restore_all()
+                enq.append(time.perf_counter() - h0)
+                b.record(copy)
+        copy.synchronize()
+        ts = sorted(a.elapsed_time(b) * 1e-3 for a, b in evs)
+        return ts[len(ts) // 2], ts, max(enq)
+
+    t_restore, restore_passes, enqueue_max = restore_alone()
 
     # a plain pinned host -> device copy of 256 MiB (the copy engines' rate)
     src = torch.empty(256 << 20, dtype=torch.uint8, pin_memory=True)
     dst = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+    reps = 3
+    e0, e1 = ev(), ev()
     with torch.cuda.stream(copy):
         dst.copy_(src, non_blocking=True)
         e0.record(copy)
@@ -639,12 +765,21 @@ def restore_secondary(torch, dps, workloads, stream, enc):
     def med(v):
         v = sorted(v)
         return v[len(v) // 2]
-    alternating = {
-        "fast_ms_median": round(med(per_mode[dps.MODE_FAST]) * 1e3, 4),
-        "full_ms_median": round(med(per_mode[dps.MODE_FULL]) * 1e3, 4),
-        "fast_GBs": round(wbytes / med(per_mode[dps.MODE_FAST]) / 1e9, 1),
-        "full_GBs": round(2 * wbytes / med(per_mode[dps.MODE_FULL]) / 1e9, 1),
-        "steps": len(seq)}
+    def roof(mode, t):
+        wb = 1 if mode == dps.MODE_FAST else 2
+        alg = sum(wb * n * k + 2 * m * (n + k) for _, n, k in layers)
+        return round(alg / (HBM_PEAK_GBS * 1e9) / t, 3)
+
+    alternating = {"steps": len(seq)}
+    for mode, key in ((dps.MODE_FAST, "fast"), (dps.MODE_FULL, "full")):
+        ts = sorted(v * 1e3 for v in per_mode[mode])
+        t = med(per_mode[mode])
+        alternating.update({
+            key + "_ms_median": round(t * 1e3, 4),
+            key + "_ms_p10": round(pct(ts, 10) * 1e3, 4),
+            key + "_ms_p90": round(pct(ts, 90) * 1e3, 4),
+            key + "_GBs": round((1 if mode == dps.MODE_FAST else 2) * wbytes / t / 1e9, 1),
+            key + "_roofline_frac": roof(mode, t)})
 
     # fast-mode decode alone
     steps = 40
@@ -680,11 +815,19 @@ def restore_secondary(torch, dps, workloads, stream, enc):
     inside = [a.elapsed_time(b) * 1e-3 for a, b in step_ev
               if start.elapsed_time(b) * 1e-3 <= t_r_conc]
     t_step_conc = sum(inside) / len(inside) if inside else None
+    # restore alone once more, after the concurrent run
+    t_restore2, restore_passes2, enqueue_max2 = restore_alone()
     return {"workload": "decode_h8192_scattered, fast mode, M=%d" % m,
             "encoding": "e4m3" if enc == dps.ENC_E4M3 else "e5m2",
             "residual_bytes": total, "chunk_bytes": 1 << log2c, "copy_bytes": dps.COPY_BYTES,
             "restore_ms": round(t_restore * 1e3, 3),
             "restore_GBs": round(total / t_restore / 1e9, 1),
+            "restore_pass_ms": [round(v * 1e3, 3) for v in restore_passes],
+            "restore_enqueue_ms_max": round(enqueue_max * 1e3, 3),
+            "restore_ms_again": round(t_restore2 * 1e3, 3),
+            "restore_GBs_again": round(total / t_restore2 / 1e9, 1),
+            "restore_pass_ms_again": [round(v * 1e3, 3) for v in restore_passes2],
+            "restore_enqueue_ms_max_again": round(enqueue_max2 * 1e3, 3),
             "plain_h2d_GBs": round((256 << 20) / t_plain / 1e9, 1),
             "decode_step_ms": round(t_step * 1e3, 4),
             "decode_step_ms_during_restore": (round(t_step_conc * 1e3, 4)
@@ -726,32 +869,160 @@ def sum_secondary(dps):
             "residuals_evicted": evicted, "binding": "python ctypes"}
 
 
+def _host_cpu():
+    """CPU model and the cores this process may run on."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:
+        usable = os.cpu_count()
+    return {"cpu_model": model, "nproc": usable, "os_cpu_count": os.cpu_count()}
+
+
 def cpu_baseline(workloads):
-    """The CPU oracle on a bounded sample of the same workload: the O layer
-    (4096x4096) at every M in {1, 8, 32, 128, 256}, fast and full mode."""
+    """The CPU oracle as it stands, on bounded samples of each workload, on the
+    host cores (OpenMP over output features).  `value` is the sample of the
+    timed workload (the hidden-4096 decode set: the O layer at every M, both
+    modes); `per_config` holds one sample per workload in that workload's own
+    unit, and the single-layer case is timed on one core as well.  Each
+    sample repeats until a few seconds have passed (about 20 s in all);
+    `seconds` is the time of one pass over the sample."""
     import numpy as np
 
     import oracle
 
+    def residual(n_words, log2c, slots=None):
+        c = 1 << log2c
+        n_chunks = -(-n_words // c)
+        if slots is None:
+            slots = np.arange(n_chunks, dtype=np.int32)
+        pool = np.zeros((int(slots.max()) + 1) * c, np.uint8)
+        return oracle.Residual(pool, slots, log2c)
+
+    def bits(t):
+        return t.numpy().view(np.uint16)
+
+    def timed(fn, min_s=2.5):
+        """Seconds per run of fn, repeated until min_s of CPU time have passed."""
+        t0 = time.perf_counter()
+        runs = 0
+        while True:
+            fn()
+            runs += 1
+            t = time.perf_counter() - t0
+            if t >= min_s:
+                return t / runs
+
+    cores = oracle.num_threads()
+    per = {}
+    t_all = time.perf_counter()
+
+    # single layer 1024 x 1024, M = 4, 64 KiB chunks (identity table): all
+    # cores and one core; GB/s of weight-plane bytes (fast N*K + full 2*N*K)
+    n = k = 1024
+    w = bits(workloads.weight_fp16(n, k, seed=11))
+    r = residual(n * k, 16)
+    hi = oracle.split(w, r)
+    x = bits(workloads.activations_fp16(4, k, seed=12))
+    reps = 10
+
+    def pair_reps():
+        for _ in range(reps):
+            oracle.linear(oracle.FAST, x, hi)
+            oracle.linear(oracle.FULL, x, hi, r)
+    t = timed(pair_reps, 1.0)
+    prev = oracle.set_num_threads(1)
+    try:
+        t1 = timed(pair_reps, 2.0)
+    finally:
+        oracle.set_num_threads(prev)
+    per["single_1024"] = {"value": round(3 * n * k * reps / t / 1e9, 4), "unit": "GB/s",
+                          "cores": cores, "seconds": round(t, 3),
+                          "one_core": {"value": round(3 * n * k * reps / t1 / 1e9, 4),
+                                       "unit": "GB/s", "cores": 1, "seconds": round(t1, 3)},
+                          "sample": "the whole workload, fast + full"}
+
+    # hidden-4096 decode set: the O layer at every M, both modes
     n = k = 4096
-    w = workloads.weight_fp16(n, k, seed=77).numpy().view(np.uint16)
-    c = 1 << LOG2_CHUNK
-    n_chunks = -(-n * k // c)
-    res = oracle.Residual(np.zeros(n_chunks * c, np.uint8), np.arange(n_chunks, dtype=np.int32),
-                          LOG2_CHUNK)
-    hi = oracle.split(w, res)
-    t0 = time.perf_counter()
-    wbytes = 0
-    for m in workloads.DECODE_M:
-        x = workloads.activations_fp16(m, k, seed=m).numpy().view(np.uint16)
-        oracle.linear(oracle.FAST, x, hi, None)
-        oracle.linear(oracle.FULL, x, hi, res)
-        wbytes += n * k * 3
-    t = time.perf_counter() - t0
-    return {"value": round(wbytes / t / 1e9, 4), "unit": "GB/s", "cores": oracle.num_threads(),
-            "kind": "oracle", "seconds": round(t, 2),
-            "sample": "O layer 4096x4096 at M in {1,8,32,128,256}, fast and full mode "
-                      "(fp64 oracle, OpenMP over output features)"}
+    w = bits(workloads.weight_fp16(n, k, seed=77))
+    r = residual(n * k, LOG2_CHUNK)
+    hi = oracle.split(w, r)
+    xs = [bits(workloads.activations_fp16(m, k, seed=m)) for m in workloads.DECODE_M]
+
+    def decode_sample():
+        for x in xs:
+            oracle.linear(oracle.FAST, x, hi)
+            oracle.linear(oracle.FULL, x, hi, r)
+    t = timed(decode_sample, 6.0)
+    wbytes = 3 * n * k * len(xs)
+    per["decode_h4096"] = {"value": round(wbytes / t / 1e9, 4), "unit": "GB/s", "cores": cores,
+                           "seconds": round(t, 3),
+                           "sample": "O layer 4096x4096 at M in {1,8,32,128,256}, fast and full"}
+
+    # hidden-4096 prefill: 64 of the 2048 rows (1% outlier channels x20) on
+    # the O layer; fast = row quantization + FP8 product, full = FP16 product
+    x = bits(workloads.activations_fp16(64, k, seed=k + 5, outlier_frac=0.01, outlier_scale=20.0))
+
+    def fast_fp8():
+        xq, s = oracle.act_quant(x)
+        oracle.linear_fp8(xq, s, hi)
+    tf = timed(fast_fp8)
+    tu = timed(lambda: oracle.linear(oracle.FULL, x, hi, r))
+    fl = 2.0 * 64 * n * k
+    per["prefill_h4096"] = {"fast_fp8": {"value": round(fl / tf / 1e12, 6), "seconds": round(tf, 3)},
+                            "full_f16": {"value": round(fl / tu / 1e12, 6), "seconds": round(tu, 3)},
+                            "unit": "TFLOP/s", "cores": cores,
+                            "sample": "O layer 4096x4096, 64 rows of the 2048-token batch"}
+
+    # grouped MoE: the down projection (4096 x 14336) of two of the 8 experts,
+    # 4 routed rows each (every expert costs the oracle the same)
+    e, n, k = 2, 4096, 14336
+    w = bits(workloads.weight_fp16(n, k, seed=910, experts=e))
+    r = residual(e * n * k, LOG2_CHUNK)
+    hi = oracle.split(w, r)
+    offs = np.arange(0, 4 * e + 1, 4, dtype=np.int64)
+    x = bits(workloads.activations_fp16(4 * e, k, seed=921))
+    tf = timed(lambda: oracle.linear_grouped(oracle.FAST, x, offs, hi))
+    tu = timed(lambda: oracle.linear_grouped(oracle.FULL, x, offs, hi, r))
+    per["moe_8x4096x14336"] = {"fast": {"value": round(e * n * k / tf / 1e9, 4),
+                                        "seconds": round(tf, 3)},
+                               "full": {"value": round(2 * e * n * k / tu / 1e9, 4),
+                                        "seconds": round(tu, 3)},
+                               "unit": "GB/s", "cores": cores,
+                               "sample": "down projection of 2 experts, 4 routed rows each"}
+
+    # hidden-8192 set with scattered 2 MiB chunks: the O layer at M = 8
+    n = k = 8192
+    n_chunks = workloads.n_chunks_for(n * k, LOG2_CHUNK)
+    slots = workloads.chunk_slots(n_chunks, 2 * n_chunks, seed=501).numpy()
+    w = bits(workloads.weight_fp16(n, k, seed=601))
+    r = residual(n * k, LOG2_CHUNK, slots)
+    hi = oracle.split(w, r)
+    x = bits(workloads.activations_fp16(8, k, seed=k))
+    tf = timed(lambda: oracle.linear(oracle.FAST, x, hi))
+    tu = timed(lambda: oracle.linear(oracle.FULL, x, hi, r))
+    per["decode_h8192_scattered"] = {"fast": {"value": round(n * k / tf / 1e9, 4),
+                                              "seconds": round(tf, 3)},
+                                     "full": {"value": round(2 * n * k / tu / 1e9, 4),
+                                              "seconds": round(tu, 3)},
+                                     "unit": "GB/s", "cores": cores,
+                                     "sample": "O layer 8192x8192 at M=8, chunks at random "
+                                               "slots of a pool twice the residual's size"}
+
+    head = per["decode_h4096"]
+    out = {"value": head["value"], "unit": "GB/s", "cores": cores, "kind": "oracle",
+           "seconds": head["seconds"], "sample": head["sample"] + " (fp64 oracle)",
+           "total_seconds": round(time.perf_counter() - t_all, 2), "per_config": per}
+    out.update(_host_cpu())
+    return out
 
 
 if __name__ == "__main__":

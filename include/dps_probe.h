@@ -1,0 +1,38 @@
+/*
+ * dps_probe.h -- measured ceilings of the MI355X units the nested linear
+ * layer is bound by (HBM streaming, FP16 and FP8 matrix cores), so roofline
+ * fractions can be stated against what the part delivers as well as against
+ * its published peaks.  A separate library (libdps_probe.so), not part of the
+ * nested-linear boundary in dps.h.
+ *
+ * Both calls enqueue one kernel on `stream` (a hipStream_t) and return 0, or
+ * 1 for a bad argument (nothing enqueued), or 5 if the launch failed.  Time
+ * them with events around the enqueued work.
+ */
+#ifndef DPS_PROBE_H
+#define DPS_PROBE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Read every byte of buf once with 16-byte loads (1 KiB per wave
+ * instruction; nontemporal != 0: nontemporal loads) over `blocks` blocks of
+ * 256 threads, block b over the b-th of `blocks` equal contiguous chunks.  buf: device, 16-byte aligned, bytes a positive
+ * multiple of 16.  out: device uint32[blocks], one folded word per block. */
+int dps_probe_stream_read(const void *buf, int64_t bytes, int nontemporal, uint32_t *out,
+                          int64_t blocks, void *stream);
+
+/* `blocks` blocks of four waves, each wave issuing 8 * iters MFMAs on
+ * register operands (fp8 == 0: v_mfma_f32_16x16x32_f16, 16384 flops each;
+ * fp8 != 0: v_mfma_f32_16x16x128_f8f6f4 with E4M3 operands, 65536 flops
+ * each).  out: device float[blocks * 256]. */
+int dps_probe_mfma(int fp8, int iters, int64_t blocks, float *out, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DPS_PROBE_H */

@@ -69,6 +69,8 @@ def _load():
     lib.oracle_linear_fp8.restype = ctypes.c_int
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
+    lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
+    lib.oracle_set_num_threads.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -265,3 +267,8 @@ def linear_fp8(xq, scale, hi, enc=E5M2):
 
 def num_threads():
     return _load().oracle_num_threads()
+
+
+def set_num_threads(n):
+    """Threads the linear routines use from now on; returns the previous count."""
+    return _load().oracle_set_num_threads(int(n))

@@ -539,3 +539,16 @@ int oracle_num_threads(void)
     return 1;
 #endif
 }
+
+/* Threads the linear routines run on from now on (n >= 1); returns the
+ * previous count.  Only the benchmark's CPU baseline changes it, to time the
+ * oracle on one core as well as on all of them.                          */
+int oracle_set_num_threads(int n)
+{
+    int prev = oracle_num_threads();
+#ifdef _OPENMP
+    if (n >= 1)
+        omp_set_num_threads(n);
+#endif
+    return prev;
+}

@@ -1,8 +1,9 @@
-"""Build libdps.so (HIP kernels + C ABI) for gfx950 with hipcc.
+"""Build libdps.so (HIP kernels + C ABI) and libdps_probe.so (the ceiling
+probes the benchmark measures against) for gfx950 with hipcc.
 
 Usage: python -m paper_2609_34380_amd.csrc.build  (or build() from Python).
-Objects go to paper_2609_34380_amd/_build/, the library to
-paper_2609_34380_amd/libdps.so.
+Objects go to paper_2609_34380_amd/_build/, the libraries to
+paper_2609_34380_amd/.
 """
 import concurrent.futures as cf
 import os
@@ -15,6 +16,8 @@ ROOT = os.path.dirname(PKG)
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libdps.so")
+PROBE_LIB = os.path.join(PKG, "libdps_probe.so")
+PROBE_SOURCES = ["dps_probe.hip"]
 SOURCES = ["dps_elementwise.hip", "dps_skinny.hip", "dps_gemv.hip", "dps_rows.hip", "dps_gemm.hip",
            "dps_restore.hip", "dps_api.hip", "dps_sum.cpp"]
 ARCH = "gfx950"
@@ -33,7 +36,7 @@ CFLAGS = [
 # in a streaming or matrix-core kernel adds memory traffic beside the weight
 # stream and costs time with no error, so the build fails on it instead.
 NO_SCRATCH = {"dps_elementwise.hip", "dps_skinny.hip", "dps_gemv.hip", "dps_rows.hip",
-              "dps_gemm.hip"}
+              "dps_gemm.hip", "dps_probe.hip"}
 
 
 def _scratch_users(report):
@@ -67,12 +70,22 @@ def _compile(src):
     return src, obj, rc, out, cmd
 
 
+def _link(objs, lib, verbose):
+    tmp = lib + ".tmp%d" % os.getpid()
+    cmd = [HIPCC, "-shared", "-fPIC", "--offload-arch=" + ARCH, *objs, "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, lib)
+
+
 def build(verbose=False, jobs=None):
     os.makedirs(BUILD_DIR, exist_ok=True)
-    jobs = jobs or min(len(SOURCES), max(1, (os.cpu_count() or 2) // 2))
-    objs = []
+    every = SOURCES + PROBE_SOURCES
+    jobs = jobs or min(len(every), max(1, (os.cpu_count() or 2) // 2))
+    objs = {}
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
-        for src, obj, rc, out, cmd in ex.map(_compile, SOURCES):
+        for src, obj, rc, out, cmd in ex.map(_compile, every):
             if verbose:
                 print(" ".join(cmd), flush=True)
             if rc != 0:
@@ -80,13 +93,9 @@ def build(verbose=False, jobs=None):
                 raise RuntimeError("hipcc failed on %s" % src)
             if out.strip() and verbose:
                 sys.stderr.write(out)
-            objs.append(obj)
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [HIPCC, "-shared", "-fPIC", "--offload-arch=" + ARCH, *objs, "-o", tmp]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
+            objs[src] = obj
+    _link([objs[s] for s in SOURCES], LIB, verbose)
+    _link([objs[s] for s in PROBE_SOURCES], PROBE_LIB, verbose)
     return LIB
 
 

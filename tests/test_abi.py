@@ -231,3 +231,28 @@ def test_grouped_grid_limit_uses_the_planned_token_tile(lib):
                                 None)
     assert st == 3, st
     assert b"too many rows" in lib.dps_last_error()
+
+
+def test_probe_library_exports_its_header():
+    """libdps_probe.so (the ceiling probes the benchmark states fractions
+    against) exports exactly what include/dps_probe.h declares, and rejects
+    bad arguments on the host with nothing enqueued."""
+    from paper_2609_34380_amd import probe
+
+    text = open(os.path.join(ROOT, "include", "dps_probe.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    declared = set(re.findall(r"\b(dps_probe_[a-z0-9_]+)\s*\(", text))
+    assert declared == set(probe.EXPORTED)
+    if not os.path.exists(probe.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    plib = probe.load_library()
+    for name in declared:
+        assert hasattr(plib, name), name
+    # NULL buffer, misaligned size, zero blocks: status 1
+    assert plib.dps_probe_stream_read(None, 1024, 0, 0x1000, 4, None) == 1
+    assert plib.dps_probe_stream_read(0x1000, 1000, 0, 0x2000, 4, None) == 1
+    assert plib.dps_probe_stream_read(0x1000, 1024, 0, 0x2000, 0, None) == 1
+    assert plib.dps_probe_mfma(0, 0, 4, 0x1000, None) == 1
+    assert plib.dps_probe_mfma(1, 8, 0, 0x1000, None) == 1
+    assert plib.dps_probe_mfma(0, 8, 4, None, None) == 1

@@ -24,3 +24,15 @@ def test_multi_rank_launch_is_refused():
     r = _run([], {"WORLD_SIZE": "2"})
     assert r.returncode == 2
     assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_percentile_helper_is_nearest_rank():
+    sys.path.insert(0, ROOT)
+    import bench
+
+    ts = [1.0, 2.0, 3.0, 4.0, 5.0, 6.0, 7.0, 8.0, 9.0, 10.0, 11.0]
+    assert bench.pct(ts, 0) == 1.0e-3
+    assert bench.pct(ts, 50) == 6.0e-3
+    assert bench.pct(ts, 90) == 10.0e-3
+    assert bench.pct(ts, 100) == 11.0e-3
+    assert bench.pct([4.0], 10) == 4.0e-3
