@@ -252,13 +252,30 @@ LinearPlan plan_linear(int mode, uint32_t flags, int64_t rows, int64_t n, int64_
                      (n * k <= (int64_t(1) << 24) && rows_per_expert <= 256))
                         ? GEMM_G4_128x32
                         : (rows_per_expert <= 64 ? GEMM_G4S_128x64 : GEMM_G4S_128x128);
-        const int64_t waves_per_block = 8;
+        // Dense prefill-sized calls take the 256 x 256 tile when it fills the
+        // chip (at least one block per CU), or fills it with two K ranges and
+        // K is long enough (>= 8192) for them to pay for their fp32 partials.
+        // MI355X, hidden-4096 set, full mode: gate+up at 1024 / 2048 tokens
+        // 318 / 619 against 345 / 669 us, down at 2048 tokens (two ranges)
+        // 284 against 302, every layer at 8192 tokens 0.82-0.92x the time
+        // (gate+up 1962 against 2340 us).  Slower on it: QKV and O at 2048
+        // tokens (192 and 128 tiles, 4-5%), down at 512 / 1024 tokens (8 / 4
+        // ranges: 89 / 161 against 80 / 154 us) and every decode call up to
+        // 256 tokens (gate+up at 256 tokens 93 against 88 us).
+        if (!grouped && rows >= 512) {
+            const int64_t t5 = cdiv(n, 256) * cdiv(rows, 256);
+            if (t5 >= cu_count || (k >= 8192 && 2 * t5 >= cu_count))
+                p.variant = GEMM_G5_256x256;
+        }
+        const bool g5 = p.variant == GEMM_G5_256x256;
         const int64_t tiles =
             cdiv(n, gemm_rows_per_block(p.variant)) * cdiv(rows, gemm_tokens_per_block(p.variant));
-        int64_t s = (8 * (int64_t)cu_count / waves_per_block) / tiles;
+        // the 256-row tiles hold one block per CU (160 KiB of LDS); the
+        // wide-row GEMM's eight waves share a CU with others
+        int64_t s = (int64_t)cu_count / tiles;
         const int64_t smax = k / 1024 > 1 ? k / 1024 : 1;
         s = s < 1 ? 1 : (s > smax ? smax : s);
-        p.ksplit = round_up(cdiv(k, s), 128);
+        p.ksplit = round_up(cdiv(k, s), g5 ? 64 : 128);
         p.splits = (int)cdiv(k, p.ksplit);
     }
     p.range_addr = mode == MODE_FULL && p.ksplit <= (int64_t(1) << log2c);

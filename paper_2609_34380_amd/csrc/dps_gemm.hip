@@ -677,6 +677,305 @@ __global__ __launch_bounds__(SPEC ? 768 : 512) void gemm4_kernel(GemmArgs a)
     }
 }
 
+// ------------------------------------------------------------------------------
+// Large-tile LDS-DMA GEMM, FP16 full/fast: 256 weight rows, 64-element stages
+// ------------------------------------------------------------------------------
+// The wide-row GEMM above is bound by its LDS traffic: a 128 x 128 tile
+// fills 64 KiB of LDS per 128-element stage for 1024 MFMA cycles per SIMD,
+// and its 64 x 64 wave tiles read 16 KiB of fragments per wave per stage.
+// This kernel takes 256 weight rows x BM tokens per block (dense calls; the
+// planner launches BM = 256) with eight waves in a 2 x 4 grid, each over a
+// 128 x BM/4 wave tile on the whole K range of every stage: per FP16 flop it fills half the LDS bytes
+// (256 x 256) and reads 0.75x the fragment bytes (12 of 16 per 32 MFMAs at
+// BM = 256) of the 128 x 128 tile, and it does twice the matrix work between
+// two barriers.
+//
+// A stage is 64 K elements.  A DMA instruction fills 1 KiB of LDS: 8 weight
+// lines of 128 bytes (full mode: 8 rows x (64 upper + 64 residual bytes);
+// fast mode: 16 rows x 64 upper bytes) or 8 token rows of 128 bytes.  The
+// 16-byte chunks sit at swizzled slots (see the weight-line and token-row
+// notes below) so that the 16 rows of every fragment read land in distinct
+// bank groups.  Lane (i, g) reads the 16-byte chunk holding K 16g .. 16g+15
+// of weight row i (both MFMA steps s, bytes 8s .. 8s+7 merged into FP16) and
+// the chunk holding K 16g+8s .. +7 of token i: both operands of every MFMA
+// pair the same K elements.  All eight waves issue their share of the
+// direct-to-LDS loads after the stage barrier; the counter scheme is the
+// wide-row GEMM's (weights and tokens in separate rings of WS and XS slots,
+// XS <= WS, exact vmcnt waits).
+template <int MODE, int BM, int WS, int XS>
+struct G5 {
+    static constexpr int PLANES = MODE == MODE_FULL ? 2 : 1;
+    static constexpr int BN = 256;
+    static constexpr int BK = 64;
+    static constexpr int W_SLOT = BN * BK * PLANES;     // 128-byte weight lines
+    static constexpr int X_SLOT = BM * BK * 2;          // BM rows x 128 bytes
+    static constexpr int X_BASE = W_SLOT * WS;
+    static constexpr int LDS = X_BASE + XS * X_SLOT;
+    static constexpr int NW = W_SLOT / 1024 / 8;        // weight instructions per wave per stage
+    static constexpr int NX = X_SLOT / 1024 / 8;
+    static constexpr int OUTSTANDING = (XS < WS ? NW : 0) + (XS - 2) * (NX + NW);
+    static constexpr int TM = BM / 4;                   // tokens per wave
+    static constexpr int MT = TM / 16;
+    static_assert(WS >= 2 && XS >= 2 && XS <= WS, "ring depths of the counter scheme");
+    static_assert(OUTSTANDING <= 63, "vmcnt range");
+    static_assert(BM == 256 || BM == 128, "token tile");
+    static_assert(NW >= 1 && NX >= 1, "DMA split over the waves");
+    static_assert(LDS <= 160 * 1024, "LDS");
+};
+
+// Weight lines: 128 bytes, 16-byte slots at slot chunk ^ swz8(line).  Full
+// mode: line r holds weight row r, its upper bytes in chunks 0-3 and its
+// residual bytes in chunks 4-7 (16 K elements each).  Fast mode: line
+// 16t + i holds row 32t + i in chunks 0-3 and row 32t + 16 + i in chunks 4-7.
+// Either way a fragment read -- lane (i, g) of 16 lines reading chunk 4q + g
+// -- is the pattern measured conflict-free on MI355X (ds_read_b128 at ~210
+// B/clk per CU), where 64-byte rows read whole lose half the rate to bank
+// conflicts.
+// Token rows: K chunk c (8 elements) of a 128-byte row sits at slot
+// sigma(c) ^ swz8(row), sigma(c) = (c >> 1) | (c & 1) << 2, so the chunks
+// 2g + s that lane group g reads in MFMA step s are slots (g + 4s) ^ swz8:
+// four consecutive slots per step.  Reading chunks 2g + s through the plain
+// swizzle costs LDS bank conflicts on MI355X (rocprofv3 SQ_LDS_BANK_CONFLICT
+// about half of the LDS active cycles); tok_chunk is sigma's inverse, the K
+// chunk the DMA writes into a slot.
+__device__ __forceinline__ int tok_chunk(int slot) { return ((slot & 3) << 1) | (slot >> 2); }
+
+template <int MODE, int ENC, int BM, int WS, int XS, bool RANGE>
+__global__ __launch_bounds__(512) void gemm5_kernel(GemmArgs a)
+{
+    using C = G5<MODE, BM, WS, XS>;
+    __shared__ __attribute__((aligned(16))) uint8_t smem[C::LDS];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int li = lane & 15;
+    const int lg = lane >> 4;
+    const int wn = wave & 1;   // 128-row half of the weight tile
+    const int wm = wave >> 1;  // BM/4-token quarter of the token tile
+
+    // 1-D grid remapped for the 8 XCDs (block L runs on XCD L % 8): XCD x
+    // takes the tile range [x * per_xcd, (x+1) * per_xcd), walked in groups
+    // of four weight tiles with the weight tile fastest, so the ~32 blocks
+    // resident on an XCD share 4 weight tiles and 8 token tiles through its L2.
+    const int64_t mtiles = (a.rows + BM - 1) / BM;
+    const int64_t ntiles = (a.n + C::BN - 1) / C::BN;
+    const int64_t total = mtiles * ntiles * a.splits;
+    const int64_t per_xcd = (total + 7) / 8;
+    const int64_t lin = blockIdx.x;
+    const int64_t tl = (lin % 8) * per_xcd + lin / 8;
+    if (tl >= total)
+        return;
+    constexpr int64_t G = 4;
+    const int s = (int)(tl / (mtiles * ntiles));
+    const int64_t rr = tl % (mtiles * ntiles);
+    const int64_t chunk = rr / (G * mtiles);
+    const int64_t within = rr % (G * mtiles);
+    const int64_t gc = ntiles - chunk * G < G ? ntiles - chunk * G : G;
+    const int ntile = (int)(chunk * G + within % gc);
+    const int64_t e = 0;
+    const int64_t mrow0 = (within / gc) * BM;
+    const int64_t mrow1 = mrow0 + BM < a.rows ? mrow0 + BM : a.rows;
+    const int64_t n0 = (int64_t)ntile * C::BN;
+    const int64_t kb0 = (int64_t)s * a.ksplit;
+    const int64_t ke = kb0 + a.ksplit < a.k ? kb0 + a.ksplit : a.k;
+    const int64_t ntk = ke > kb0 ? (ke - kb0 + C::BK - 1) / C::BK : 0;
+
+    // ---- per-lane DMA state (fixed across stages) ------------------------------
+    // weight instruction j: lines 8j .. 8j+7, lane -> line 8j + lane/8, slot
+    // lane%8 = chunk c ^ swz8(line): K chunk c & 3 of the upper bytes (full
+    // mode c < 4, fast mode any c) or of the residual (full mode c >= 4).
+    // Stage t of the lane's piece starts at p0 + 64 t, or for a residual piece
+    // past the row range's chunk boundary (stages >= tsw) at p1 + 64 t.
+    const uint8_t *p0[C::NW], *p1[C::NW];
+    int64_t wlog[C::NW];
+    int wlim[C::NW], tsw[C::NW];
+    bool lo[C::NW], ok0[C::NW], ok1[C::NW];
+#pragma unroll
+    for (int jj = 0; jj < C::NW; ++jj) {
+        const int j = wave * C::NW + jj;
+        const int line = 8 * j + (lane >> 3);
+        const int c = (lane & 7) ^ swz8(line);
+        const int r = MODE == MODE_FULL ? line : (2 * (line >> 4) + (c >> 2)) * 16 + (line & 15);
+        int64_t nr = n0 + r;
+        nr = nr < a.n ? nr : a.n - 1;
+        const int wel = (c & 3) * 16;
+        const int64_t wl = (e * a.n + nr) * a.k;
+        lo[jj] = MODE == MODE_FULL && c >= 4;
+        p0[jj] = p1[jj] = a.hi + wl + kb0 + wel;
+        wlim[jj] = (int)(ke - kb0 - wel);
+        wlog[jj] = wl + kb0 + wel;
+        tsw[jj] = 0;
+        ok0[jj] = ok1[jj] = true;
+        if (lo[jj]) {
+            p0[jj] = p1[jj] = a.res.pool;
+            ok0[jj] = ok1[jj] = false;
+            if (RANGE && ke > kb0) {
+                const RangeResidual rr = range_residual(a.res, wl + kb0, wl + ke);
+                p0[jj] = a.res.pool + rr.delta0 + wlog[jj];
+                p1[jj] = a.res.pool + rr.delta1 + wlog[jj];
+                ok0[jj] = rr.ok0;
+                ok1[jj] = rr.ok1;
+                const int64_t d = rr.bnd - wlog[jj];  // first stage at or past the chunk boundary
+                tsw[jj] = d <= 0 ? 0 : (int)((d + C::BK - 1) / C::BK);
+            }
+        }
+    }
+    // token instruction j: rows 8j .. 8j+7, lane -> row 8j + lane/8, slot
+    // lane%8.  The wave's rows are 8 apart from one instruction to the next,
+    // so one row pointer serves them all (rows past the tile's last token
+    // load zeros); the swizzled K offset alternates with the instruction's
+    // parity.
+    const int xr0 = 8 * wave * C::NX + (lane >> 3);
+    const uint16_t *xp0 = static_cast<const uint16_t *>(a.x) + (mrow0 + xr0) * a.k + kb0;
+    int xel[2];
+#pragma unroll
+    for (int par = 0; par < 2; ++par)
+        xel[par] = tok_chunk((lane & 7) ^ swz8(xr0 + 8 * par)) * 8;
+    const int64_t t_full = (ke - kb0) / C::BK;  // stages entirely inside the K range
+    // K walk rotated per group of four weight tiles (rows a multiple of 4 KiB
+    // apart would otherwise put every block on the same address bits at once)
+    const int64_t grot = a.rotate && ntk > 0 ? (int64_t)(ntile >> 2) % ntk : 0;
+    auto tk = [&](int64_t t) {
+        return t < ntk ? (t + grot < ntk ? t + grot : t + grot - ntk) : t;
+    };
+
+    auto issue_w = [&](int64_t t) {
+        uint8_t *st = smem + (int)(t % WS) * C::W_SLOT;
+        const int64_t tr = tk(t);
+        const bool masked = tr >= t_full;
+        const int64_t off = tr * C::BK;
+#pragma unroll
+        for (int jj = 0; jj < C::NW; ++jj) {
+            const int j = wave * C::NW + jj;
+            const bool ok = !masked || off < wlim[jj];
+            const void *src = g_zero16;
+            if (!lo[jj] || RANGE) {
+                const bool second = tr >= tsw[jj];
+                if (ok && (second ? ok1[jj] : ok0[jj]))
+                    src = (second ? p1[jj] : p0[jj]) + off;
+            } else {
+                const int64_t o = residual_offset(a.res, wlog[jj] + (ok ? off : 0));
+                if (ok && o >= 0)
+                    src = a.res.pool + o;
+            }
+            dma16(src, st + j * 1024);
+        }
+    };
+    auto issue_x = [&](int64_t t) {
+        uint8_t *st = smem + C::X_BASE + (int)(t % XS) * C::X_SLOT;
+        const int64_t tr = tk(t);
+        const bool masked = tr >= t_full;
+        const int64_t off = tr * C::BK;
+#pragma unroll
+        for (int jj = 0; jj < C::NX; ++jj) {
+            const int j = wave * C::NX + jj;
+            const int xe = xel[jj & 1];
+            const bool ok = (mrow0 + xr0 + 8 * jj < mrow1) &&
+                            (!masked || off + xe < ke - kb0);
+            dma16(ok ? (const void *)(xp0 + (int64_t)(8 * jj) * a.k + off + xe)
+                     : (const void *)g_zero16,
+                  st + j * 1024);
+        }
+    };
+
+    f32x4 acc[8][C::MT];
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < C::MT; ++j)
+            acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // fragment offsets: the swizzles depend on the low bits of the line or
+    // row only, which every 16-line tile shares with the lane's li.  Row
+    // tile nt of the wave: full mode upper bytes at aoff + 2048 nt, residual
+    // 64 bytes further in the swizzled line (aoff_lo); fast mode at
+    // aoff_f[nt & 1] + 2048 (nt >> 1).
+    const int aoff = (wn * 128 + li) * 128 + ((lg ^ swz8(li)) << 4);
+    const int aoff_lo = (wn * 128 + li) * 128 + (((4 + lg) ^ swz8(li)) << 4);
+    int aoff_f[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+        aoff_f[q] = (wn * 64 + li) * 128 + (((4 * q + lg) ^ swz8(li)) << 4);
+    int boff[2];
+#pragma unroll
+    for (int sidx = 0; sidx < 2; ++sidx)
+        boff[sidx] = (wm * C::TM + li) * 128 + (((lg + 4 * sidx) ^ swz8(li)) << 4);
+
+#pragma unroll
+    for (int u = -(WS - 1); u < 0; ++u) {
+        if (u + XS - 1 >= 0)
+            issue_x(u + XS - 1);
+        if (u + WS - 1 >= 0)
+            issue_w(u + WS - 1);
+    }
+    for (int64_t t = 0; t < ntk; ++t) {
+        DPS_WAIT_VMCNT(C::OUTSTANDING);  // tokens t and weights t have landed
+        stage_barrier();
+        const uint8_t *st = smem + (int)(t % WS) * C::W_SLOT;
+        const uint8_t *xs = smem + C::X_BASE + (int)(t % XS) * C::X_SLOT;
+        // token fragments of both MFMA steps stay in registers for the stage;
+        // the weight fragments go two row tiles at a time: the next pair is
+        // read while this pair's MFMAs run, and a pair's raw bytes die as it is
+        // merged, which keeps the wave within 256 registers
+        half8 bv[2][C::MT];
+#pragma unroll
+        for (int sidx = 0; sidx < 2; ++sidx)
+#pragma unroll
+            for (int mt = 0; mt < C::MT; ++mt)
+                bv[sidx][mt] =
+                    as_half8(*reinterpret_cast<const u32x4 *>(xs + boff[sidx] + mt * 2048));
+        u32x4 hv[2], lv[2];
+        auto read_a = [&](int g) {
+#pragma unroll
+            for (int q = 0; q < 2; ++q) {
+                const int nt = 2 * g + q;
+                lv[q] = u32x4{0u, 0u, 0u, 0u};
+                if (MODE == MODE_FULL) {
+                    hv[q] = *reinterpret_cast<const u32x4 *>(st + aoff + nt * 2048);
+                    lv[q] = *reinterpret_cast<const u32x4 *>(st + aoff_lo + nt * 2048);
+                } else {
+                    hv[q] = *reinterpret_cast<const u32x4 *>(st + aoff_f[q] + g * 2048);
+                }
+            }
+        };
+        read_a(0);
+        // the next stages' DMA goes out while the first fragment reads are in flight
+        issue_x(t + XS - 1);
+        issue_w(t + WS - 1);
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            half8 av[2][2];
+#pragma unroll
+            for (int q = 0; q < 2; ++q) {
+                av[0][q] = weight8<MODE, ENC>(hv[q].x, hv[q].y, lv[q].x, lv[q].y);
+                av[1][q] = weight8<MODE, ENC>(hv[q].z, hv[q].w, lv[q].z, lv[q].w);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            if (g < 3)
+                read_a(g + 1);
+#pragma unroll
+            for (int sidx = 0; sidx < 2; ++sidx)
+#pragma unroll
+                for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+                    for (int q = 0; q < 2; ++q)
+                        acc[2 * g + q][mt] =
+                            mfma16x16x32(av[sidx][q], bv[sidx][mt], acc[2 * g + q][mt]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+    DPS_WAIT_VMCNT(0);  // no DMA may still target this block's LDS when it exits
+
+#pragma unroll
+    for (int mt = 0; mt < C::MT; ++mt) {
+        const int64_t m = mrow0 + wm * C::TM + mt * 16 + li;
+#pragma unroll
+        for (int nt = 0; nt < 8; ++nt)
+            store_tile_out(a, s, m, n0 + wn * 128 + nt * 16 + lg * 4, acc[nt][mt], mrow1);
+    }
+}
+
 int64_t token_tiles(int64_t rows, int64_t experts, bool grouped, int bm = BM)
 {
     return grouped ? (rows + bm - 1) / bm + experts : (rows + bm - 1) / bm;
@@ -686,12 +985,16 @@ int64_t token_tiles(int64_t rows, int64_t experts, bool grouped, int bm = BM)
 
 int gemm_rows_per_block(int variant)
 {
-    return (variant == GEMM_G3_256x256 || variant == GEMM_G3_256x128) ? 256 : 128;
+    return (variant == GEMM_G3_256x256 || variant == GEMM_G3_256x128 ||
+            variant == GEMM_G5_256x256)
+               ? 256
+               : 128;
 }
 int gemm_tokens_per_block(int variant)
 {
     switch (variant) {
     case GEMM_G3_256x256: return 256;
+    case GEMM_G5_256x256: return 256;
     case GEMM_G4S_128x64: return 64;
     case GEMM_G4_128x32: return 32;
     default: return 128;
@@ -744,6 +1047,21 @@ hipError_t launch_g4(const GemmArgs &a, const LinearPlan &plan, bool grouped, hi
     return hipGetLastError();
 }
 
+template <int MODE, int ENC, int BM, int WS, int XS>
+hipError_t launch_g5(const GemmArgs &a, const LinearPlan &plan, bool grouped, hipStream_t stream)
+{
+    if (grouped)  // dense calls only
+        return hipErrorInvalidValue;
+    const dim3 grid = dense_grid((a.n + 255) / 256 * plan.splits * ((a.rows + BM - 1) / BM));
+    if (MODE == MODE_FULL && plan.range_addr)
+        hipLaunchKernelGGL((gemm5_kernel<MODE, ENC, BM, WS, XS, true>), grid, dim3(512), 0,
+                           stream, a);
+    else
+        hipLaunchKernelGGL((gemm5_kernel<MODE, ENC, BM, WS, XS, false>), grid, dim3(512), 0,
+                           stream, a);
+    return hipGetLastError();
+}
+
 // (token tile, weight slots, token slots) per mode, each within 160 KiB:
 // weights want depth (HBM), tokens at least a second slot ahead where it fits
 template <int MODE, int ENC>
@@ -755,6 +1073,7 @@ hipError_t launch_g4_variant(const GemmArgs &a, const LinearPlan &plan, bool gro
         case GEMM_G4_128x32: return launch_g4<MODE, ENC, 32, 4, 4, false>(a, plan, grouped, stream);
         case GEMM_G4S_128x128: return launch_g4<MODE, ENC, 128, 3, 2, true>(a, plan, grouped, stream);
         case GEMM_G4S_128x64: return launch_g4<MODE, ENC, 64, 4, 2, true>(a, plan, grouped, stream);
+        case GEMM_G5_256x256: return launch_g5<MODE, ENC, 256, 3, 2>(a, plan, grouped, stream);
         default: return hipErrorInvalidValue;
         }
     } else {
@@ -762,6 +1081,7 @@ hipError_t launch_g4_variant(const GemmArgs &a, const LinearPlan &plan, bool gro
         case GEMM_G4_128x32: return launch_g4<MODE, ENC, 32, 8, 4, false>(a, plan, grouped, stream);
         case GEMM_G4S_128x128: return launch_g4<MODE, ENC, 128, 4, 3, true>(a, plan, grouped, stream);
         case GEMM_G4S_128x64: return launch_g4<MODE, ENC, 64, 6, 4, true>(a, plan, grouped, stream);
+        case GEMM_G5_256x256: return launch_g5<MODE, ENC, 256, 4, 3>(a, plan, grouped, stream);
         default: return hipErrorInvalidValue;
         }
     }

@@ -61,7 +61,10 @@ enum GemmVariant {
     // tokens on four dedicated DMA waves do (the planner's three tiles)
     GEMM_G4_128x32 = 2,
     GEMM_G4S_128x64 = 3,
-    GEMM_G4S_128x128 = 4
+    GEMM_G4S_128x128 = 4,
+    // FP16 activations, prefill: 256 weight rows x 256 tokens, 64-element
+    // stages, 128 x 64 wave tiles
+    GEMM_G5_256x256 = 5
 };
 // Decode-kernel variants 0 and 1 keep the weight stream in registers (16 or
 // 32 weight rows per wave); SKINNY_RING streams it through per-wave LDS rings.
