@@ -198,8 +198,18 @@ def test_plan_info_names_the_kernel_of_each_shape_class(lib):
     assert d.plan_info(1, "fp16", 8, 6144, 4096)["kernel"] == "rows"
     p = d.plan_info(1, "fp16", 8, 4096, 4096, experts=8)
     assert p["kernel"] == "decode"
-    p = d.plan_info(0, "fp16", 2048, 28672, 4096)
+    p = d.plan_info(0, "fp16", 256, 28672, 4096)
     assert (p["kernel"], p["tile_rows"], p["tile_tokens"], p["splits"]) == ("gemm_f16", 128, 128, 1)
+    p = d.plan_info(0, "fp16", 2048, 6144, 4096)       # 192 large tiles: the 128 x 128 tile
+    assert (p["kernel"], p["tile_rows"], p["tile_tokens"], p["splits"]) == ("gemm_f16", 128, 128, 1)
+    p = d.plan_info(0, "fp16", 2048, 28672, 4096)      # 896 large tiles fill the chip
+    assert (p["kernel"], p["tile_rows"], p["tile_tokens"], p["splits"]) == ("gemm_f16", 256, 256, 1)
+    p = d.plan_info(1, "fp16", 2048, 4096, 14336)      # 128 tiles, two K ranges
+    assert (p["kernel"], p["tile_rows"], p["tile_tokens"], p["splits"]) == ("gemm_f16", 256, 256, 2)
+    p = d.plan_info(1, "fp16", 512, 4096, 14336)       # 32 tiles would need 8 ranges
+    assert (p["kernel"], p["tile_rows"]) == ("gemm_f16", 128)
+    p = d.plan_info(1, "fp16", 4096, 4096, 4096, experts=2)   # grouped calls keep 128 rows
+    assert (p["kernel"], p["tile_rows"]) == ("gemm_f16", 128)
     p = d.plan_info(1, "fp8", 4096, 4096, 1024)
     assert (p["kernel"], p["tile_rows"], p["tile_tokens"]) == ("gemm_fp8", 256, 256)
     p = d.plan_info(1, "fp8", 2048, 6144, 4096)
