@@ -484,6 +484,12 @@ dps_status run_linear(int mode, uint32_t flags, const uint16_t *x, const int32_t
         (grouped ? w->experts : 0);
     REQUIRE(token_tiles <= 65535, DPS_ERR_UNSUPPORTED, "too many rows for one call");
     REQUIRE(plan.splits <= 65535, DPS_ERR_UNSUPPORTED, "k too large for one call");
+    // dense GEMMs run a 1-D grid of up to 768 threads per block, whose size
+    // in threads must fit 32 bits
+    if (gemm && !grouped)
+        REQUIRE(cdiv(w->n, dps::gemm_rows_per_block(plan.variant)) * plan.splits * token_tiles <=
+                    (int64_t)(0xFFFFFFFFu / 768),
+                DPS_ERR_UNSUPPORTED, "call too large for one grid");
 
     float *partial = plan.splits > 1 ? static_cast<float *>(ws) : nullptr;
     dps::LinearProblem p;

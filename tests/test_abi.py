@@ -266,3 +266,14 @@ def test_probe_library_exports_its_header():
     assert plib.dps_probe_mfma(0, 0, 4, 0x1000, None) == 1
     assert plib.dps_probe_mfma(1, 8, 0, 0x1000, None) == 1
     assert plib.dps_probe_mfma(0, 8, 4, None, None) == 1
+
+
+def test_dense_grid_limit_is_refused_on_the_host(lib):
+    """A dense call whose GEMM grid would exceed 2^32 threads (here 2^30 - 16
+    weight rows at 8192 tokens: 8.4 M tiles of 128 x 128 on 768-thread blocks)
+    is refused before anything is enqueued."""
+    n, k, rows = (1 << 30) - 16, 16, 8192
+    w = _weight(n=n, k=k, n_chunks=1 << 20, log2=30, pool_bytes=1 << 30)
+    st = lib.dps_linear(1, 0, 0x4000, rows, ctypes.byref(w), 0x5000, None, 0, None)
+    assert st == 3, st
+    assert b"too large for one grid" in lib.dps_last_error()
