@@ -55,6 +55,11 @@ def parse():
                          "copy kernel of known size, then exit; ':fp8' = fast mode on FP8 "
                          "activations (prefill)")
     ap.add_argument("--probe-reps", type=int, default=20)
+    ap.add_argument("--probe-set", choices=("h4096", "h8192"), default="h4096",
+                    help="layer set of --probe-call")
+    ap.add_argument("--probe-slots", choices=("identity", "scattered"), default="identity",
+                    help="residual chunk table of --probe-call: chunk c in slot c, or chunks at "
+                         "seeded random slots of a pool twice the residual's size")
     ap.add_argument("--ceilings", action="store_true",
                     help="measure only the HBM streaming-read and MFMA-loop ceilings "
                          "(libdps_probe), print them as JSON and exit")
@@ -86,6 +91,8 @@ def main():
 
     layers = workloads.H4096_SET
     enc = dps.ENC_E4M3 if args.enc == "e4m3" else dps.ENC_E5M2
+    if args.probe_set == "h8192":
+        layers = workloads.H8192_SET
     if args.ceilings:
         print(json.dumps({"ceilings": measured_ceilings(torch, stream)}), flush=True)
         return
@@ -367,9 +374,11 @@ def measured_traffic(probe_call, enc):
 
 
 def probe(args, torch, dps, workloads, layers, dev, stream, enc):
-    """One call of the decode set, launched back to back on rotating weight
-    copies, then a device-to-device copy of 256 MiB (a kernel of known HBM
-    traffic, to calibrate rocprofv3's FETCH_SIZE / WRITE_SIZE)."""
+    """One call of a layer set (hidden 4096 or 8192), launched back to back
+    on rotating weight copies whose residuals sit in 2 MiB chunks (identity
+    table, or seeded random slots of a pool twice the residual's size), then a
+    device-to-device copy of 256 MiB (a kernel of known HBM traffic, to
+    calibrate rocprofv3's FETCH_SIZE / WRITE_SIZE)."""
     parts = args.probe_call.split(":")
     name, m, mode_name = parts[:3]
     act = parts[3] if len(parts) > 3 else "fp16"
@@ -383,7 +392,14 @@ def probe(args, torch, dps, workloads, layers, dev, stream, enc):
         nws = []
         for c in range(COPIES):
             w = workloads.weight_fp16(n, k, seed=1000 * c + li, device=dev)
-            nws.append(dps.split(w, dps.make_residual(n * k, LOG2_CHUNK, dev), enc=enc))
+            if args.probe_slots == "scattered":
+                n_chunks = workloads.n_chunks_for(n * k, LOG2_CHUNK)
+                slots = workloads.chunk_slots(n_chunks, 2 * n_chunks, seed=500 + li + 10 * c)
+                pool = torch.empty(2 * n_chunks << LOG2_CHUNK, dtype=torch.uint8, device=dev)
+                res = dps.Residual(pool, slots.to(dev), LOG2_CHUNK)
+            else:
+                res = dps.make_residual(n * k, LOG2_CHUNK, dev)
+            nws.append(dps.split(w, res, enc=enc))
             del w
         x = workloads.activations_fp16(m, k, seed=m * 7 + k, device=dev,
                                        outlier_frac=0.01 if act == "fp8" else 0.0)
@@ -406,7 +422,8 @@ def probe(args, torch, dps, workloads, layers, dev, stream, enc):
             dst.copy_(src)
         stream.synchronize()
     t = e0.elapsed_time(e1) * 1e-3 / args.probe_reps
-    print(json.dumps({"probe_call": args.probe_call, "us_per_call": round(t * 1e6, 2),
+    print(json.dumps({"probe_call": args.probe_call, "layer_set": args.probe_set,
+                      "slots": args.probe_slots, "us_per_call": round(t * 1e6, 2),
                       "kernels_per_call": 1 if need == 0 else 2,
                       "flops_per_call": 2.0 * m * n * k,
                       "copy_bytes_each_way": 256 << 20}), flush=True)
