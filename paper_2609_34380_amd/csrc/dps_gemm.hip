@@ -684,11 +684,13 @@ __global__ __launch_bounds__(SPEC ? 768 : 512) void gemm4_kernel(GemmArgs a)
 // fills 64 KiB of LDS per 128-element stage for 1024 MFMA cycles per SIMD,
 // and its 64 x 64 wave tiles read 16 KiB of fragments per wave per stage.
 // This kernel takes 256 weight rows x BM tokens per block (dense calls; the
-// planner launches BM = 256) with eight waves in a 2 x 4 grid, each over a
-// 128 x BM/4 wave tile on the whole K range of every stage: per FP16 flop it fills half the LDS bytes
-// (256 x 256) and reads 0.75x the fragment bytes (12 of 16 per 32 MFMAs at
-// BM = 256) of the 128 x 128 tile, and it does twice the matrix work between
-// two barriers.
+// planner launches BM = 256) with eight waves in a 4 x 2 grid, each over a
+// 64 x BM/2 wave tile on the whole K range of every stage: per FP16 flop it
+// fills half the LDS bytes (256 x 256) and reads 0.75x the fragment bytes
+// (12 of 16 per 32 MFMAs at BM = 256) of the 128 x 128 tile, and it does
+// twice the matrix work between two barriers.  Each wave merges its 64
+// weight rows once per stage (two waves share them), keeps them in registers
+// and streams the token fragments past them.
 //
 // A stage is 64 K elements.  A DMA instruction fills 1 KiB of LDS: 8 weight
 // lines of 128 bytes (full mode: 8 rows x (64 upper + 64 residual bytes);
@@ -714,7 +716,7 @@ struct G5 {
     static constexpr int NW = W_SLOT / 1024 / 8;        // weight instructions per wave per stage
     static constexpr int NX = X_SLOT / 1024 / 8;
     static constexpr int OUTSTANDING = (XS < WS ? NW : 0) + (XS - 2) * (NX + NW);
-    static constexpr int TM = BM / 4;                   // tokens per wave
+    static constexpr int TM = BM / 2;                   // tokens per wave
     static constexpr int MT = TM / 16;
     static_assert(WS >= 2 && XS >= 2 && XS <= WS, "ring depths of the counter scheme");
     static_assert(OUTSTANDING <= 63, "vmcnt range");
@@ -751,8 +753,8 @@ __global__ __launch_bounds__(512) void gemm5_kernel(GemmArgs a)
     const int wave = tid >> 6;
     const int li = lane & 15;
     const int lg = lane >> 4;
-    const int wn = wave & 1;   // 128-row half of the weight tile
-    const int wm = wave >> 1;  // BM/4-token quarter of the token tile
+    const int wn = wave & 3;   // 64-row quarter of the weight tile
+    const int wm = wave >> 2;  // BM/2-token half of the token tile
 
     // 1-D grid remapped for the 8 XCDs (block L runs on XCD L % 8): XCD x
     // takes the tile range [x * per_xcd, (x+1) * per_xcd), walked in groups
@@ -879,24 +881,24 @@ __global__ __launch_bounds__(512) void gemm5_kernel(GemmArgs a)
         }
     };
 
-    f32x4 acc[8][C::MT];
+    f32x4 acc[4][C::MT];
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < C::MT; ++j)
             acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     // fragment offsets: the swizzles depend on the low bits of the line or
     // row only, which every 16-line tile shares with the lane's li.  Row
-    // tile nt of the wave: full mode upper bytes at aoff + 2048 nt, residual
-    // 64 bytes further in the swizzled line (aoff_lo); fast mode at
-    // aoff_f[nt & 1] + 2048 (nt >> 1).
-    const int aoff = (wn * 128 + li) * 128 + ((lg ^ swz8(li)) << 4);
-    const int aoff_lo = (wn * 128 + li) * 128 + (((4 + lg) ^ swz8(li)) << 4);
+    // tile nt (0-3) of the wave: full mode upper bytes at aoff + 2048 nt,
+    // residual 64 bytes further in the swizzled line (aoff_lo); fast mode at
+    // aoff_f[nt & 1] + 2048 (nt >> 1).  Token tile mt at boff[s] + 2048 mt.
+    const int aoff = (wn * 64 + li) * 128 + ((lg ^ swz8(li)) << 4);
+    const int aoff_lo = (wn * 64 + li) * 128 + (((4 + lg) ^ swz8(li)) << 4);
     int aoff_f[2];
 #pragma unroll
     for (int q = 0; q < 2; ++q)
-        aoff_f[q] = (wn * 64 + li) * 128 + (((4 * q + lg) ^ swz8(li)) << 4);
+        aoff_f[q] = (wn * 32 + li) * 128 + (((4 * q + lg) ^ swz8(li)) << 4);
     int boff[2];
 #pragma unroll
     for (int sidx = 0; sidx < 2; ++sidx)
@@ -914,55 +916,50 @@ __global__ __launch_bounds__(512) void gemm5_kernel(GemmArgs a)
         stage_barrier();
         const uint8_t *st = smem + (int)(t % WS) * C::W_SLOT;
         const uint8_t *xs = smem + C::X_BASE + (int)(t % XS) * C::X_SLOT;
-        // token fragments of both MFMA steps stay in registers for the stage;
-        // the weight fragments go two row tiles at a time: the next pair is
-        // read while this pair's MFMAs run, and a pair's raw bytes die as it is
-        // merged, which keeps the wave within 256 registers
-        half8 bv[2][C::MT];
+        // the wave's four weight row tiles are read and merged once per
+        // stage and stay in registers (both MFMA steps); the token fragments
+        // stream one 16-token tile at a time, the next read while this one's
+        // MFMAs run
+        half8 av[2][4];
+        {
+            u32x4 hv[4], lv[4];
 #pragma unroll
-        for (int sidx = 0; sidx < 2; ++sidx)
-#pragma unroll
-            for (int mt = 0; mt < C::MT; ++mt)
-                bv[sidx][mt] =
-                    as_half8(*reinterpret_cast<const u32x4 *>(xs + boff[sidx] + mt * 2048));
-        u32x4 hv[2], lv[2];
-        auto read_a = [&](int g) {
-#pragma unroll
-            for (int q = 0; q < 2; ++q) {
-                const int nt = 2 * g + q;
-                lv[q] = u32x4{0u, 0u, 0u, 0u};
+            for (int nt = 0; nt < 4; ++nt) {
+                lv[nt] = u32x4{0u, 0u, 0u, 0u};
                 if (MODE == MODE_FULL) {
-                    hv[q] = *reinterpret_cast<const u32x4 *>(st + aoff + nt * 2048);
-                    lv[q] = *reinterpret_cast<const u32x4 *>(st + aoff_lo + nt * 2048);
+                    hv[nt] = *reinterpret_cast<const u32x4 *>(st + aoff + nt * 2048);
+                    lv[nt] = *reinterpret_cast<const u32x4 *>(st + aoff_lo + nt * 2048);
                 } else {
-                    hv[q] = *reinterpret_cast<const u32x4 *>(st + aoff_f[q] + g * 2048);
+                    hv[nt] = *reinterpret_cast<const u32x4 *>(st + aoff_f[nt & 1] + (nt >> 1) * 2048);
                 }
             }
-        };
-        read_a(0);
-        // the next stages' DMA goes out while the first fragment reads are in flight
-        issue_x(t + XS - 1);
-        issue_w(t + WS - 1);
+            // the next stages' DMA goes out while the fragment reads are in flight
+            issue_x(t + XS - 1);
+            issue_w(t + WS - 1);
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            half8 av[2][2];
-#pragma unroll
-            for (int q = 0; q < 2; ++q) {
-                av[0][q] = weight8<MODE, ENC>(hv[q].x, hv[q].y, lv[q].x, lv[q].y);
-                av[1][q] = weight8<MODE, ENC>(hv[q].z, hv[q].w, lv[q].z, lv[q].w);
+            for (int nt = 0; nt < 4; ++nt) {
+                av[0][nt] = weight8<MODE, ENC>(hv[nt].x, hv[nt].y, lv[nt].x, lv[nt].y);
+                av[1][nt] = weight8<MODE, ENC>(hv[nt].z, hv[nt].w, lv[nt].z, lv[nt].w);
             }
+        }
+        half8 bv[2][2];
+        auto read_b = [&](int buf, int mt) {
+#pragma unroll
+            for (int sidx = 0; sidx < 2; ++sidx)
+                bv[buf][sidx] =
+                    as_half8(*reinterpret_cast<const u32x4 *>(xs + boff[sidx] + mt * 2048));
+        };
+        read_b(0, 0);
+#pragma unroll
+        for (int mt = 0; mt < C::MT; ++mt) {
             __builtin_amdgcn_sched_barrier(0);
-            if (g < 3)
-                read_a(g + 1);
+            if (mt + 1 < C::MT)
+                read_b((mt + 1) & 1, mt + 1);
 #pragma unroll
             for (int sidx = 0; sidx < 2; ++sidx)
 #pragma unroll
-                for (int mt = 0; mt < C::MT; ++mt)
-#pragma unroll
-                    for (int q = 0; q < 2; ++q)
-                        acc[2 * g + q][mt] =
-                            mfma16x16x32(av[sidx][q], bv[sidx][mt], acc[2 * g + q][mt]);
-            __builtin_amdgcn_sched_barrier(0);
+                for (int nt = 0; nt < 4; ++nt)
+                    acc[nt][mt] = mfma16x16x32(av[sidx][nt], bv[mt & 1][sidx], acc[nt][mt]);
         }
     }
     DPS_WAIT_VMCNT(0);  // no DMA may still target this block's LDS when it exits
@@ -971,8 +968,8 @@ __global__ __launch_bounds__(512) void gemm5_kernel(GemmArgs a)
     for (int mt = 0; mt < C::MT; ++mt) {
         const int64_t m = mrow0 + wm * C::TM + mt * 16 + li;
 #pragma unroll
-        for (int nt = 0; nt < 8; ++nt)
-            store_tile_out(a, s, m, n0 + wn * 128 + nt * 16 + lg * 4, acc[nt][mt], mrow1);
+        for (int nt = 0; nt < 4; ++nt)
+            store_tile_out(a, s, m, n0 + wn * 64 + nt * 16 + lg * 4, acc[nt][mt], mrow1);
     }
 }
 
