@@ -191,7 +191,7 @@ def main():
             flops = 2.0 * m * n * k
             bound_t = max(alg / (HBM_PEAK_GBS * 1e9), flops / (MFMA_F16_TFLOPS * 1e12))
             breakdown.append({"layer": name, "M": m, "mode": mname, "us": round(t * 1e6, 2),
-                              "us_p10": round(p10 * 1e3, 2), "us_p90": round(p90 * 1e3, 2),
+                              "us_p10": round(p10 * 1e6, 2), "us_p90": round(p90 * 1e6, 2),
                               "eff_weight_GBs": round(wb / t / 1e9, 1),
                               "alg_GBs": round(alg / t / 1e9, 1),
                               "TFLOPs": round(flops / t / 1e12, 2),
@@ -259,6 +259,7 @@ def main():
     torch.cuda.synchronize()
     if not args.no_secondary:
         secondary["library_fp16"] = library_fp16_secondary(torch, workloads, layers, ms, stream)
+        secondary["single_layer"] = single_layer_secondary(torch, dps, workloads, stream, enc)
         secondary["moe_grouped"] = moe_secondary(torch, dps, workloads, stream, enc)
         secondary["restore"] = restore_secondary(torch, dps, workloads, stream, enc)
         secondary["sum_manager"] = sum_secondary(dps)
@@ -492,11 +493,73 @@ def prefill_secondary(torch, dps, workloads, nws, layers, stream):
     return res
 
 
+def single_layer_secondary(torch, dps, workloads, stream, enc):
+    """The single-layer case as a latency figure: W 1024 x 1024 (residual in
+    64 KiB chunks, identity table), X 4 x 1024, both modes.  Per call: HIP
+    events around each of 50 eager launches (median, p10, p90), and 40 calls
+    captured in one graph, replayed five times (time per call).  The 1 or 2
+    MiB of weight planes stay in the caches, so this is launch latency, not
+    bandwidth."""
+    dev = torch.device("cuda:0")
+    n = k = 1024
+    m = 4
+    res = {"workload": "single_1024x1024, M=4, 64 KiB chunks, identity table",
+           "encoding": "e4m3" if enc == dps.ENC_E4M3 else "e5m2"}
+    with torch.cuda.stream(stream):
+        w = workloads.weight_fp16(n, k, seed=1101, device=dev)
+        nw = dps.split(w, dps.make_residual(n * k, 16, dev), enc=enc)
+        x = workloads.activations_fp16(m, k, seed=1102, device=dev)
+        y = torch.empty((m, n), dtype=torch.float16, device=dev)
+        need = max(dps.workspace_bytes(md, 0, m, n, k) for md in (dps.MODE_FAST, dps.MODE_FULL))
+        ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+        for label, mode in (("fast", dps.MODE_FAST), ("full", dps.MODE_FULL)):
+            wb = n * k * (1 if mode == dps.MODE_FAST else 2)
+            for _ in range(5):
+                dps.linear(x, nw, mode, out=y, workspace=ws)
+            reps = 50
+            evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                   for _ in range(reps)]
+            for r in range(reps):
+                evs[r][0].record(stream)
+                dps.linear(x, nw, mode, out=y, workspace=ws)
+                evs[r][1].record(stream)
+            stream.synchronize()
+            ts = sorted(a.elapsed_time(b) for a, b in evs)
+            t = ts[len(ts) // 2] * 1e-3
+            g = torch.cuda.CUDAGraph()
+            per_graph = 40
+            with torch.cuda.graph(g, stream=stream):
+                for _ in range(per_graph):
+                    dps.linear(x, nw, mode, out=y, workspace=ws)
+            g.replay()
+            stream.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(5):
+                g.replay()
+            e1.record(stream)
+            stream.synchronize()
+            tg = e0.elapsed_time(e1) * 1e-3 / (5 * per_graph)
+            del g
+            plan = dps.plan_info(mode, "fp16", m, n, k)
+            res[label] = {"kernel": plan["kernel"], "us": round(t * 1e6, 2),
+                          "us_p10": round(pct(ts, 10) * 1e6, 2),
+                          "us_p90": round(pct(ts, 90) * 1e6, 2),
+                          "us_per_call_in_graph": round(tg * 1e6, 2),
+                          "weight_GBs_in_graph": round(wb / tg / 1e9, 1),
+                          "roofline_frac_in_graph": round(
+                              (wb + 2 * m * (n + k)) / (HBM_PEAK_GBS * 1e9) / tg, 3)}
+        del w, nw, x, y, ws
+    torch.cuda.synchronize()
+    return res
+
+
 def moe_secondary(torch, dps, workloads, stream, enc):
     """Grouped MoE linear (8 experts, hidden 4096, ffn 14336; 512 tokens routed
     top-2 by uniform random choice, so 1024 rows grouped by expert): the
     stacked gate+up and down weights through dps_linear_grouped in both
-    modes.  One weight copy per layer (1.41 GB of upper bytes, as much again
+    modes with FP16 activations, and in fast mode with FP8 activations.  One weight copy per layer (1.41 GB of upper bytes, as much again
     of residual) is far beyond the 256 MB Infinity Cache, so reads come from
     HBM.  GB/s counts the weight-plane bytes each mode must read."""
     dev = torch.device("cuda:0")
@@ -516,13 +579,16 @@ def moe_secondary(torch, dps, workloads, stream, enc):
             x = workloads.activations_fp16(tokens, k, seed=920 + li, device=dev)
             layers.append((nw, x[tok_dev].contiguous(),
                            torch.empty((rows, n), dtype=torch.float16, device=dev), n, k))
-        need = max(dps.workspace_bytes(mode, 0, rows, n, k, experts)
-                   for _, _, _, n, k in layers for mode in (dps.MODE_FAST, dps.MODE_FULL))
+        legs = (("fast", dps.MODE_FAST, "fp16", MFMA_F16_TFLOPS),
+                ("full", dps.MODE_FULL, "fp16", MFMA_F16_TFLOPS),
+                ("fast_fp8", dps.MODE_FAST, "fp8", MFMA_FP8_TFLOPS))
+        need = max(dps.workspace_bytes(mode, dps._act_flag(act), rows, n, k, experts)
+                   for _, _, _, n, k in layers for _, mode, act, _ in legs)
         ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
-        for label, mode in (("fast", dps.MODE_FAST), ("full", dps.MODE_FULL)):
+        for label, mode, act, peak in legs:
             wb = 1 if mode == dps.MODE_FAST else 2
             for nw, x, y, _, _ in layers:
-                dps.linear_grouped(x, off_dev, nw, mode, out=y, workspace=ws)
+                dps.linear_grouped(x, off_dev, nw, mode, act=act, out=y, workspace=ws)
             stream.synchronize()
             reps = 10
             ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -533,7 +599,7 @@ def moe_secondary(torch, dps, workloads, stream, enc):
             for r in range(reps):
                 for li, (nw, x, y, _, _) in enumerate(layers):
                     ev[r][li][0].record(stream)
-                    dps.linear_grouped(x, off_dev, nw, mode, out=y, workspace=ws)
+                    dps.linear_grouped(x, off_dev, nw, mode, act=act, out=y, workspace=ws)
                     ev[r][li][1].record(stream)
             e1.record(stream)
             stream.synchronize()
@@ -546,20 +612,21 @@ def moe_secondary(torch, dps, workloads, stream, enc):
                 tc = ts[len(ts) // 2] * 1e-3
                 alg = wb * experts * n * k + 2 * rows * k + 2 * rows * n
                 fl = 2.0 * rows * n * k
-                bound = max(alg / (HBM_PEAK_GBS * 1e9), fl / (MFMA_F16_TFLOPS * 1e12))
+                bound = max(alg / (HBM_PEAK_GBS * 1e9), fl / (peak * 1e12))
                 calls.append({"layer": workloads.MOE_SHAPES[li][0], "us": round(tc * 1e6, 1),
                               "us_p10": round(pct(ts, 10) * 1e6, 1),
                               "us_p90": round(pct(ts, 90) * 1e6, 1),
                               "weight_GBs": round(wb * experts * n * k / tc / 1e9, 1),
                               "roofline_frac": round(bound / tc, 3),
                               "bound": "hbm" if alg / (HBM_PEAK_GBS * 1e9) >= fl / (
-                                  MFMA_F16_TFLOPS * 1e12) else "mfma"})
+                                  peak * 1e12) else "mfma"})
             ideal = sum(max((wb * experts * n * k + 2 * rows * (n + k)) / (HBM_PEAK_GBS * 1e9),
-                            2.0 * rows * n * k / (MFMA_F16_TFLOPS * 1e12))
+                            2.0 * rows * n * k / (peak * 1e12))
                         for _, _, _, n, k in layers)
-            res[label] = {"ms": round(t * 1e3, 3), "GBs": round(wbytes / t / 1e9, 1),
+            res[label] = {"activations": act, "ms": round(t * 1e3, 3),
+                          "GBs": round(wbytes / t / 1e9, 1),
                           "TFLOPs": round(flops / t / 1e12, 1),
-                          "frac_of_mfma_peak": round(flops / t / 1e12 / MFMA_F16_TFLOPS, 3),
+                          "frac_of_mfma_peak": round(flops / t / 1e12 / peak, 3),
                           "roofline_frac": round(ideal / t, 3), "calls": calls}
         del layers, ws
     torch.cuda.synchronize()

@@ -273,8 +273,10 @@ dps_status dps_linear_static(int mode, uint32_t flags, const uint16_t *x, int64_
  *   y         device FP16 [rows][w->n].
  * With w->experts == 1 the call is the dense one (dps_linear on all rows,
  * same kernels and results); offsets is then checked but not read.
- * Other arguments as dps_linear.  DPS_ACT_FP8_ROWSCALE is not supported
- * here (DPS_ERR_UNSUPPORTED). */
+ * Other arguments as dps_linear.  With DPS_ACT_FP8_ROWSCALE (fast mode only)
+ * every row of x_sorted is quantized to E4M3 with its own power-of-two scale,
+ * as in dps_quant_rows_e4m3, and multiplied on the FP8 matrix cores against
+ * its expert's upper bytes (Sec. IV-C: fast-mode prefill, MoE case). */
 dps_status dps_linear_grouped(int mode, uint32_t flags, const uint16_t *x_sorted,
                               const int32_t *offsets, int64_t rows, const dps_weight *w,
                               uint16_t *y, void *ws, size_t ws_bytes, void *stream);

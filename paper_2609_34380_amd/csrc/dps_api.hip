@@ -156,11 +156,13 @@ LinearPlan plan_linear(int mode, uint32_t flags, int64_t rows, int64_t n, int64_
         // against 165 us, down and O at 4096 tokens (256) 245 / 78 against
         // 297 / 95; QKV at 2048 tokens (192) 94 against 110 and at 3072
         // (288, a last round of 32) 129 against 139 on the smaller tile.
+        // Grouped calls take the 128-token tile: an expert's rows rarely
+        // fill 256.
         {
             const int64_t cus = cu_count;
             const int64_t big = cdiv(n, 256) * cdiv(rows, 256);
             const bool fills = big >= cus && (big % cus == 0 || 2 * (big % cus) >= cus);
-            p.variant = fills ? GEMM_G3_256x256 : GEMM_G3_256x128;
+            p.variant = fills && !grouped ? GEMM_G3_256x256 : GEMM_G3_256x128;
         }
         // K is split only while the tiles alone leave CUs idle: the fp32
         // partials cost more than a half-filled last wave of blocks (MI355X,
@@ -512,8 +514,8 @@ dps_status run_linear(int mode, uint32_t flags, const uint16_t *x, const int32_t
         st = launched(dps::launch_quant_rows(x, rows, w->k, xq, scale, stream));
         if (st != DPS_OK)
             return st;
-        st = launched(dps::launch_gemm_fp8(w->enc, xq, scale, rows, w->n, w->k, w->hi, y, plan, partial,
-                                           stream));
+        st = launched(dps::launch_gemm_fp8(w->enc, xq, scale, offsets, rows, w->experts, w->n,
+                                           w->k, w->hi, y, plan, partial, stream));
     } else if (plan.kind == dps::KIND_GEMV) {
         st = launched(dps::launch_gemv(p, plan, stream));
     } else if (plan.kind == dps::KIND_ROWS) {
@@ -561,8 +563,8 @@ DPS_EXPORT dps_status dps_linear_grouped(int mode, uint32_t flags, const uint16_
     REQUIRE(mode == DPS_MODE_FULL || mode == DPS_MODE_FAST, DPS_ERR_INVALID_ARG, "unknown mode");
     REQUIRE(flags == DPS_ACT_FP16 || flags == DPS_ACT_FP8_ROWSCALE, DPS_ERR_INVALID_ARG,
             "unknown flags");
-    REQUIRE(flags == DPS_ACT_FP16, DPS_ERR_UNSUPPORTED,
-            "grouped linear supports FP16 activations only");
+    REQUIRE(!(flags == DPS_ACT_FP8_ROWSCALE && mode != DPS_MODE_FAST), DPS_ERR_INVALID_ARG,
+            "FP8 activations need fast mode");
     dps_status s = check_weight(w, mode);
     if (s != DPS_OK)
         return s;

@@ -186,23 +186,34 @@ __global__ __launch_bounds__(WN * WM * 64 + (DW ? 256 : 0)) void gemm3_kernel(Ge
     const int iss = DW ? wave - C::NWAVES : wave;  // index among the issuing waves
     const bool issues = !DW || dma_wave;
 
-    // 1-D grid remapped for the 8 XCDs: block L runs on XCD L % 8, so XCD x
-    // is given the contiguous tile range [x * per_xcd, (x+1) * per_xcd),
-    // walked with the token tile fastest.  Blocks sharing a weight tile then
-    // run together on one XCD and fetch it into that XCD's L2 once.
-    const int64_t mtiles = (a.rows + BM_ - 1) / BM_;
-    const int64_t ntiles = (a.n + BN_ - 1) / BN_;
-    const int64_t total = mtiles * ntiles * a.splits;
-    const int64_t per_xcd = (total + 7) / 8;
-    const int64_t lin = blockIdx.x;
-    const int64_t t0 = (lin % 8) * per_xcd + lin / 8;
-    if (t0 >= total)
-        return;
-    const int64_t mtile = t0 % mtiles;
-    const int ntile = (int)((t0 / mtiles) % ntiles);
-    const int s = (int)(t0 / (mtiles * ntiles));
-    const int64_t mrow0 = mtile * BM_;
-    const int64_t mrow1 = mrow0 + BM_ < a.rows ? mrow0 + BM_ : a.rows;
+    int64_t e, mrow0, mrow1;
+    int ntile, s;
+    if (a.offsets) {
+        // grouped: grid.y walks the experts' token tiles, grid.x the weight
+        // tiles times the K ranges
+        if (!block_rows(a, e, mrow0, mrow1, BM_))
+            return;
+        ntile = blockIdx.x / a.splits;
+        s = blockIdx.x % a.splits;
+    } else {
+        // 1-D grid remapped for the 8 XCDs: block L runs on XCD L % 8, so XCD
+        // x is given the contiguous tile range [x * per_xcd, (x+1) * per_xcd),
+        // walked with the token tile fastest.  Blocks sharing a weight tile
+        // then run together on one XCD and fetch it into that XCD's L2 once.
+        const int64_t mtiles = (a.rows + BM_ - 1) / BM_;
+        const int64_t ntiles = (a.n + BN_ - 1) / BN_;
+        const int64_t total = mtiles * ntiles * a.splits;
+        const int64_t per_xcd = (total + 7) / 8;
+        const int64_t lin = blockIdx.x;
+        const int64_t t0 = (lin % 8) * per_xcd + lin / 8;
+        if (t0 >= total)
+            return;
+        ntile = (int)((t0 / mtiles) % ntiles);
+        s = (int)(t0 / (mtiles * ntiles));
+        e = 0;
+        mrow0 = (t0 % mtiles) * BM_;
+        mrow1 = mrow0 + BM_ < a.rows ? mrow0 + BM_ : a.rows;
+    }
     const int64_t n0 = (int64_t)ntile * BN_;
     const int64_t kb0 = (int64_t)s * a.ksplit;
     const int64_t ke = kb0 + a.ksplit < a.k ? kb0 + a.ksplit : a.k;
@@ -219,7 +230,7 @@ __global__ __launch_bounds__(WN * WM * 64 + (DW ? 256 : 0)) void gemm3_kernel(Ge
         const int r = 8 * j + (lane >> 3);
         int64_t nr = n0 + r;
         nr = nr < a.n ? nr : a.n - 1;
-        wsrc[jj] = a.hi + nr * a.k;
+        wsrc[jj] = a.hi + (e * a.n + nr) * a.k;
         wel[jj] = ((lane & 7) ^ g3_swz(r)) * 16;
     }
     const uint8_t *xsrc[C::X_INSTR];
@@ -1010,7 +1021,9 @@ template <int ENC, int BN_, int BM_, int WN, int WM, int WS, int XS, bool DW>
 hipError_t launch_g3(const GemmArgs &a, const LinearPlan &plan, hipStream_t stream)
 {
     const int64_t nt = (a.n + BN_ - 1) / BN_;
-    const dim3 grid = dense_grid(nt * plan.splits * ((a.rows + BM_ - 1) / BM_));
+    const dim3 grid = a.offsets ? dim3((unsigned)(nt * plan.splits),
+                                       (unsigned)token_tiles(a.rows, a.experts, true, BM_), 1)
+                                : dense_grid(nt * plan.splits * ((a.rows + BM_ - 1) / BM_));
     hipLaunchKernelGGL((gemm3_kernel<ENC, BN_, BM_, WN, WM, WS, XS, DW>), grid,
                        dim3(WN * WM * 64 + (DW ? 256 : 0)), 0,
                        stream, a);
@@ -1112,15 +1125,15 @@ hipError_t launch_gemm_f16(const LinearProblem &p, const LinearPlan &plan, float
                                : launch_g4_variant<MODE_FAST, ENC_E5M2>(a, plan, grouped, stream);
 }
 
-hipError_t launch_gemm_fp8(int enc, const uint8_t *xq, const float *scale, int64_t m, int64_t n,
-                           int64_t k, const uint8_t *hi, uint16_t *y, const LinearPlan &plan,
-                           float *partial, hipStream_t stream)
+hipError_t launch_gemm_fp8(int enc, const uint8_t *xq, const float *scale, const int32_t *offsets,
+                           int64_t m, int64_t experts, int64_t n, int64_t k, const uint8_t *hi,
+                           uint16_t *y, const LinearPlan &plan, float *partial, hipStream_t stream)
 {
     GemmArgs a;
     a.x = xq;
-    a.offsets = nullptr;
+    a.offsets = offsets;
     a.rows = m;
-    a.experts = 1;
+    a.experts = experts;
     a.hi = hi;
     a.res = ResidualView{nullptr, nullptr, 0, 0, 0};
     a.n = n;

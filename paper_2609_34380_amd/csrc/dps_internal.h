@@ -94,8 +94,11 @@ hipError_t launch_gemv(const LinearProblem &p, const LinearPlan &plan, hipStream
 hipError_t launch_rows(const LinearProblem &p, const LinearPlan &plan, hipStream_t stream);
 hipError_t launch_gemm_f16(const LinearProblem &p, const LinearPlan &plan, float *partial,
                            hipStream_t stream);
-hipError_t launch_gemm_fp8(int enc, const uint8_t *xq, const float *scale, int64_t m, int64_t n,
-                           int64_t k, const uint8_t *hi, uint16_t *y, const LinearPlan &plan,
-                           float *partial, hipStream_t stream);
+// FP8 activations (E4M3 codes and row scales from launch_quant_rows) against
+// the upper bytes; offsets == nullptr: dense, else rows grouped by expert as
+// in LinearProblem (weights [experts][n][k]).
+hipError_t launch_gemm_fp8(int enc, const uint8_t *xq, const float *scale, const int32_t *offsets,
+                           int64_t m, int64_t experts, int64_t n, int64_t k, const uint8_t *hi,
+                           uint16_t *y, const LinearPlan &plan, float *partial, hipStream_t stream);
 
 }  // namespace dps

@@ -345,17 +345,18 @@ def linear_static(x, nw, mode, act="fp16", out=None):
     return out
 
 
-def linear_grouped(x_sorted, offsets, nw, mode, out=None, workspace=None):
+def linear_grouped(x_sorted, offsets, nw, mode, act="fp16", out=None, workspace=None):
     """MoE grouped linear through dps_linear_grouped; offsets is an int32
     device tensor of experts + 1 row offsets."""
     lib = load_library()
     _require_cuda(x_sorted, offsets)
     assert offsets.dtype == torch.int32 and offsets.numel() == nw.experts + 1
+    flag = _act_flag(act)
     rows = x_sorted.shape[0]
     if out is None:
         out = torch.empty((rows, nw.n), dtype=torch.float16, device=x_sorted.device)
-    ws, ws_bytes = _workspace(mode, ACT_FP16, rows, nw, x_sorted.device, workspace)
-    _check(lib.dps_linear_grouped(mode, ACT_FP16, _ptr(x_sorted), _ptr(offsets), rows,
+    ws, ws_bytes = _workspace(mode, flag, rows, nw, x_sorted.device, workspace)
+    _check(lib.dps_linear_grouped(mode, flag, _ptr(x_sorted), _ptr(offsets), rows,
                                   ctypes.byref(nw.c()), _ptr(out), _ptr(ws), ws_bytes,
                                   _stream()))
     return out

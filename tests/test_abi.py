@@ -100,7 +100,9 @@ def test_grouped_rejects_bad_arguments(lib):
     args = lambda **kw: (kw.get("mode", 1), kw.get("flags", 0), kw.get("x", 0x4000),
                          kw.get("off", 0x6000), kw.get("rows", 8), ctypes.byref(w),
                          kw.get("y", 0x5000), None, 0, None)
-    assert lib.dps_linear_grouped(*args(flags=1)) == 3
+    assert lib.dps_linear_grouped(*args(flags=2)) == 1            # unknown flags
+    assert lib.dps_linear_grouped(*args(mode=0, flags=1)) == 1    # FP8 needs fast mode
+    assert lib.dps_linear_grouped(*args(flags=1)) == 4            # FP8 staging: no workspace
     assert lib.dps_linear_grouped(*args(off=0)) == 1
     assert lib.dps_linear_grouped(*args(off=0x6002)) == 2
     assert lib.dps_linear_grouped(*args(rows=-3)) == 1
@@ -214,6 +216,9 @@ def test_plan_info_names_the_kernel_of_each_shape_class(lib):
     assert (p["kernel"], p["tile_rows"], p["tile_tokens"]) == ("gemm_fp8", 256, 256)
     p = d.plan_info(1, "fp8", 2048, 6144, 4096)
     assert (p["kernel"], p["tile_rows"], p["tile_tokens"]) == ("gemm_fp8", 256, 128)
+    p = d.plan_info(1, "fp8", 8192, 28672, 4096, experts=8)   # grouped: 128-token tiles
+    assert (p["kernel"], p["tile_rows"], p["tile_tokens"]) == ("gemm_fp8", 256, 128)
+    assert d.workspace_bytes(1, 1, 1024, 4096, 14336, 8) >= 1024 * 14336 + 1024 * 4
     # the workspace query follows the same plan
     for mode, act, m, n, k in ((0, "fp16", 128, 4096, 4096), (1, "fp8", 512, 4096, 4096)):
         p = d.plan_info(mode, act, m, n, k)

@@ -1,17 +1,19 @@
-"""bench.py's command-line contract on the host: it measures one GPU and
-refuses more, before anything touches a device."""
+"""bench.py's contract: on the host it refuses more than one GPU before
+anything touches a device; on the GPU a short run prints the one JSON line."""
 import os
 import subprocess
 import sys
 
+import pytest
+
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
-def _run(args, env_extra=None):
+def _run(args, env_extra=None, timeout=120):
     env = dict(os.environ)
     env.update(env_extra or {})
     return subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *args], cwd=ROOT,
-                          env=env, capture_output=True, text=True, timeout=120)
+                          env=env, capture_output=True, text=True, timeout=timeout)
 
 
 def test_more_than_one_gpu_is_refused():
@@ -36,3 +38,29 @@ def test_percentile_helper_is_nearest_rank():
     assert bench.pct(ts, 90) == 10.0e-3
     assert bench.pct(ts, 100) == 11.0e-3
     assert bench.pct([4.0], 10) == 4.0e-3
+
+
+@pytest.mark.gpu
+def test_bench_line_on_the_gpu():
+    """One short run of the decode-step benchmark: one JSON line with the
+    contract's keys, and per-call spreads that bracket their medians."""
+    import json
+
+    r = _run(["--steps", "3", "--warmup", "1", "--no-secondary", "--no-cpu-baseline",
+              "--roofline-reps", "4"], timeout=600)
+    assert r.returncode == 0, r.stderr[-2000:]
+    lines = [ln for ln in r.stdout.splitlines() if ln.strip()]
+    assert len(lines) == 1
+    d = json.loads(lines[0])
+    for key in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step",
+                "higher_is_better", "scaling", "vs_baseline", "dtype", "data", "config",
+                "roofline", "breakdown"):
+        assert key in d, key
+    assert d["n_gpus"] == 1 and d["steps"] == 3 and d["value"] > 0
+    assert d["config"]["workload"]
+    rl = d["roofline"]
+    assert rl["bound"] in ("hbm", "mfma")
+    assert 0 < rl["frac"] == pytest.approx(rl["achieved"] / rl["peak"], abs=1e-3)
+    assert len(d["breakdown"]) == 40
+    for c in d["breakdown"]:
+        assert 0 < c["us_p10"] <= c["us"] <= c["us_p90"], c

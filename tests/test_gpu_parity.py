@@ -444,6 +444,40 @@ def test_grouped_single_expert_workspace_and_values(m):
         assert_close(y, ref, "m=%d mode=%d" % (m, mode))
 
 
+@pytest.mark.parametrize("counts,n,k", [
+    ((5, 0, 17, 64, 1, 3), 192, 512),                  # short groups, an empty expert
+    ((100, 0, 300, 129, 7), 160, 1024),                # ragged 128-token tiles, weight-tile tail
+    ((128, 140, 120, 133, 110, 125, 131, 137), 256, 256),
+    ((300, 0, 41), 256, 4096),                         # few weight tiles: K split
+])
+@pytest.mark.parametrize("enc", [dps.ENC_E5M2, dps.ENC_E4M3], ids=["e5m2", "e4m3"])
+def test_grouped_fp8_matches_oracle(counts, n, k, enc):
+    """Grouped fast mode with FP8 activations: every row quantized with its
+    own scale, then each expert's rows against its upper bytes."""
+    e = len(counts)
+    rows = sum(counts)
+    w = workloads.weight_fp16(n, k, seed=91, experts=e)
+    x = workloads.activations_fp16(rows, k, seed=92, outlier_frac=0.01, outlier_scale=20.0)
+    offsets = np.zeros(e + 1, dtype=np.int64)
+    offsets[1:] = np.cumsum(counts)
+    nst = Nested(w, 16, enc=enc)
+    off_dev = torch.from_numpy(offsets.astype(np.int32)).to(DEV)
+    p = dps.plan_info(FAST, "fp8", rows, n, k, experts=e)
+    assert p["kernel"] == "gemm_fp8"
+    if k == 4096:
+        assert p["splits"] > 1
+    y = dps.linear_grouped(x.to(DEV), off_dev, nst.nw, FAST, act="fp8")
+    torch.cuda.synchronize()
+    xq, s = oracle.act_quant(u16(x))
+    oenc = oracle.E4M3 if enc == dps.ENC_E4M3 else oracle.E5M2
+    ref = np.zeros((rows, n))
+    for ex in range(e):
+        r0, r1 = offsets[ex], offsets[ex + 1]
+        if r1 > r0:
+            ref[r0:r1] = oracle.linear_fp8(xq[r0:r1], s[r0:r1], nst.hi_ref[ex], enc=oenc)
+    assert_close(y, ref)
+
+
 def test_grouped_single_expert_equals_dense():
     n, k, m = 300, 512, 90
     w = workloads.weight_fp16(n, k, seed=71)

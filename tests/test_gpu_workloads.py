@@ -11,8 +11,9 @@ weight tensor.  Which rows are checked follows the call's launch plan
   - decode (hidden-4096 set, M in {1, 8, 32, 128, 256}): every row up to
     32 tokens, else two seeded rows of every 16-row sub-tile of the first
     and the last token tile;
-  - MoE (8 experts, hidden 4096, ffn 14336, 512 tokens routed top-2): one
-    seeded row of every 16-row sub-tile of every expert's rows;
+  - MoE (8 experts, hidden 4096, ffn 14336, 512 tokens routed top-2), both
+    modes and fast mode with FP8 activations: one seeded row of every 16-row
+    sub-tile of every expert's rows;
   - hidden-8192 decode set at M = 64 with residual chunks at random slots of
     a pool whose other slots hold 16-token FP16 KV blocks, modes alternating
     call to call.
@@ -177,6 +178,25 @@ def test_moe_grouped(moe, mode):
                                     LOG2C)
             ref = oracle.linear_rows(_omode(mode), u16(xs), rows, nst.hi_ref[e],
                                      res_e if mode == FULL else None, enc=nst.enc)
+            assert_close(y[torch.from_numpy(rows).to(DEV)], ref, "%s expert %d" % (name, e))
+
+
+def test_moe_grouped_fp8(moe):
+    """The MoE layers in fast mode with FP8 activations: every routed row
+    quantized on its own, each expert's rows on the FP8 matrix cores."""
+    offsets, layers = moe
+    off_dev = torch.from_numpy(offsets.numpy().astype(np.int32)).to(DEV)
+    experts = len(offsets) - 1
+    rng = np.random.default_rng(840)
+    for name, n, k, nst, xs in layers:
+        y = dps.linear_grouped(xs.to(DEV), off_dev, nst.nw, FAST, act="fp8")
+        torch.cuda.synchronize()
+        xq, sc = oracle.act_quant(u16(xs))
+        for e in range(experts):
+            r0, r1 = int(offsets[e]), int(offsets[e + 1])
+            rows = np.array([int(rng.integers(s0, min(s0 + 16, r1))) for s0 in range(r0, r1, 16)],
+                            dtype=np.int64)
+            ref = oracle.linear_fp8(xq[rows], sc[rows], nst.hi_ref[e], enc=nst.enc)
             assert_close(y[torch.from_numpy(rows).to(DEV)], ref, "%s expert %d" % (name, e))
 
 
