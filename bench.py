@@ -305,9 +305,11 @@ def pct(sorted_ms, q):
 def measured_ceilings(torch, stream):
     """What the part delivers, from libdps_probe: a 512 MiB buffer read once
     with 16-byte loads (plain and nontemporal; 2048 blocks of 256 threads,
-    grid-stride), and back-to-back FP16 16x16x32 / FP8 16x16x128 MFMAs on
-    register operands (2048 blocks of four waves, 8 x 512 MFMAs per wave).
-    Best of five launches each, HIP events on the launching stream."""
+    grid-stride), back-to-back FP16 16x16x32 / FP8 16x16x128 MFMAs on
+    register operands (2048 blocks of four waves, 8 x 512 MFMAs per wave),
+    and the GEMMs' global -> LDS fill alone per CU (4, 8 or 16 issuing
+    waves).  Best of five launches each, HIP events on the launching
+    stream."""
     from paper_2609_34380_amd import probe
 
     dev = torch.device("cuda:0")
@@ -338,11 +340,23 @@ def measured_ceilings(torch, stream):
             t = best(lambda: probe.mfma(fp8, iters, facc))
             flops = 2048 * 4 * 8 * iters * probe.FLOPS_PER_MFMA[fp8]
             res[key] = round(flops / t / 1e12, 1)
-        del buf, out, facc
+        cus = torch.cuda.get_device_properties(dev).multi_processor_count
+        fout = torch.empty(cus, dtype=torch.int32, device=dev)
+        fill = {}
+        stages = 400
+        for window, wname in ((1 << 20, "l2_1MiB"), (512 << 20, "hbm_512MiB")):
+            for loaders in (4, 8, 16):
+                t = best(lambda: probe.lds_fill(buf, window, loaders, stages, fout))
+                fill["%s_%dwaves" % (wname, loaders)] = round(65536 * stages / t / 1e9, 1)
+        res["lds_fill_GBs_per_CU"] = fill
+        del buf, out, facc, fout
     torch.cuda.synchronize()
     res["what"] = ("stream read: 512 MiB once, 16-byte loads, 2048 blocks x 256 threads, one "
                    "contiguous chunk per block; MFMA loop: "
-                   "register operands, 2048 blocks x 4 waves x 4096 MFMAs; best of 5")
+                   "register operands, 2048 blocks x 4 waves x 4096 MFMAs; LDS fill: one block "
+                   "per CU, 4/8/16 waves issuing direct-to-LDS loads (8 rows x 128 B per "
+                   "instruction, rows 4 KiB apart) into 64 KiB stages, 400 stages, from a 1 MiB "
+                   "(L2-resident) or 512 MiB window, GB/s per CU; best of 5")
     return res
 
 

@@ -5,7 +5,7 @@
  * its published peaks.  A separate library (libdps_probe.so), not part of the
  * nested-linear boundary in dps.h.
  *
- * Both calls enqueue one kernel on `stream` (a hipStream_t) and return 0, or
+ * Each call enqueues one kernel on `stream` (a hipStream_t) and returns 0, or
  * 1 for a bad argument (nothing enqueued), or 5 if the launch failed.  Time
  * them with events around the enqueued work.
  */
@@ -30,6 +30,16 @@ int dps_probe_stream_read(const void *buf, int64_t bytes, int nontemporal, uint3
  * fp8 != 0: v_mfma_f32_16x16x128_f8f6f4 with E4M3 operands, 65536 flops
  * each).  out: device float[blocks * 256]. */
 int dps_probe_mfma(int fp8, int iters, int64_t blocks, float *out, void *stream);
+
+/* The global -> LDS fill of the GEMMs, alone: `blocks` blocks (one per CU
+ * when blocks = CUs; 128 KiB of LDS each) of `loaders` waves (4, 8 or 16),
+ * which fill iters stages of 64 KiB by direct-to-LDS loads of 8 rows x 128
+ * bytes per instruction from rows 4 KiB apart inside the first window_bytes
+ * of buf, into a two-slot ring with one barrier per stage.  Bytes moved:
+ * 65536 * iters * blocks.  buf: device, 16-byte aligned; window_bytes a
+ * multiple of 4096, at least 1 MiB.  out: device uint32[blocks]. */
+int dps_probe_lds_fill(const void *buf, int64_t window_bytes, int loaders, int iters,
+                       int64_t blocks, uint32_t *out, void *stream);
 
 #ifdef __cplusplus
 }

@@ -9,6 +9,10 @@
 //   - mfma_loop_kernel: back-to-back MFMAs on register operands, eight
 //     independent accumulator chains per wave, FP16 16x16x32 or FP8
 //     16x16x128, nothing from memory inside the loop.
+//   - lds_fill_kernel: the GEMMs' global -> LDS fill alone: one block per
+//     CU, NL waves issuing direct-to-LDS loads of 8 rows x 128 bytes per
+//     instruction (rows 4 KiB apart, the weight planes' pitch at K = 4096)
+//     into 64 KiB stages of a two-slot ring, one barrier per stage.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -109,6 +113,43 @@ __global__ __launch_bounds__(512) void mfma_loop_kernel(int iters, float seed, f
     out[(int64_t)blockIdx.x * kThreads + threadIdx.x] = s;
 }
 
+// NL loader waves fill 64 KiB per stage (64 / NL instructions each) into
+// slot t & 1 while the previous stage's slot is free; every wave waits for
+// its own loads and meets the others at one barrier per stage.  Stage t of
+// block b covers rows b * 2048 + 512 t (mod the window's rows) at byte column
+// 128 (t mod 32) of each 4 KiB row: every address stays inside the window.
+template <int NL>
+__global__ __launch_bounds__(NL * 64) void lds_fill_kernel(const uint8_t *src, int64_t rows,
+                                                           int iters, uint32_t *out)
+{
+    constexpr int G = 64 / NL;
+    __shared__ __attribute__((aligned(16))) uint8_t ring[2][65536];
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    auto issue = [&](int t) {
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+            const int ins = wave * G + j;  // 0 .. 63
+            const int64_t row =
+                ((int64_t)blockIdx.x * 2048 + (int64_t)t * 512 + ins * 8) % (rows - 8) + (lane >> 3);
+            const uint8_t *g = src + row * 4096 + (t & 31) * 128 + (lane & 7) * 16;
+            __builtin_amdgcn_global_load_lds(
+                g, (__attribute__((address_space(3))) void *)&ring[t & 1][ins * 1024], 16, 0, 0);
+        }
+    };
+    issue(0);
+    for (int t = 0; t < iters; ++t) {
+        __builtin_amdgcn_s_waitcnt(0);  // this wave's loads of stage t have landed
+        __syncthreads();
+        if (t + 1 < iters)
+            issue(t + 1);
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0)
+        out[blockIdx.x] = *reinterpret_cast<const uint32_t *>(&ring[(iters - 1) & 1][0]);
+}
+
 }  // namespace
 
 DPS_PROBE_EXPORT int dps_probe_stream_read(const void *buf, int64_t bytes, int nontemporal,
@@ -140,5 +181,34 @@ DPS_PROBE_EXPORT int dps_probe_mfma(int fp8, int iters, int64_t blocks, float *o
     else
         hipLaunchKernelGGL(mfma_loop_kernel<0>, grid, dim3(kThreads), 0, (hipStream_t)stream,
                            iters, 0.5f, out);
+    return hipGetLastError() == hipSuccess ? 0 : 5;
+}
+
+DPS_PROBE_EXPORT int dps_probe_lds_fill(const void *buf, int64_t window_bytes, int loaders,
+                                        int iters, int64_t blocks, uint32_t *out, void *stream)
+{
+    if (buf == nullptr || out == nullptr || window_bytes < (int64_t(1) << 20) ||
+        window_bytes % 4096 != 0 || iters < 1 || blocks < 1 || blocks > (1 << 20) ||
+        ((uintptr_t)buf & 15) != 0)
+        return 1;
+    const dim3 grid((unsigned)blocks);
+    const int64_t rows = window_bytes / 4096;
+    const uint8_t *src = static_cast<const uint8_t *>(buf);
+    switch (loaders) {
+    case 4:
+        hipLaunchKernelGGL(lds_fill_kernel<4>, grid, dim3(256), 0, (hipStream_t)stream, src, rows,
+                           iters, out);
+        break;
+    case 8:
+        hipLaunchKernelGGL(lds_fill_kernel<8>, grid, dim3(512), 0, (hipStream_t)stream, src, rows,
+                           iters, out);
+        break;
+    case 16:
+        hipLaunchKernelGGL(lds_fill_kernel<16>, grid, dim3(1024), 0, (hipStream_t)stream, src,
+                           rows, iters, out);
+        break;
+    default:
+        return 1;
+    }
     return hipGetLastError() == hipSuccess ? 0 : 5;
 }

@@ -1,7 +1,7 @@
 """Python binding of libdps_probe (include/dps_probe.h): the measured ceilings
 of the MI355X units the nested linear layer is bound by -- a streaming read
-of HBM with 16-byte loads, and back-to-back FP16 / FP8 MFMAs on register
-operands.  Argument marshalling only; the kernels are in dps_probe.hip.
+of HBM with 16-byte loads, back-to-back FP16 / FP8 MFMAs on register
+operands, and the GEMMs' global -> LDS fill per CU.  Argument marshalling only; the kernels are in dps_probe.hip.
 Not part of the nested-linear boundary: the benchmark states its roofline
 fractions against these as well as against the published peaks.
 """
@@ -12,7 +12,7 @@ import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libdps_probe.so")
-EXPORTED = ("dps_probe_stream_read", "dps_probe_mfma")
+EXPORTED = ("dps_probe_stream_read", "dps_probe_mfma", "dps_probe_lds_fill")
 FLOPS_PER_MFMA = {0: 16384, 1: 65536}  # 16x16x32 FP16, 16x16x128 FP8
 
 _lib = None
@@ -30,6 +30,8 @@ def load_library(path=LIB_PATH):
     lib.dps_probe_stream_read.restype = C
     lib.dps_probe_mfma.argtypes = [C, C, I64, P, P]
     lib.dps_probe_mfma.restype = C
+    lib.dps_probe_lds_fill.argtypes = [P, I64, C, C, I64, P, P]
+    lib.dps_probe_lds_fill.restype = C
     _lib = lib
     return lib
 
@@ -61,3 +63,15 @@ def mfma(fp8, iters, out):
     assert out.is_cuda and out.dtype == torch.float32 and out.numel() % 256 == 0
     _check(lib.dps_probe_mfma(1 if fp8 else 0, int(iters), out.numel() // 256,
                               ctypes.c_void_p(out.data_ptr()), _stream()), "dps_probe_mfma")
+
+
+def lds_fill(buf, window_bytes, loaders, stages, out):
+    """One block per element of out (int32 device tensor; use one per CU),
+    each with `loaders` waves filling `stages` 64 KiB stages of LDS from the
+    first window_bytes of the uint8 device tensor buf."""
+    lib = load_library()
+    assert buf.is_cuda and buf.dtype == torch.uint8 and buf.numel() >= window_bytes
+    assert out.is_cuda and out.dtype == torch.int32 and out.is_contiguous()
+    _check(lib.dps_probe_lds_fill(ctypes.c_void_p(buf.data_ptr()), int(window_bytes), int(loaders),
+                                  int(stages), out.numel(), ctypes.c_void_p(out.data_ptr()),
+                                  _stream()), "dps_probe_lds_fill")

@@ -271,6 +271,11 @@ def test_probe_library_exports_its_header():
     assert plib.dps_probe_mfma(0, 0, 4, 0x1000, None) == 1
     assert plib.dps_probe_mfma(1, 8, 0, 0x1000, None) == 1
     assert plib.dps_probe_mfma(0, 8, 4, None, None) == 1
+    # window under 1 MiB or not whole 4 KiB rows, loader count not 4/8/16
+    assert plib.dps_probe_lds_fill(0x1000, 1 << 19, 8, 4, 4, 0x2000, None) == 1
+    assert plib.dps_probe_lds_fill(0x1000, (1 << 20) + 16, 8, 4, 4, 0x2000, None) == 1
+    assert plib.dps_probe_lds_fill(0x1000, 1 << 20, 6, 4, 4, 0x2000, None) == 1
+    assert plib.dps_probe_lds_fill(0x1000, 1 << 20, 8, 0, 4, 0x2000, None) == 1
 
 
 def test_dense_grid_limit_is_refused_on_the_host(lib):

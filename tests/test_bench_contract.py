@@ -64,3 +64,21 @@ def test_bench_line_on_the_gpu():
     assert len(d["breakdown"]) == 40
     for c in d["breakdown"]:
         assert 0 < c["us_p10"] <= c["us"] <= c["us_p90"], c
+
+
+@pytest.mark.gpu
+def test_ceiling_probes_on_the_gpu():
+    """bench.py --ceilings: the probe kernels run, and what they measure is
+    positive and within the published peaks (HBM 8 TB/s, FP16 2.5 and FP8
+    5.0 PFLOP/s dense); the LDS fill grows with the issuing waves on
+    L2-resident data."""
+    import json
+
+    r = _run(["--ceilings"], timeout=300)
+    assert r.returncode == 0, r.stderr[-2000:]
+    c = json.loads(r.stdout.strip().splitlines()[-1])["ceilings"]
+    assert 0 < c["hbm_read_GBs_plain"] <= 8000 and 0 < c["hbm_read_GBs_nontemporal"] <= 8000
+    assert 0 < c["mfma_f16_TFLOPs"] <= 2500 and 0 < c["mfma_fp8_TFLOPs"] <= 5000
+    fill = c["lds_fill_GBs_per_CU"]
+    assert len(fill) == 6 and all(v > 0 for v in fill.values())
+    assert fill["l2_1MiB_16waves"] > fill["l2_1MiB_4waves"]
