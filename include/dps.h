@@ -346,6 +346,56 @@ dps_status dps_sum_counts(const dps_sum *s, int64_t *counts);
 dps_status dps_sum_slots(const dps_sum *s, int64_t residual, int64_t chunks_per_unit,
                          int64_t n_chunks, int32_t *slots_host);
 
+/* ------------------------------------------------------------------------
+ * Shared region through the HIP virtual memory API (Sec. IV-B "Shared
+ * Region", dual-mapping property): n_units physical units of unit_bytes
+ * each, mapped once in unit order into the KV view and again, per residual
+ * tensor, into a residual view whose piece i maps the unit holding the
+ * tensor's chunk i.  The residual view is contiguous, so the residual
+ * descriptor {pool = view, pool_bytes = count * unit_bytes, slots = the
+ * identity table 0 .. count-1, log2_chunk = log2(unit_bytes)} addresses it
+ * in every call above, and a byte written through either view is the same
+ * physical byte.  This is the optional allocator of the region (the linear
+ * path itself never allocates).  Mapping changes are not ordered with work
+ * queued on any stream: nothing that uses a view may run while the view is
+ * remapped or unmapped.  Host calls; they work on the device current at
+ * dps_vmm_create and leave the caller's current device as it was.  A HIP
+ * runtime without VMM support gives DPS_ERR_UNSUPPORTED.
+ * ------------------------------------------------------------------------ */
+typedef struct dps_vmm dps_vmm;
+
+/* Minimum VMM allocation granularity of the current device, bytes. */
+dps_status dps_vmm_granularity(int64_t *bytes_out);
+
+/* n_units (1..2^20) units of unit_bytes (a power of two, 4 KiB..1 GiB, a
+ * multiple of the granularity) on the current device, all mapped into the
+ * KV view.  *out is owned by the caller (dps_vmm_destroy). */
+dps_status dps_vmm_create(int64_t n_units, int64_t unit_bytes, dps_vmm **out);
+
+/* The KV view: device address of n_units * unit_bytes bytes, unit u at
+ * u * unit_bytes (NULL for a NULL region). */
+void *dps_vmm_kv_view(const dps_vmm *v);
+int64_t dps_vmm_unit_bytes(const dps_vmm *v);
+
+/* A new residual view of count (1..64 * n_units) pieces, piece i mapping
+ * unit units_host[i] (host int32, each in 0..n_units-1); *view_out its
+ * device address. */
+dps_status dps_vmm_map_residual(dps_vmm *v, const int32_t *units_host, int64_t count,
+                                void **view_out);
+
+/* Map unit `unit` at piece `piece` of a residual view instead of the unit
+ * there (a residual restored into another unit). */
+dps_status dps_vmm_remap(dps_vmm *v, void *view, int64_t piece, int32_t unit);
+
+/* Unmap a residual view and free its address range. */
+dps_status dps_vmm_unmap_residual(dps_vmm *v, void *view);
+
+/* Unmap every view and release the units (NULL: no-op). */
+void dps_vmm_destroy(dps_vmm *v);
+
+/* Detail of the last dps_vmm_* error on the calling thread ("" if none). */
+const char *dps_vmm_last_error(void);
+
 /* Static description of a status code. */
 const char *dps_status_str(dps_status s);
 

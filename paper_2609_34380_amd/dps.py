@@ -30,7 +30,10 @@ EXPORTED = ("dps_select_enc", "dps_split", "dps_merge", "dps_restore", "dps_back
             "dps_plan_info", "dps_linear", "dps_linear_static", "dps_linear_grouped", "dps_status_str", "dps_last_error",
             "dps_sum_create", "dps_sum_destroy", "dps_sum_alloc", "dps_sum_free",
             "dps_sum_restore_begin", "dps_sum_restore_done", "dps_sum_mode",
-            "dps_sum_unit_state", "dps_sum_unit_of", "dps_sum_counts", "dps_sum_slots")
+            "dps_sum_unit_state", "dps_sum_unit_of", "dps_sum_counts", "dps_sum_slots",
+            "dps_vmm_granularity", "dps_vmm_create", "dps_vmm_kv_view", "dps_vmm_unit_bytes",
+            "dps_vmm_map_residual", "dps_vmm_remap", "dps_vmm_unmap_residual", "dps_vmm_destroy",
+            "dps_vmm_last_error")
 
 
 class DpsError(RuntimeError):
@@ -112,6 +115,24 @@ def load_library(path=LIB_PATH):
     lib.dps_sum_counts.restype = ST
     lib.dps_sum_slots.argtypes = [P, I64, I64, I64, P]
     lib.dps_sum_slots.restype = ST
+    lib.dps_vmm_granularity.argtypes = [PI64]
+    lib.dps_vmm_granularity.restype = ST
+    lib.dps_vmm_create.argtypes = [I64, I64, ctypes.POINTER(P)]
+    lib.dps_vmm_create.restype = ST
+    lib.dps_vmm_kv_view.argtypes = [P]
+    lib.dps_vmm_kv_view.restype = P
+    lib.dps_vmm_unit_bytes.argtypes = [P]
+    lib.dps_vmm_unit_bytes.restype = I64
+    lib.dps_vmm_map_residual.argtypes = [P, P, I64, ctypes.POINTER(P)]
+    lib.dps_vmm_map_residual.restype = ST
+    lib.dps_vmm_remap.argtypes = [P, P, I64, I32]
+    lib.dps_vmm_remap.restype = ST
+    lib.dps_vmm_unmap_residual.argtypes = [P, P]
+    lib.dps_vmm_unmap_residual.restype = ST
+    lib.dps_vmm_destroy.argtypes = [P]
+    lib.dps_vmm_destroy.restype = None
+    lib.dps_vmm_last_error.argtypes = []
+    lib.dps_vmm_last_error.restype = ctypes.c_char_p
     lib.dps_status_str.argtypes = [ST]
     lib.dps_status_str.restype = ctypes.c_char_p
     lib.dps_last_error.argtypes = []
@@ -447,3 +468,82 @@ class SumManager:
         _check(_lib.dps_sum_slots(self._h, residual, chunks_per_unit, n_chunks,
                                   ctypes.c_void_p(out.data_ptr())))
         return out[:n_chunks]
+
+
+class _DeviceBytes:
+    """A __cuda_array_interface__ over device bytes the library mapped, so
+    torch can view them (torch.as_tensor) without owning them."""
+
+    def __init__(self, ptr, nbytes):
+        self.__cuda_array_interface__ = {"shape": (int(nbytes),), "typestr": "|u1",
+                                         "data": (int(ptr), False), "version": 3,
+                                         "strides": None}
+
+
+def _check_vmm(status):
+    if status != 0:
+        raise DpsError(status, _lib.dps_vmm_last_error().decode())
+
+
+def vmm_granularity():
+    """Minimum VMM allocation granularity of the current device, bytes."""
+    lib = load_library()
+    g = ctypes.c_int64()
+    _check_vmm(lib.dps_vmm_granularity(ctypes.byref(g)))
+    return g.value
+
+
+class VmmRegion:
+    """The shared region through the HIP virtual memory API (dps_vmm_*):
+    n_units physical units of unit_bytes, all mapped into the KV view
+    (`kv`, a uint8 device tensor over n_units * unit_bytes), and residual
+    views mapping chosen units in chunk order.  The tensors returned view
+    memory the region owns: drop them before unmapping or closing."""
+
+    def __init__(self, n_units, unit_bytes, device=None):
+        lib = load_library()
+        self.device = torch.device(device) if device is not None else torch.device(
+            "cuda", torch.cuda.current_device())
+        h = ctypes.c_void_p()
+        with torch.cuda.device(self.device):
+            _check_vmm(lib.dps_vmm_create(n_units, unit_bytes, ctypes.byref(h)))
+        self._h = h
+        self.n_units, self.unit_bytes = int(n_units), int(unit_bytes)
+        self.log2_unit = self.unit_bytes.bit_length() - 1
+        self.kv = torch.as_tensor(_DeviceBytes(lib.dps_vmm_kv_view(h), n_units * unit_bytes),
+                                  device=self.device)
+
+    def map_residual(self, units):
+        """A residual view (uint8 device tensor of len(units) * unit_bytes)
+        whose piece i maps unit units[i]."""
+        arr = (ctypes.c_int32 * len(units))(*[int(u) for u in units])
+        va = ctypes.c_void_p()
+        _check_vmm(_lib.dps_vmm_map_residual(self._h, arr, len(units), ctypes.byref(va)))
+        return torch.as_tensor(_DeviceBytes(va.value, len(units) * self.unit_bytes),
+                               device=self.device)
+
+    def remap(self, view, piece, unit):
+        _check_vmm(_lib.dps_vmm_remap(self._h, ctypes.c_void_p(view.data_ptr()), int(piece),
+                                      int(unit)))
+
+    def unmap(self, view):
+        _check_vmm(_lib.dps_vmm_unmap_residual(self._h, ctypes.c_void_p(view.data_ptr())))
+
+    def residual(self, view):
+        """The Residual descriptor of a view: the view as its pool, the
+        identity chunk table, chunks of one unit."""
+        n = view.numel() // self.unit_bytes
+        slots = torch.arange(n, dtype=torch.int32, device=self.device)
+        return Residual(view, slots, self.log2_unit)
+
+    def close(self):
+        if self._h:
+            self.kv = None
+            _lib.dps_vmm_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

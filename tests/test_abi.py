@@ -287,3 +287,20 @@ def test_dense_grid_limit_is_refused_on_the_host(lib):
     st = lib.dps_linear(1, 0, 0x4000, rows, ctypes.byref(w), 0x5000, None, 0, None)
     assert st == 3, st
     assert b"too large for one grid" in lib.dps_last_error()
+
+
+def test_vmm_rejects_bad_arguments_on_the_host(lib):
+    """The shared-region calls check their arguments before any HIP call."""
+    out = ctypes.c_void_p()
+    assert lib.dps_vmm_create(0, 1 << 21, ctypes.byref(out)) == 1          # no units
+    assert lib.dps_vmm_create(4, 3 << 20, ctypes.byref(out)) == 1          # not a power of two
+    assert b"power of two" in lib.dps_vmm_last_error()
+    assert lib.dps_vmm_create(4, 2048, ctypes.byref(out)) == 1             # under 4 KiB
+    assert lib.dps_vmm_create(4, 1 << 21, None) == 1
+    units = (ctypes.c_int32 * 2)(0, 1)
+    assert lib.dps_vmm_map_residual(None, units, 2, ctypes.byref(out)) == 1
+    assert lib.dps_vmm_remap(None, 0x1000, 0, 0) == 1
+    assert lib.dps_vmm_unmap_residual(None, 0x1000) == 1
+    assert lib.dps_vmm_kv_view(None) is None
+    assert lib.dps_vmm_unit_bytes(None) == 0
+    lib.dps_vmm_destroy(None)
