@@ -48,7 +48,8 @@ typedef enum {
     DPS_ERR_UNSUPPORTED = 3, /* valid request the library does not implement */
     DPS_ERR_WORKSPACE = 4,   /* workspace missing or smaller than required   */
     DPS_ERR_HIP = 5,         /* the HIP runtime reported an error on launch  */
-    DPS_ERR_NO_SPACE = 6     /* SUM manager: not enough room for the request */
+    DPS_ERR_NO_SPACE = 6,    /* SUM manager: not enough room for the request */
+    DPS_ERR_TIMEOUT = 7      /* restore worker: still busy when the wait ended */
 } dps_status;
 
 /* Precision mode of one call; a whole forward pass runs in one mode
@@ -345,6 +346,48 @@ dps_status dps_sum_counts(const dps_sum *s, int64_t *counts);
  * residual must be bound or being restored (else DPS_ERR_INVALID_ARG). */
 dps_status dps_sum_slots(const dps_sum *s, int64_t residual, int64_t chunks_per_unit,
                          int64_t n_chunks, int32_t *slots_host);
+
+/* ------------------------------------------------------------------------
+ * Restore worker (Sec. IV-B "SUM manager": a background thread drains the
+ * restore queue; Sec. IV-C restoration paragraph: copies on their own
+ * stream, beside fast-mode passes).  A host thread that, each time it is
+ * woken, takes restores from the SUM manager for as long as it hands them
+ * out (dps_sum_restore_begin): it rewrites the residual's device chunk table
+ * (res.slots, chunks_per_unit slots per unit, dps_sum_slots) to the unit it
+ * was given, copies the host backup into those slots (as dps_restore, in
+ * copies of at most copy_bytes) on a stream of its own, waits for them and
+ * reports dps_sum_restore_done.  The SUM manager is safe to call from the
+ * serving loop meanwhile; it must outlive the worker.  Only full-mode calls
+ * read a residual, and the mode is full only after every copy completed.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+    const uint8_t *backup; /* host backup of the residual's logical stream
+                              (dps_backup), pinned for asynchronous copies  */
+    int64_t numel;         /* its bytes                                       */
+    dps_residual res;      /* the descriptor the linear calls use; the worker
+                              rewrites the device table res.slots points to   */
+} dps_restore_target;
+
+typedef struct dps_restore_worker dps_restore_worker;
+
+/* A worker for the SUM manager's residuals 0 .. n_targets-1 (targets: host
+ * array, copied; each residual's n_chunks at most chunks_per_unit), on the
+ * current device.  Free it with dps_restore_worker_destroy. */
+dps_status dps_restore_worker_create(dps_sum *sum, const dps_restore_target *targets,
+                                     int64_t n_targets, int64_t chunks_per_unit,
+                                     int64_t copy_bytes, dps_restore_worker **out);
+/* Wake the worker (after KV blocks were freed, or any time). */
+dps_status dps_restore_worker_kick(dps_restore_worker *w);
+/* Wait until the worker has taken up every wake-up and has nothing left it
+ * can restore: DPS_OK, DPS_ERR_TIMEOUT after timeout_ms, or the error that
+ * stopped the worker (it then restores nothing more). */
+dps_status dps_restore_worker_wait_idle(dps_restore_worker *w, int64_t timeout_ms);
+/* Residuals restored so far (-1 for NULL). */
+int64_t dps_restore_worker_restored(dps_restore_worker *w);
+/* Stop the thread (a restore in progress completes first) and free it. */
+void dps_restore_worker_destroy(dps_restore_worker *w);
+/* Detail of the last dps_restore_worker_* error on the calling thread. */
+const char *dps_restore_worker_last_error(void);
 
 /* ------------------------------------------------------------------------
  * Shared region through the HIP virtual memory API (Sec. IV-B "Shared

@@ -19,7 +19,8 @@ LIB = os.path.join(PKG, "libdps.so")
 PROBE_LIB = os.path.join(PKG, "libdps_probe.so")
 PROBE_SOURCES = ["dps_probe.hip"]
 SOURCES = ["dps_elementwise.hip", "dps_skinny.hip", "dps_gemv.hip", "dps_rows.hip", "dps_gemm.hip",
-           "dps_restore.hip", "dps_api.hip", "dps_sum.cpp", "dps_vmm.hip"]
+           "dps_restore.hip", "dps_api.hip", "dps_sum.cpp", "dps_vmm.hip",
+           "dps_worker.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -297,6 +297,7 @@ DPS_EXPORT const char *dps_status_str(dps_status s)
     case DPS_ERR_WORKSPACE: return "workspace too small";
     case DPS_ERR_HIP: return "HIP error";
     case DPS_ERR_NO_SPACE: return "no space";
+    case DPS_ERR_TIMEOUT: return "timed out";
     }
     return "unknown status";
 }

@@ -4,6 +4,9 @@
 // evicted, and the precision mode that follows from it.  Host-only C++; the
 // copies a restore needs are dps_restore's.
 //
+// Every call locks the manager, so a restore worker thread may drive the
+// restores while the serving loop allocates and frees KV blocks.
+//
 // Units are numbered 0 .. n_units-1, each with blocks_per_unit KV blocks
 // (block id = unit * blocks_per_unit + index).  Residual r starts bound to
 // unit r.  Every state set is ordered by unit id and "pop" takes the lowest
@@ -11,6 +14,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <mutex>
 #include <new>
 #include <set>
 #include <vector>
@@ -29,6 +33,9 @@ struct dps_sum {
     std::vector<std::vector<uint8_t>> taken;  // per unit: block index -> allocated
     std::vector<int64_t> unit_of;          // per residual: bound or restoring unit, or -1
     std::vector<int64_t> resident;         // per unit: residual bound to it, or -1
+    // every call holds it: the serving loop and a restore worker thread
+    // (dps_restore_worker_*) may call at the same time
+    mutable std::mutex mu;
 };
 
 namespace {
@@ -102,6 +109,7 @@ DPS_EXPORT dps_status dps_sum_alloc(dps_sum *s, int64_t n, int64_t *blocks)
 {
     if (s == nullptr || n < 0 || (n > 0 && blocks == nullptr))
         return DPS_ERR_INVALID_ARG;
+    std::lock_guard<std::mutex> lock(s->mu);
     int64_t room = (int64_t)(s->free_.size() + s->backed.size()) * s->blocks_per_unit;
     for (int64_t u : s->avail)
         room += s->blocks_per_unit - s->used[u];
@@ -150,6 +158,7 @@ DPS_EXPORT dps_status dps_sum_free(dps_sum *s, const int64_t *blocks, int64_t n,
 {
     if (s == nullptr || n < 0 || (n > 0 && blocks == nullptr))
         return DPS_ERR_INVALID_ARG;
+    std::lock_guard<std::mutex> lock(s->mu);
     if (wake)
         *wake = 0;
     const int64_t total = s->n_units * s->blocks_per_unit;
@@ -188,6 +197,7 @@ DPS_EXPORT dps_status dps_sum_restore_begin(dps_sum *s, int64_t *residual, int64
 {
     if (s == nullptr || residual == nullptr || unit == nullptr)
         return DPS_ERR_INVALID_ARG;
+    std::lock_guard<std::mutex> lock(s->mu);
     *residual = -1;
     *unit = -1;
     if (s->stale.empty() || s->free_.empty())
@@ -208,6 +218,7 @@ DPS_EXPORT dps_status dps_sum_restore_done(dps_sum *s, int64_t residual)
 {
     if (s == nullptr || residual < 0 || residual >= s->n_res)
         return DPS_ERR_INVALID_ARG;
+    std::lock_guard<std::mutex> lock(s->mu);
     const int64_t u = s->unit_of[residual];
     if (u < 0 || s->state[u] != DPS_UNIT_RESTORING || !s->evicted.count(residual))
         return DPS_ERR_INVALID_ARG;
@@ -218,12 +229,19 @@ DPS_EXPORT dps_status dps_sum_restore_done(dps_sum *s, int64_t residual)
     return DPS_OK;
 }
 
-DPS_EXPORT int32_t dps_sum_mode(const dps_sum *s) { return s ? s->mode : -1; }
+DPS_EXPORT int32_t dps_sum_mode(const dps_sum *s)
+{
+    if (s == nullptr)
+        return -1;
+    std::lock_guard<std::mutex> lock(s->mu);
+    return s->mode;
+}
 
 DPS_EXPORT int32_t dps_sum_unit_state(const dps_sum *s, int64_t unit)
 {
     if (s == nullptr || unit < 0 || unit >= s->n_units)
         return -1;
+    std::lock_guard<std::mutex> lock(s->mu);
     return s->state[unit];
 }
 
@@ -231,6 +249,7 @@ DPS_EXPORT int64_t dps_sum_unit_of(const dps_sum *s, int64_t residual)
 {
     if (s == nullptr || residual < 0 || residual >= s->n_res)
         return -1;
+    std::lock_guard<std::mutex> lock(s->mu);
     return s->unit_of[residual];
 }
 
@@ -238,6 +257,7 @@ DPS_EXPORT dps_status dps_sum_counts(const dps_sum *s, int64_t *counts)
 {
     if (s == nullptr || counts == nullptr)
         return DPS_ERR_INVALID_ARG;
+    std::lock_guard<std::mutex> lock(s->mu);
     int64_t free_blocks = 0;
     for (int64_t u : s->avail)
         free_blocks += s->blocks_per_unit - s->used[u];
@@ -261,6 +281,7 @@ DPS_EXPORT dps_status dps_sum_slots(const dps_sum *s, int64_t residual, int64_t 
     if (s == nullptr || residual < 0 || residual >= s->n_res || chunks_per_unit < 1 ||
         n_chunks < 0 || n_chunks > chunks_per_unit || (n_chunks > 0 && slots_host == nullptr))
         return DPS_ERR_INVALID_ARG;
+    std::lock_guard<std::mutex> lock(s->mu);
     const int64_t u = s->unit_of[residual];
     if (u < 0)
         return DPS_ERR_INVALID_ARG;

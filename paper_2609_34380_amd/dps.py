@@ -22,7 +22,7 @@ ACT_FP8_ROWSCALE = 1
 
 _STATUS = {0: "DPS_OK", 1: "DPS_ERR_INVALID_ARG", 2: "DPS_ERR_ALIGNMENT",
            3: "DPS_ERR_UNSUPPORTED", 4: "DPS_ERR_WORKSPACE", 5: "DPS_ERR_HIP",
-           6: "DPS_ERR_NO_SPACE"}
+           6: "DPS_ERR_NO_SPACE", 7: "DPS_ERR_TIMEOUT"}
 ERR_NO_SPACE = 6
 UNIT_FREE, UNIT_BACKED, UNIT_AVAIL, UNIT_FULL, UNIT_RESTORING = 0, 1, 2, 3, 4
 
@@ -33,7 +33,9 @@ EXPORTED = ("dps_select_enc", "dps_split", "dps_merge", "dps_restore", "dps_back
             "dps_sum_unit_state", "dps_sum_unit_of", "dps_sum_counts", "dps_sum_slots",
             "dps_vmm_granularity", "dps_vmm_create", "dps_vmm_kv_view", "dps_vmm_unit_bytes",
             "dps_vmm_map_residual", "dps_vmm_remap", "dps_vmm_unmap_residual", "dps_vmm_destroy",
-            "dps_vmm_last_error")
+            "dps_vmm_last_error", "dps_restore_worker_create", "dps_restore_worker_kick",
+            "dps_restore_worker_wait_idle", "dps_restore_worker_restored",
+            "dps_restore_worker_destroy", "dps_restore_worker_last_error")
 
 
 class DpsError(RuntimeError):
@@ -47,6 +49,10 @@ class CResidual(ctypes.Structure):
     _fields_ = [("pool", ctypes.c_void_p), ("pool_bytes", ctypes.c_int64),
                 ("slots", ctypes.c_void_p), ("n_chunks", ctypes.c_int64),
                 ("log2_chunk", ctypes.c_int32)]
+
+
+class CRestoreTarget(ctypes.Structure):
+    _fields_ = [("backup", ctypes.c_void_p), ("numel", ctypes.c_int64), ("res", CResidual)]
 
 
 class CWeight(ctypes.Structure):
@@ -133,6 +139,18 @@ def load_library(path=LIB_PATH):
     lib.dps_vmm_destroy.restype = None
     lib.dps_vmm_last_error.argtypes = []
     lib.dps_vmm_last_error.restype = ctypes.c_char_p
+    lib.dps_restore_worker_create.argtypes = [P, P, I64, I64, I64, ctypes.POINTER(P)]
+    lib.dps_restore_worker_create.restype = ST
+    lib.dps_restore_worker_kick.argtypes = [P]
+    lib.dps_restore_worker_kick.restype = ST
+    lib.dps_restore_worker_wait_idle.argtypes = [P, I64]
+    lib.dps_restore_worker_wait_idle.restype = ST
+    lib.dps_restore_worker_restored.argtypes = [P]
+    lib.dps_restore_worker_restored.restype = I64
+    lib.dps_restore_worker_destroy.argtypes = [P]
+    lib.dps_restore_worker_destroy.restype = None
+    lib.dps_restore_worker_last_error.argtypes = []
+    lib.dps_restore_worker_last_error.restype = ctypes.c_char_p
     lib.dps_status_str.argtypes = [ST]
     lib.dps_status_str.restype = ctypes.c_char_p
     lib.dps_last_error.argtypes = []
@@ -540,6 +558,52 @@ class VmmRegion:
         if self._h:
             self.kv = None
             _lib.dps_vmm_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class RestoreWorker:
+    """The SUM manager's restore worker (dps_restore_worker_*): a native
+    thread that, when kicked, restores every evicted residual the manager
+    hands out -- rewrites its device chunk table to the new unit, copies the
+    host backup in on its own stream, reports the restore done.
+    targets[r] = (backup pinned uint8 CPU tensor, numel, Residual) of the
+    manager's residual r; the tensors must outlive the worker."""
+
+    def __init__(self, sum_manager, targets, chunks_per_unit, copy_bytes=COPY_BYTES):
+        lib = load_library()
+        arr = (CRestoreTarget * len(targets))()
+        for i, (bk, numel, res) in enumerate(targets):
+            assert bk.dtype == torch.uint8 and not bk.is_cuda and bk.numel() >= numel
+            arr[i] = CRestoreTarget(bk.data_ptr(), int(numel), res.c())
+        self._keep = (sum_manager, targets)
+        h = ctypes.c_void_p()
+        rc = lib.dps_restore_worker_create(sum_manager._h, arr, len(targets), chunks_per_unit,
+                                           copy_bytes, ctypes.byref(h))
+        if rc != 0:
+            raise DpsError(rc, lib.dps_restore_worker_last_error().decode())
+        self._h = h
+
+    def kick(self):
+        _check(_lib.dps_restore_worker_kick(self._h))
+
+    def wait_idle(self, timeout_ms=60000):
+        rc = _lib.dps_restore_worker_wait_idle(self._h, int(timeout_ms))
+        if rc != 0:
+            raise DpsError(rc, _lib.dps_restore_worker_last_error().decode())
+
+    @property
+    def restored(self):
+        return _lib.dps_restore_worker_restored(self._h)
+
+    def close(self):
+        if self._h:
+            _lib.dps_restore_worker_destroy(self._h)
             self._h = ctypes.c_void_p()
 
     def __del__(self):

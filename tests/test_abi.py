@@ -43,9 +43,11 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_status_strings(lib):
-    for code in range(6):
-        assert lib.dps_status_str(code)
+    for code in range(8):
+        assert lib.dps_status_str(code) != b"unknown status"
     assert lib.dps_status_str(0) == b"ok"
+    assert lib.dps_status_str(7) == b"timed out"
+    assert lib.dps_status_str(8) == b"unknown status"
 
 
 def _weight(n=64, k=64, experts=1, enc=0, hi=0x1000, pool=0x2000, slots=0x3000,
@@ -304,3 +306,27 @@ def test_vmm_rejects_bad_arguments_on_the_host(lib):
     assert lib.dps_vmm_kv_view(None) is None
     assert lib.dps_vmm_unit_bytes(None) == 0
     lib.dps_vmm_destroy(None)
+
+
+def test_restore_worker_rejects_bad_arguments_on_the_host(lib):
+    """Worker creation checks the manager, the targets and the sizes before it
+    touches the device; the other calls refuse NULL."""
+    sm = dps.SumManager(4, 8, 2)
+    res = dps.CResidual(0x2000, 8 << 21, 0x3000, 8, 21)
+    good = dps.CRestoreTarget(0x9000, 8 << 21, res)
+    arr = (dps.CRestoreTarget * 2)(good, good)
+    out = ctypes.c_void_p()
+    create = lib.dps_restore_worker_create
+    assert create(None, arr, 2, 8, 4 << 20, ctypes.byref(out)) == 1
+    assert create(sm._h, None, 2, 8, 4 << 20, ctypes.byref(out)) == 1
+    assert create(sm._h, arr, 0, 8, 4 << 20, ctypes.byref(out)) == 1
+    assert create(sm._h, arr, 2, 4, 4 << 20, ctypes.byref(out)) == 1      # 8 chunks > 4 per unit
+    assert create(sm._h, arr, 2, 8, 0, ctypes.byref(out)) == 1
+    big = dps.CRestoreTarget(0x9000, (8 << 21) + 1, res)                   # beyond its chunks
+    assert create(sm._h, (dps.CRestoreTarget * 1)(big), 1, 8, 4 << 20, ctypes.byref(out)) == 1
+    assert b"target 0" in lib.dps_restore_worker_last_error()
+    assert lib.dps_restore_worker_kick(None) == 1
+    assert lib.dps_restore_worker_wait_idle(None, 10) == 1
+    assert lib.dps_restore_worker_restored(None) == -1
+    lib.dps_restore_worker_destroy(None)
+    sm.close()

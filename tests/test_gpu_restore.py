@@ -182,3 +182,63 @@ def test_sum_managed_eviction_and_restore():
     compute.wait_stream(copy)
     for nw, want in zip(layers, y_full):
         assert torch.equal(dps.linear(x, nw, FULL).view(torch.int16), want.view(torch.int16))
+
+
+def test_restore_worker_thread_restores_evicted_residuals():
+    """The same eviction as above, restored by the native restore worker: a
+    host thread that, once kicked, rewrites each evicted residual's device
+    chunk table to the unit the manager gives it and copies the backup in on
+    its own stream, while fast-mode passes keep running on the compute
+    stream with unchanged bits.  When it is idle the mode is full and full
+    mode gives its first bits again."""
+    n = k = 4096
+    log2c = 21
+    chunks_per_unit = 8
+    unit_bytes = chunks_per_unit << log2c
+    kv_bytes = 64 << 10
+    n_units, n_res = 6, 3
+    sum_mgr = dps.SumManager(n_units, unit_bytes // kv_bytes, n_res)
+    pool = torch.zeros(n_units * unit_bytes, dtype=torch.uint8, device=DEV)
+    x = workloads.activations_fp16(64, k, seed=30).to(DEV)
+    layers, y_full, y_fast, backups = [], [], [], []
+    for r in range(n_res):
+        slots = sum_mgr.slots(r, chunks_per_unit, chunks_per_unit)
+        res = dps.Residual(pool, slots.to(DEV), log2c)
+        nw = dps.split(workloads.weight_fp16(n, k, seed=31 + r).to(DEV), res)
+        layers.append(nw)
+        y_full.append(dps.linear(x, nw, FULL))
+        y_fast.append(dps.linear(x, nw, FAST))
+        backups.append(dps.backup(res, n * k, slots_host=slots))
+    torch.cuda.synchronize()
+    worker = dps.RestoreWorker(sum_mgr, [(backups[r], n * k, layers[r].residual)
+                                         for r in range(n_res)], chunks_per_unit)
+
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(32)
+    held = []
+    while sum_mgr.counts()["evicted"] < 2:
+        blocks = sum_mgr.alloc(100)
+        for b in blocks:
+            pool[b * kv_bytes:(b + 1) * kv_bytes] = torch.randint(
+                0, 256, (kv_bytes,), dtype=torch.uint8, device=DEV, generator=gen)
+        held += blocks
+    torch.cuda.synchronize()
+    assert sum_mgr.mode == dps.MODE_FAST
+    worker.kick()                      # nothing to restore yet: no unit is free
+    worker.wait_idle(10000)
+    assert worker.restored == 0 and sum_mgr.mode == dps.MODE_FAST
+
+    bpu = unit_bytes // kv_bytes
+    assert sum_mgr.free([b for b in held if b // bpu != 0])
+    worker.kick()
+    passes = 0
+    while sum_mgr.mode == dps.MODE_FAST and passes < 2000:   # fast passes meanwhile
+        for nw, want in zip(layers, y_fast):
+            assert torch.equal(dps.linear(x, nw, FAST).view(torch.int16), want.view(torch.int16))
+        passes += 1
+    worker.wait_idle(60000)
+    assert worker.restored == 2 and sum_mgr.mode == dps.MODE_FULL
+    assert [sum_mgr.unit_of(r) for r in range(n_res)] == [1, 3, 2]
+    for nw, want in zip(layers, y_full):
+        assert torch.equal(dps.linear(x, nw, FULL).view(torch.int16), want.view(torch.int16))
+    worker.close()

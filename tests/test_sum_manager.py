@@ -84,3 +84,53 @@ def test_slots_follow_the_binding():
     assert s.slots(0, 8, 5).tolist() == [24, 25, 26, 27, 28]
     with pytest.raises(dps.DpsError):
         s.slots(0, 8, 9)                 # more chunks than a unit holds
+
+
+def test_concurrent_callers_keep_the_bookkeeping_whole():
+    """The native manager locks every call: two host threads allocating and
+    freeing KV blocks (the calls release the GIL) while a third reads the
+    counts leave it exactly where it started, with every block handed out
+    to one caller at a time."""
+    import threading
+
+    sm = dps.SumManager(8, 64, 2)
+    start = sm.counts()
+    seen = set()
+    seen_lock = threading.Lock()
+    errors = []
+
+    def churn(seed):
+        rnd = random.Random(seed)
+        try:
+            for _ in range(1500):
+                blocks = sm.alloc(rnd.randint(1, 40))
+                if blocks is None:
+                    continue
+                with seen_lock:
+                    assert not seen.intersection(blocks)
+                    seen.update(blocks)
+                with seen_lock:
+                    seen.difference_update(blocks)
+                sm.free(blocks)
+        except Exception as e:  # surfaced below
+            errors.append(e)
+
+    def read():
+        try:
+            for _ in range(3000):
+                c = sm.counts()
+                assert sum(c[k] for k in ("free", "backed", "avail", "full", "restoring")) == 8
+        except Exception as e:  # surfaced below
+            errors.append(e)
+
+    threads = [threading.Thread(target=churn, args=(s,)) for s in (1, 2)]
+    threads.append(threading.Thread(target=read))
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    end = sm.counts()
+    assert end["free_blocks"] == end["avail"] * 64 and end["full"] == 0
+    assert end["backed"] + end["evicted"] == start["backed"] == 2
+    sm.close()
