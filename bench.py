@@ -262,6 +262,7 @@ def main():
         secondary["single_layer"] = single_layer_secondary(torch, dps, workloads, stream, enc)
         secondary["moe_grouped"] = moe_secondary(torch, dps, workloads, stream, enc)
         secondary["restore"] = restore_secondary(torch, dps, workloads, stream, enc)
+        secondary["vmm_views"] = vmm_secondary(torch, dps, workloads, stream, enc)
         secondary["sum_manager"] = sum_secondary(dps)
     torch.cuda.synchronize()
 
@@ -763,6 +764,76 @@ def library_fp16_secondary(torch, workloads, layers, ms, stream):
             "decode_pass_us": per_pass,
             "decode_sum_of_passes_ms": round(sum(per_pass.values()) / 1e3, 4),
             "prefill_M2048": {"ms": round(t * 1e3, 3), "TFLOPs": round(flops / t / 1e12, 1)}}
+
+
+def vmm_secondary(torch, dps, workloads, stream, enc):
+    """The hidden-8192 set at 64 tokens with each layer's residual in a
+    contiguous view of 2 MiB physical units (dps_vmm_*), scattered over a
+    region whose other units stand for KV blocks, against the same residuals
+    addressed through scattered chunk tables in an ordinary pool: full-mode
+    passes (four layers), median of 20 each, interleaved."""
+    dev = torch.device("cuda:0")
+    log2c = 21
+    m = 64
+    layers = workloads.H8192_SET
+    chunks = [workloads.n_chunks_for(n * k, log2c) for _, n, k in layers]
+    n_units = 2 * sum(chunks)
+    res = {"workload": "h8192 set, M=64, full mode; 2 MiB units", "units": n_units}
+    try:
+        region = dps.VmmRegion(n_units, 1 << log2c, device=dev)
+    except dps.DpsError as e:
+        res["skipped"] = str(e)
+        return res
+    perm = torch.randperm(n_units, generator=torch.Generator().manual_seed(1401)).tolist()
+    views, via_vmm, via_table, cursor = [], [], [], 0
+    with torch.cuda.stream(stream):
+        for li, (name, n, k) in enumerate(layers):
+            units = perm[cursor:cursor + chunks[li]]
+            cursor += chunks[li]
+            view = region.map_residual(units)
+            views.append(view)
+            w = workloads.weight_fp16(n, k, seed=1410 + li, device=dev)
+            via_vmm.append(dps.split(w, region.residual(view), enc=enc))
+            slots = workloads.chunk_slots(chunks[li], 2 * chunks[li], seed=1420 + li)
+            pool = torch.empty(2 * chunks[li] << log2c, dtype=torch.uint8, device=dev)
+            via_table.append(dps.split(w, dps.Residual(pool, slots.to(dev), log2c), enc=enc))
+            del w
+        xs = {k: workloads.activations_fp16(m, k, seed=k, device=dev)
+              for k in sorted({k for _, _, k in layers})}
+        ys = {n: torch.empty((m, n), dtype=torch.float16, device=dev)
+              for n in sorted({n for _, n, _ in layers})}
+        same = True
+        for li, (name, n, k) in enumerate(layers):
+            a = dps.linear(xs[k], via_vmm[li], dps.MODE_FULL)
+            b = dps.linear(xs[k], via_table[li], dps.MODE_FULL)
+            same = same and bool(torch.equal(a.view(torch.int16), b.view(torch.int16)))
+        times = {"vmm": [], "table": []}
+        for r in range(21):
+            for key, nws in (("vmm", via_vmm), ("table", via_table)):
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                for li, (name, n, k) in enumerate(layers):
+                    dps.linear(xs[k], nws[li], dps.MODE_FULL, out=ys[n])
+                e1.record(stream)
+                if r:
+                    times[key].append((e0, e1))
+    stream.synchronize()
+    wbytes = 2 * sum(n * k for _, n, k in layers)
+    for key in ("vmm", "table"):
+        ts = sorted(a.elapsed_time(b) for a, b in times[key])
+        t = ts[len(ts) // 2] * 1e-3
+        res[key] = {"pass_ms": round(t * 1e3, 4), "pass_ms_p10": round(pct(ts, 10) * 1e3, 4),
+                    "pass_ms_p90": round(pct(ts, 90) * 1e3, 4),
+                    "weight_GBs": round(wbytes / t / 1e9, 1)}
+    res["outputs_identical"] = same
+    del via_vmm, via_table, xs, ys
+    torch.cuda.synchronize()
+    for v in views:
+        region.unmap(v)
+    del views
+    region.close()
+    return res
 
 
 def restore_secondary(torch, dps, workloads, stream, enc):
