@@ -350,14 +350,30 @@ def measured_ceilings(torch, stream):
                 t = best(lambda: probe.lds_fill(buf, window, loaders, stages, fout))
                 fill["%s_%dwaves" % (wname, loaders)] = round(65536 * stages / t / 1e9, 1)
         res["lds_fill_GBs_per_CU"] = fill
-        del buf, out, facc, fout
+        loop = {}
+        lout = torch.empty(256 * 512, dtype=torch.float32, device=dev)
+        for shape, merge, bar, name in ((0, False, True, "8waves_64x128_barrier"),
+                                        (0, True, True, "8waves_64x128_barrier_merge"),
+                                        (0, True, False, "8waves_64x128_merge_no_barrier"),
+                                        (1, True, True, "4waves_128x64_barrier_merge")):
+            fl = [0.0]
+
+            def run(shape=shape, merge=merge, bar=bar):
+                fl[0] = probe.mfma_lds(shape, merge, bar, 2000, 256, lout)
+            t = best(run)
+            loop[name] = round(fl[0] / t / 1e12, 1)
+        res["mfma_lds_loop_TFLOPs"] = loop
+        del buf, out, facc, fout, lout
     torch.cuda.synchronize()
     res["what"] = ("stream read: 512 MiB once, 16-byte loads, 2048 blocks x 256 threads, one "
                    "contiguous chunk per block; MFMA loop: "
                    "register operands, 2048 blocks x 4 waves x 4096 MFMAs; LDS fill: one block "
                    "per CU, 4/8/16 waves issuing direct-to-LDS loads (8 rows x 128 B per "
                    "instruction, rows 4 KiB apart) into 64 KiB stages, 400 stages, from a 1 MiB "
-                   "(L2-resident) or 512 MiB window, GB/s per CU; best of 5")
+                   "(L2-resident) or 512 MiB window, GB/s per CU; MFMA-LDS loop: the FP16 "
+                   "GEMMs' fragment reads (optionally merged from two byte planes) and MFMAs "
+                   "per 64-element stage, optionally a barrier per stage, 256 blocks x 2000 "
+                   "stages; best of 5")
     return res
 
 

@@ -31,6 +31,17 @@ int dps_probe_stream_read(const void *buf, int64_t bytes, int nontemporal, uint3
  * each).  out: device float[blocks * 256]. */
 int dps_probe_mfma(int fp8, int iters, int64_t blocks, float *out, void *stream);
 
+/* The FP16 GEMMs' compute loop alone: `blocks` blocks, shape 0: eight waves
+ * of 64 x 128 wave tiles (the 256 x 256 tile's grid), shape 1: four waves of
+ * 128 x 64 (one wave per SIMD); per 64-element stage every wave reads its weight and token
+ * fragments from LDS (merge != 0: weight fragments from two byte planes
+ * interleaved into FP16, as full mode does) and runs 2 x (TN/16) x (TM/16)
+ * v_mfma_f32_16x16x32_f16 (16384 flops each); barrier != 0 ends every stage
+ * at a block barrier.  iters stages; no global memory inside the loop.
+ * out: device float[blocks * 64 * waves]. */
+int dps_probe_mfma_lds(int shape, int merge, int barrier, int iters, int64_t blocks, float *out,
+                       void *stream);
+
 /* The global -> LDS fill of the GEMMs, alone: `blocks` blocks (one per CU
  * when blocks = CUs; 128 KiB of LDS each) of `loaders` waves (4, 8 or 16),
  * which fill iters stages of 64 KiB by direct-to-LDS loads of 8 rows x 128

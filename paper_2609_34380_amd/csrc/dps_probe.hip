@@ -9,6 +9,11 @@
 //   - mfma_loop_kernel: back-to-back MFMAs on register operands, eight
 //     independent accumulator chains per wave, FP16 16x16x32 or FP8
 //     16x16x128, nothing from memory inside the loop.
+//   - mfma_lds_kernel: the FP16 GEMMs' compute loop alone: per 64-element
+//     stage each wave reads its weight fragments (b128, optionally a second
+//     plane merged byte by byte as full mode does) and its token fragments
+//     from LDS and runs the MFMAs of its wave tile, optionally ending the
+//     stage at a block barrier; no global memory inside the loop.
 //   - lds_fill_kernel: the GEMMs' global -> LDS fill alone: one block per
 //     CU, NL waves issuing direct-to-LDS loads of 8 rows x 128 bytes per
 //     instruction (rows 4 KiB apart, the weight planes' pitch at K = 4096)
@@ -113,6 +118,81 @@ __global__ __launch_bounds__(512) void mfma_loop_kernel(int iters, float seed, f
     out[(int64_t)blockIdx.x * kThreads + threadIdx.x] = s;
 }
 
+__device__ __forceinline__ int probe_swz8(int r) { return (r >> 1) & 7; }
+
+// NW waves of TN x TM tiles over a 256-row tile; LDS holds one 32 KiB stage
+// of each operand, read with the 128-byte-row swizzle of the GEMMs (every
+// address modulo 32 KiB).  MERGE: weight fragments come from two planes 64
+// bytes apart and are interleaved into FP16 words with v_perm.  BAR: a block
+// barrier ends every stage.
+template <int NW, int TN, int TM, bool MERGE, bool BAR>
+__global__ __launch_bounds__(NW * 64) void mfma_lds_kernel(int iters, float *out)
+{
+    __shared__ __attribute__((aligned(16))) unsigned char A[32768], B[32768];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int li = lane & 15, lg = lane >> 4;
+    for (int i = threadIdx.x; i < 32768 / 16; i += NW * 64) {
+        reinterpret_cast<u32x4 *>(A)[i] = u32x4{0x3c003c00u + i, 0x3c003c00u, 0x3c003c00u, 0x3c003c00u};
+        reinterpret_cast<u32x4 *>(B)[i] = u32x4{0x3c003c00u, 0x3c003c00u + i, 0x3c003c00u, 0x3c003c00u};
+    }
+    __syncthreads();
+    constexpr int NT = TN / 16, MT = TM / 16, WN = 256 / TN;
+    const int wn = wave % WN, wm = wave / WN;
+    f32x4 acc[NT][MT];
+#pragma unroll
+    for (int i = 0; i < NT; ++i)
+#pragma unroll
+        for (int j = 0; j < MT; ++j)
+            acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int aoff = ((wn * TN + li) * 128 + ((lg ^ probe_swz8(li)) << 4)) % 32768;
+    const int boff0 = ((wm * TM + li) * 128 + ((lg ^ probe_swz8(li)) << 4)) % 32768;
+    const int boff1 = ((wm * TM + li) * 128 + (((lg + 4) ^ probe_swz8(li)) << 4)) % 32768;
+    for (int it = 0; it < iters; ++it) {
+        if (BAR) {
+            __builtin_amdgcn_s_waitcnt(0xC07F);
+            __builtin_amdgcn_s_barrier();
+        }
+        half8 av[2][NT];
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            const u32x4 h = *reinterpret_cast<const u32x4 *>(A + (aoff + nt * 2048) % 32768);
+            if (MERGE) {
+                const u32x4 l = *reinterpret_cast<const u32x4 *>(A + (aoff + nt * 2048 + 64) % 32768);
+                av[0][nt] = __builtin_bit_cast(
+                    half8, u32x4{__builtin_amdgcn_perm(h.x, l.x, 0x05010400u),
+                                 __builtin_amdgcn_perm(h.x, l.x, 0x07030602u),
+                                 __builtin_amdgcn_perm(h.y, l.y, 0x05010400u),
+                                 __builtin_amdgcn_perm(h.y, l.y, 0x07030602u)});
+                av[1][nt] = __builtin_bit_cast(
+                    half8, u32x4{__builtin_amdgcn_perm(h.z, l.z, 0x05010400u),
+                                 __builtin_amdgcn_perm(h.z, l.z, 0x07030602u),
+                                 __builtin_amdgcn_perm(h.w, l.w, 0x05010400u),
+                                 __builtin_amdgcn_perm(h.w, l.w, 0x07030602u)});
+            } else {
+                av[0][nt] = __builtin_bit_cast(half8, u32x4{h.x, h.y, h.x, h.y});
+                av[1][nt] = __builtin_bit_cast(half8, u32x4{h.z, h.w, h.z, h.w});
+            }
+        }
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            const half8 b0 = *reinterpret_cast<const half8 *>(B + (boff0 + mt * 2048) % 32768);
+            const half8 b1 = *reinterpret_cast<const half8 *>(B + (boff1 + mt * 2048) % 32768);
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+                acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av[0][nt], b0, acc[nt][mt], 0, 0, 0);
+                acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av[1][nt], b1, acc[nt][mt], 0, 0, 0);
+            }
+        }
+    }
+    float sum = 0.f;
+#pragma unroll
+    for (int i = 0; i < NT; ++i)
+#pragma unroll
+        for (int j = 0; j < MT; ++j)
+            sum += acc[i][j].x + acc[i][j].w;
+    out[(int64_t)blockIdx.x * NW * 64 + threadIdx.x] = sum;
+}
+
 // NL loader waves fill 64 KiB per stage (64 / NL instructions each) into
 // slot t & 1 while the previous stage's slot is free; every wave waits for
 // its own loads and meets the others at one barrier per stage.  Stage t of
@@ -209,6 +289,28 @@ DPS_PROBE_EXPORT int dps_probe_lds_fill(const void *buf, int64_t window_bytes, i
         break;
     default:
         return 1;
+    }
+    return hipGetLastError() == hipSuccess ? 0 : 5;
+}
+
+DPS_PROBE_EXPORT int dps_probe_mfma_lds(int shape, int merge, int barrier, int iters,
+                                        int64_t blocks, float *out, void *stream)
+{
+    if (out == nullptr || iters < 1 || blocks < 1 || blocks > (1 << 20) || shape < 0 ||
+        shape > 1)
+        return 1;
+    const dim3 grid((unsigned)blocks);
+    hipStream_t st = (hipStream_t)stream;
+    const int sel = shape * 4 + (merge ? 2 : 0) + (barrier ? 1 : 0);
+    switch (sel) {
+    case 0: hipLaunchKernelGGL((mfma_lds_kernel<8, 64, 128, false, false>), grid, dim3(512), 0, st, iters, out); break;
+    case 1: hipLaunchKernelGGL((mfma_lds_kernel<8, 64, 128, false, true>), grid, dim3(512), 0, st, iters, out); break;
+    case 2: hipLaunchKernelGGL((mfma_lds_kernel<8, 64, 128, true, false>), grid, dim3(512), 0, st, iters, out); break;
+    case 3: hipLaunchKernelGGL((mfma_lds_kernel<8, 64, 128, true, true>), grid, dim3(512), 0, st, iters, out); break;
+    case 4: hipLaunchKernelGGL((mfma_lds_kernel<4, 128, 64, false, false>), grid, dim3(256), 0, st, iters, out); break;
+    case 5: hipLaunchKernelGGL((mfma_lds_kernel<4, 128, 64, false, true>), grid, dim3(256), 0, st, iters, out); break;
+    case 6: hipLaunchKernelGGL((mfma_lds_kernel<4, 128, 64, true, false>), grid, dim3(256), 0, st, iters, out); break;
+    default: hipLaunchKernelGGL((mfma_lds_kernel<4, 128, 64, true, true>), grid, dim3(256), 0, st, iters, out); break;
     }
     return hipGetLastError() == hipSuccess ? 0 : 5;
 }

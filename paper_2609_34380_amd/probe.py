@@ -12,7 +12,7 @@ import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libdps_probe.so")
-EXPORTED = ("dps_probe_stream_read", "dps_probe_mfma", "dps_probe_lds_fill")
+EXPORTED = ("dps_probe_stream_read", "dps_probe_mfma", "dps_probe_lds_fill", "dps_probe_mfma_lds")
 FLOPS_PER_MFMA = {0: 16384, 1: 65536}  # 16x16x32 FP16, 16x16x128 FP8
 
 _lib = None
@@ -32,6 +32,8 @@ def load_library(path=LIB_PATH):
     lib.dps_probe_mfma.restype = C
     lib.dps_probe_lds_fill.argtypes = [P, I64, C, C, I64, P, P]
     lib.dps_probe_lds_fill.restype = C
+    lib.dps_probe_mfma_lds.argtypes = [C, C, C, C, I64, P, P]
+    lib.dps_probe_mfma_lds.restype = C
     _lib = lib
     return lib
 
@@ -75,3 +77,19 @@ def lds_fill(buf, window_bytes, loaders, stages, out):
     _check(lib.dps_probe_lds_fill(ctypes.c_void_p(buf.data_ptr()), int(window_bytes), int(loaders),
                                   int(stages), out.numel(), ctypes.c_void_p(out.data_ptr()),
                                   _stream()), "dps_probe_lds_fill")
+
+
+MFMA_LDS_SHAPES = {0: (8, 64, 128), 1: (4, 128, 64)}   # waves, wave-tile rows, tokens
+
+
+def mfma_lds(shape, merge, barrier, iters, blocks, out):
+    """The GEMMs' compute loop from LDS (dps_probe_mfma_lds); out: float32
+    device tensor of at least blocks * 64 * waves elements.  Returns the
+    flops the launch performs."""
+    lib = load_library()
+    waves, tn, tm = MFMA_LDS_SHAPES[shape]
+    assert out.is_cuda and out.dtype == torch.float32 and out.numel() >= blocks * 64 * waves
+    _check(lib.dps_probe_mfma_lds(int(shape), int(bool(merge)), int(bool(barrier)), int(iters),
+                                  int(blocks), ctypes.c_void_p(out.data_ptr()), _stream()),
+           "dps_probe_mfma_lds")
+    return blocks * waves * (tn // 16) * (tm // 16) * 2 * 16384.0 * iters

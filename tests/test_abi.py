@@ -278,6 +278,9 @@ def test_probe_library_exports_its_header():
     assert plib.dps_probe_lds_fill(0x1000, (1 << 20) + 16, 8, 4, 4, 0x2000, None) == 1
     assert plib.dps_probe_lds_fill(0x1000, 1 << 20, 6, 4, 4, 0x2000, None) == 1
     assert plib.dps_probe_lds_fill(0x1000, 1 << 20, 8, 0, 4, 0x2000, None) == 1
+    assert plib.dps_probe_mfma_lds(2, 0, 1, 8, 4, 0x1000, None) == 1     # no such shape
+    assert plib.dps_probe_mfma_lds(0, 0, 1, 0, 4, 0x1000, None) == 1
+    assert plib.dps_probe_mfma_lds(0, 0, 1, 8, 4, None, None) == 1
 
 
 def test_dense_grid_limit_is_refused_on_the_host(lib):

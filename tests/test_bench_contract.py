@@ -82,3 +82,5 @@ def test_ceiling_probes_on_the_gpu():
     fill = c["lds_fill_GBs_per_CU"]
     assert len(fill) == 6 and all(v > 0 for v in fill.values())
     assert fill["l2_1MiB_16waves"] > fill["l2_1MiB_4waves"]
+    loop = c["mfma_lds_loop_TFLOPs"]
+    assert len(loop) == 4 and all(0 < v <= 2500 for v in loop.values())
