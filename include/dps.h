@@ -427,7 +427,9 @@ dps_status dps_vmm_map_residual(dps_vmm *v, const int32_t *units_host, int64_t c
                                 void **view_out);
 
 /* Map unit `unit` at piece `piece` of a residual view instead of the unit
- * there (a residual restored into another unit). */
+ * there (a residual restored into another unit).  If mapping the new unit
+ * fails, the piece is left unmapped (the call returns the error): nothing
+ * may read the view until a later remap of that piece succeeds. */
 dps_status dps_vmm_remap(dps_vmm *v, void *view, int64_t piece, int32_t unit);
 
 /* Unmap a residual view and free its address range. */
