@@ -15,6 +15,8 @@
 // remapped for the 8 XCDs; grouped (MoE) calls map grid.y onto (expert,
 // token tile) by scanning the device offsets, so only `experts` blocks at
 // most find no work.
+#include <type_traits>
+
 #include "dps_internal.h"
 
 namespace dps {
@@ -40,8 +42,13 @@ struct GemmArgs {
 
 // Token range of this block: dense calls use grid.y as the token tile;
 // grouped calls walk the experts' tile counts.  Returns false if no work.
+// With tail > 0 (grouped calls) an expert's last tile also takes up to `tail`
+// rows beyond bm, so an expert of bm + 1 .. bm + tail rows is one tile, not
+// two: its weights are read once.  Such a range [m0, m1) spans more than bm
+// rows; the kernel treats rows m0 + bm .. m1 - 1 as its tail.  The tile
+// count per expert never grows, so the host's grid bound still holds.
 __device__ __forceinline__ bool block_rows(const GemmArgs &a, int64_t &e, int64_t &m0,
-                                           int64_t &m1, int bm = BM)
+                                           int64_t &m1, int bm = BM, int tail = 0)
 {
     const int64_t t = blockIdx.y;
     if (!a.offsets) {
@@ -55,11 +62,13 @@ __device__ __forceinline__ bool block_rows(const GemmArgs &a, int64_t &e, int64_
     for (int64_t ex = 0; ex < a.experts; ++ex) {
         int64_t o1 = a.offsets[ex + 1];
         o1 = o1 < prev ? prev : (o1 > a.rows ? a.rows : o1);
-        const int64_t tiles = (o1 - prev + bm - 1) / bm;
+        const int64_t r = o1 - prev;
+        const int64_t tiles =
+            r <= 0 ? 0 : (r <= bm + tail ? 1 : (r - tail + bm - 1) / bm);
         if (t < cum + tiles) {
             e = ex;
             m0 = prev + (t - cum) * bm;
-            m1 = m0 + bm < o1 ? m0 + bm : o1;
+            m1 = t == cum + tiles - 1 ? o1 : m0 + bm;  // the last tile takes the tail
             return true;
         }
         cum += tiles;
@@ -404,10 +413,20 @@ struct G4 {
 __device__ __forceinline__ int swz8(int r) { return (r >> 1) & 7; }
 __device__ __forceinline__ int swz16(int r) { return r & 15; }
 
-template <int MODE, int ENC, int BM, int WS, int XS, bool RANGE, bool SPEC>
+// TAIL (grouped calls, 128-token tiles with DMA waves): the block's token
+// range may run up to TAIL rows past its 128-token tile (block_rows).  Those
+// rows take no LDS: each compute wave loads its K-half of their 16-token
+// fragment straight from memory into registers after the stage barrier (the
+// tokens of a call are a few MiB and sit in L2) and runs it against the
+// weight fragments it already holds, waves of token half 0 on the first two
+// 16-row weight sub-tiles of their quarter and waves of half 1 on the other
+// two, so every compute wave does 36 MFMAs per stage instead of 32.  The
+// tail's K-half sums go through LDS with the others.
+template <int MODE, int ENC, int BM, int WS, int XS, bool RANGE, bool SPEC, int TAIL = 0>
 __global__ __launch_bounds__(SPEC ? 768 : 512) void gemm4_kernel(GemmArgs a)
 {
     using C = G4<MODE, BM, WS, XS, SPEC ? 4 : 8>;
+    static_assert(TAIL == 0 || (TAIL == 16 && SPEC && BM == 128), "tail rows: 128-token DMA-wave tile");
     __shared__ __attribute__((aligned(16))) uint8_t smem[C::LDS];
 
     const int tid = threadIdx.x;
@@ -422,10 +441,12 @@ __global__ __launch_bounds__(SPEC ? 768 : 512) void gemm4_kernel(GemmArgs a)
     const int wm = wave & 1;         // BM/2-token half
 
     int64_t e, mrow0, mrow1;
+    int64_t mtail1 = 0;  // end of the tail rows (TAIL blocks whose range passes BM)
     int ntile, s;
     if (a.offsets) {
-        if (!block_rows(a, e, mrow0, mrow1, BM))
+        if (!block_rows(a, e, mrow0, mtail1, BM, TAIL))
             return;
+        mrow1 = mrow0 + BM < mtail1 ? mrow0 + BM : mtail1;
         ntile = blockIdx.x / a.splits;
         s = blockIdx.x % a.splits;
     } else {
@@ -454,11 +475,30 @@ __global__ __launch_bounds__(SPEC ? 768 : 512) void gemm4_kernel(GemmArgs a)
         e = 0;
         mrow0 = mt * BM;
         mrow1 = mrow0 + BM < a.rows ? mrow0 + BM : a.rows;
+        mtail1 = mrow1;
     }
     const int64_t n0 = (int64_t)ntile * 128;
     const int64_t kb0 = (int64_t)s * a.ksplit;
     const int64_t ke = kb0 + a.ksplit < a.k ? kb0 + a.ksplit : a.k;
     const int64_t ntk = ke > kb0 ? (ke - kb0 + C::BK - 1) / C::BK : 0;
+
+    // Tail rows: lane (i, g) of a compute wave loads 32 bytes of token
+    // mrow0 + BM + i per stage, K 64 kh + 16 g .. +15 (its two MFMA steps).
+    // K being a multiple of 16, such a piece lies inside [kb0, ke) whenever
+    // it starts there (stage offset below xtlim); otherwise the lane reads the
+    // row's first 16 elements of the range and zeroes them.  Lanes past the
+    // tail read its last row, whose sums they do not store.
+    const bool has_tail = TAIL > 0 && mtail1 > mrow0 + BM;
+    const uint16_t *xt = static_cast<const uint16_t *>(a.x);
+    const int xtk = 64 * kh + 16 * lg;
+    int xtlim = 0;
+    if (has_tail) {
+        int64_t m = mrow0 + BM + li;
+        m = m < mtail1 ? m : mtail1 - 1;
+        xt += m * a.k + kb0;
+        xtlim = (int)(ke - kb0 - xtk);
+    }
+    const int wmu = __builtin_amdgcn_readfirstlane(wm);  // token half, wave-uniform
 
     // ---- per-lane DMA state (fixed across stages) ------------------------------
     // Stage t of a lane's weight piece starts at wp + 128 t (upper bytes) and,
@@ -591,10 +631,23 @@ __global__ __launch_bounds__(SPEC ? 768 : 512) void gemm4_kernel(GemmArgs a)
             boff[mt][sidx] = r * 256 + (((8 * kh + 2 * lg + sidx) ^ swz16(r)) << 4);
     }
 
-    // one stage of matrix work on the slots of stage t
-    auto compute = [&](int64_t t) {
+    f32x4 tacc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+
+    // one stage of matrix work on the slots of stage t (tail_c: std::true_type
+    // in blocks with tail rows)
+    auto compute = [&](int64_t t, auto tail_c) {
+        constexpr bool TL = decltype(tail_c)::value;
         const uint8_t *st = smem + (int)(t % WS) * C::W_SLOT;
         const uint8_t *xs = smem + C::X_BASE + (int)(t % XS) * C::X_SLOT;
+        u32x4 tx0 = {0u, 0u, 0u, 0u}, tx1 = {0u, 0u, 0u, 0u};
+        if constexpr (TL) {
+            const int64_t off = tk(t) * C::BK;
+            const bool ok = off < xtlim;
+            const uint32_t msk = 0u - (uint32_t)ok;
+            const uint16_t *p = xt + (ok ? off + xtk : 0);
+            tx0 = load16(p) & u32x4{msk, msk, msk, msk};
+            tx1 = load16(p + 8) & u32x4{msk, msk, msk, msk};
+        }
         u32x4 hv[4], lv[4];
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt) {
@@ -625,6 +678,20 @@ __global__ __launch_bounds__(SPEC ? 768 : 512) void gemm4_kernel(GemmArgs a)
                     acc[nt][mt] = mfma16x16x32(sidx ? a1[nt] : a0[nt], bv, acc[nt][mt]);
             }
         }
+        if constexpr (TL) {
+            const half8 b0 = as_half8(tx0), b1 = as_half8(tx1);
+            if (wmu == 0) {
+                tacc[0] = mfma16x16x32(a0[0], b0, tacc[0]);
+                tacc[1] = mfma16x16x32(a0[1], b0, tacc[1]);
+                tacc[0] = mfma16x16x32(a1[0], b1, tacc[0]);
+                tacc[1] = mfma16x16x32(a1[1], b1, tacc[1]);
+            } else {
+                tacc[0] = mfma16x16x32(a0[2], b0, tacc[0]);
+                tacc[1] = mfma16x16x32(a0[3], b0, tacc[1]);
+                tacc[0] = mfma16x16x32(a1[2], b1, tacc[0]);
+                tacc[1] = mfma16x16x32(a1[3], b1, tacc[1]);
+            }
+        }
     };
 
     if (!SPEC || dma_wave) {
@@ -642,7 +709,7 @@ __global__ __launch_bounds__(SPEC ? 768 : 512) void gemm4_kernel(GemmArgs a)
         for (int64_t t = 0; t < ntk; ++t) {
             DPS_WAIT_VMCNT(C::OUTSTANDING);  // tokens t and weights t have landed
             stage_barrier();
-            compute(t);
+            compute(t, std::false_type{});
         }
     } else if (dma_wave) {
         // separate loops per role keep the DMA state out of the compute waves'
@@ -657,23 +724,34 @@ __global__ __launch_bounds__(SPEC ? 768 : 512) void gemm4_kernel(GemmArgs a)
         __syncthreads();    // matches the compute waves' two barriers below
         __syncthreads();
         return;
+    } else if (has_tail) {
+        for (int64_t t = 0; t < ntk; ++t) {
+            stage_barrier();
+            compute(t, std::integral_constant<bool, (TAIL > 0)>{});
+        }
     } else {
         for (int64_t t = 0; t < ntk; ++t) {
             stage_barrier();
-            compute(t);
+            compute(t, std::false_type{});
         }
     }
     DPS_WAIT_VMCNT(0);  // no DMA may still target this block's LDS
     __syncthreads();    // every wave is done reading the stages
 
     // K-half 1 hands its partial sums to K-half 0 through LDS (4 KB per tile)
-    f32x4 *red = reinterpret_cast<f32x4 *>(smem) + (wave & 3) * (4 * C::MT * 64);
+    constexpr int RED = 4 * C::MT + (TAIL > 0 ? 2 : 0);  // 16 x 16 tiles per wave
+    static_assert(4 * RED * 64 * 16 <= C::LDS, "K-half reduction area");
+    f32x4 *red = reinterpret_cast<f32x4 *>(smem) + (wave & 3) * (RED * 64);
     if (kh == 1) {
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
             for (int mt = 0; mt < C::MT; ++mt)
                 red[(nt * C::MT + mt) * 64 + lane] = acc[nt][mt];
+        if (TAIL > 0 && has_tail) {
+            red[(4 * C::MT) * 64 + lane] = tacc[0];
+            red[(4 * C::MT + 1) * 64 + lane] = tacc[1];
+        }
     }
     __syncthreads();
     if (kh == 1)
@@ -685,6 +763,13 @@ __global__ __launch_bounds__(SPEC ? 768 : 512) void gemm4_kernel(GemmArgs a)
         for (int nt = 0; nt < 4; ++nt)
             store_tile_out(a, s, m, n0 + wn * 64 + nt * 16 + lg * 4,
                            acc[nt][mt] + red[(nt * C::MT + mt) * 64 + lane], mrow1);
+    }
+    if (TAIL > 0 && has_tail) {
+        const int64_t m = mrow0 + BM + li;
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+            store_tile_out(a, s, m, n0 + wn * 64 + (2 * wmu + j) * 16 + lg * 4,
+                           tacc[j] + red[(4 * C::MT + j) * 64 + lane], mtail1);
     }
 }
 
@@ -1015,6 +1100,12 @@ int gemm_tokens_per_block(int variant)
 
 namespace {
 
+// Instances that take grouped tail rows: all but E4M3 full mode, whose
+// longer merge leaves its compute waves no room for the tail's 16 registers
+// within the 168 that three waves per SIMD allow (it would spill).
+template <int MODE, int ENC>
+constexpr bool kGroupedTail = !(MODE == MODE_FULL && ENC == ENC_E4M3);
+
 // dense calls: a 1-D grid, padded to a multiple of the 8 XCDs
 dim3 dense_grid(int64_t tiles)
 {
@@ -1044,6 +1135,9 @@ hipError_t launch_g3_variant(const GemmArgs &a, const LinearPlan &plan, hipStrea
     }
 }
 
+// Grouped calls on the 128-token tile with DMA waves take up to 16 tail rows
+// per expert into its last tile (gemm4_kernel, block_rows): an expert of
+// 129-144 rows reads its weights once, not twice.
 template <int MODE, int ENC, int BM, int WS, int XS, bool SPEC>
 hipError_t launch_g4(const GemmArgs &a, const LinearPlan &plan, bool grouped, hipStream_t stream)
 {
@@ -1052,12 +1146,22 @@ hipError_t launch_g4(const GemmArgs &a, const LinearPlan &plan, bool grouped, hi
                                      (unsigned)token_tiles(a.rows, a.experts, true, BM), 1)
                               : dense_grid(nt * plan.splits * ((a.rows + BM - 1) / BM));
     const dim3 block(SPEC ? 768 : 512);
-    if (MODE == MODE_FULL && plan.range_addr)
-        hipLaunchKernelGGL((gemm4_kernel<MODE, ENC, BM, WS, XS, true, SPEC>), grid, block, 0,
-                           stream, a);
-    else
-        hipLaunchKernelGGL((gemm4_kernel<MODE, ENC, BM, WS, XS, false, SPEC>), grid, block, 0,
-                           stream, a);
+    constexpr int TL = SPEC && BM == 128 && kGroupedTail<MODE, ENC> ? 16 : 0;
+    if (MODE == MODE_FULL && plan.range_addr) {
+        if (TL > 0 && grouped)
+            hipLaunchKernelGGL((gemm4_kernel<MODE, ENC, BM, WS, XS, true, SPEC, TL>), grid, block,
+                               0, stream, a);
+        else
+            hipLaunchKernelGGL((gemm4_kernel<MODE, ENC, BM, WS, XS, true, SPEC>), grid, block, 0,
+                               stream, a);
+    } else {
+        if (TL > 0 && grouped)
+            hipLaunchKernelGGL((gemm4_kernel<MODE, ENC, BM, WS, XS, false, SPEC, TL>), grid,
+                               block, 0, stream, a);
+        else
+            hipLaunchKernelGGL((gemm4_kernel<MODE, ENC, BM, WS, XS, false, SPEC>), grid, block,
+                               0, stream, a);
+    }
     return hipGetLastError();
 }
 

@@ -492,6 +492,60 @@ def test_grouped_single_expert_equals_dense():
         assert torch.equal(a.view(torch.int16), b.view(torch.int16))
 
 
+@pytest.mark.parametrize("counts,n,k", [
+    ((129, 144, 545), 256, 1040),                # tails of 1 and 16 rows; 5 tiles; a K tail
+    ((145, 272, 0, 273, 600), 384, 1040),        # 128 + 17; 128 + 144; empty; 128, 128, 17
+    ((129, 144, 600), 128, 4112),                # one weight tile: four K ranges, the last ragged
+])
+@pytest.mark.parametrize("enc", [dps.ENC_E5M2, dps.ENC_E4M3], ids=["e5m2", "e4m3"])
+@pytest.mark.parametrize("mode", [FAST, FULL], ids=["fast", "full"])
+def test_grouped_tail_rows_match_oracle(counts, n, k, enc, mode):
+    """Grouped calls on the 128-token tile: an expert's last tile takes up to
+    16 rows past its 128 (129 or 144 rows: one tile; 145: 128 + 17; 272: 128
+    + 144; 273: three tiles), against the oracle.  (E4M3 full mode keeps
+    separate tiles for such rows; it runs here too.)"""
+    e = len(counts)
+    rows = sum(counts)
+    p = dps.plan_info(mode, "fp16", rows, n, k, experts=e)
+    assert p["kernel"] == "gemm_f16" and p["tile_tokens"] == 128, p
+    if n == 128:
+        assert p["splits"] == 4 and k % p["ksplit"] != 0, p
+    w = workloads.weight_fp16(n, k, seed=131, experts=e)
+    x = workloads.activations_fp16(rows, k, seed=132)
+    offsets = np.zeros(e + 1, dtype=np.int64)
+    offsets[1:] = np.cumsum(counts)
+    nst = Nested(w, 21, enc=enc)
+    off_dev = torch.from_numpy(offsets.astype(np.int32)).to(DEV)
+    y = dps.linear_grouped(x.to(DEV), off_dev, nst.nw, mode)
+    torch.cuda.synchronize()
+    oenc = oracle.E4M3 if enc == dps.ENC_E4M3 else oracle.E5M2
+    ref = oracle.linear_grouped(_omode(mode), u16(x), offsets, nst.hi_ref,
+                                nst.res_ref if mode == FULL else None, enc=oenc)
+    assert_close(y, ref)
+
+
+@pytest.mark.parametrize("m", [257, 270, 272])
+def test_grouped_tail_rows_equal_dense(m):
+    """One expert of 257-272 rows is two 128-token tiles grouped (the second
+    with 1-16 tail rows) and three dense; both plans split K alike, and the
+    tail rows go through the same MFMA and K-half order as a third tile's:
+    the outputs agree bit for bit in both modes."""
+    n, k = 300, 512
+    w = workloads.weight_fp16(n, k, seed=141)
+    x = workloads.activations_fp16(m, k, seed=142).to(DEV)
+    nst = Nested(w, 12)
+    off = torch.tensor([0, m], dtype=torch.int32, device=DEV)
+    nw1 = dps.NestedWeight(nst.nw.hi.view(1, n, k), nst.res)
+    for mode in (FAST, FULL):
+        pd = dps.plan_info(mode, "fp16", m, n, k)
+        pg = dps.plan_info(mode, "fp16", m, n, k, experts=1)
+        assert pd == pg and pd["tile_tokens"] == 128, (pd, pg)
+        a = dps.linear(x, nst.nw, mode)
+        b = dps.linear_grouped(x, off, nw1, mode)
+        torch.cuda.synchronize()
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16)), (m, mode)
+
+
 # -----------------------------------------------------------------------------
 # error paths on the device-side entry points
 # -----------------------------------------------------------------------------
