@@ -177,10 +177,18 @@ struct G3 {
 
 __device__ __forceinline__ int g3_swz(int r) { return (r >> 1) & 7; }
 
-template <int ENC, int BN_, int BM_, int WN, int WM, int WS, int XS, bool DW>
+// TAIL (grouped calls on the 256 x 128 tile): as in the FP16 wide-row GEMM,
+// an expert's last token tile may run up to TAIL rows past 128 (block_rows);
+// each compute wave loads the 32-byte K slices of the 16 tail tokens for
+// every stage straight from memory into registers and runs them against
+// two of its four weight fragments (token half 0 the first two, half 1 the
+// last two): 18 MFMAs per stage instead of 16.
+template <int ENC, int BN_, int BM_, int WN, int WM, int WS, int XS, bool DW, int TAIL = 0>
 __global__ __launch_bounds__(WN * WM * 64 + (DW ? 256 : 0)) void gemm3_kernel(GemmArgs a)
 {
     using C = G3<BN_, BM_, WN, WM, WS, XS, DW>;
+    static_assert(TAIL == 0 || (TAIL == 16 && DW && BM_ == 128 && WM == 2 && C::NT == 4),
+                  "tail rows: the 256 x 128 tile with DMA waves");
     __shared__ __attribute__((aligned(16))) uint8_t smem[C::LDS];
 
     const int tid = threadIdx.x;
@@ -196,12 +204,14 @@ __global__ __launch_bounds__(WN * WM * 64 + (DW ? 256 : 0)) void gemm3_kernel(Ge
     const bool issues = !DW || dma_wave;
 
     int64_t e, mrow0, mrow1;
+    int64_t mtail1 = 0;  // end of the tail rows (TAIL blocks whose range passes BM_)
     int ntile, s;
     if (a.offsets) {
         // grouped: grid.y walks the experts' token tiles, grid.x the weight
         // tiles times the K ranges
-        if (!block_rows(a, e, mrow0, mrow1, BM_))
+        if (!block_rows(a, e, mrow0, mtail1, BM_, TAIL))
             return;
+        mrow1 = mrow0 + BM_ < mtail1 ? mrow0 + BM_ : mtail1;
         ntile = blockIdx.x / a.splits;
         s = blockIdx.x % a.splits;
     } else {
@@ -222,11 +232,26 @@ __global__ __launch_bounds__(WN * WM * 64 + (DW ? 256 : 0)) void gemm3_kernel(Ge
         e = 0;
         mrow0 = (t0 % mtiles) * BM_;
         mrow1 = mrow0 + BM_ < a.rows ? mrow0 + BM_ : a.rows;
+        mtail1 = mrow1;
     }
     const int64_t n0 = (int64_t)ntile * BN_;
     const int64_t kb0 = (int64_t)s * a.ksplit;
     const int64_t ke = kb0 + a.ksplit < a.k ? kb0 + a.ksplit : a.k;
     const int64_t ntk = ke > kb0 ? (ke - kb0 + C::BK - 1) / C::BK : 0;
+
+    // Tail rows: lane (i, g) of a compute wave reads bytes 16g .. 16g+15 and
+    // 64+16g .. 64+16g+15 of each stage of token mrow0 + BM_ + i (the slice
+    // its MFMA operand takes).  K being a multiple of 16, a piece is inside
+    // [kb0, ke) whenever it starts there; otherwise the lane reads the row's
+    // first 16 bytes of the range and zeroes them.  Lanes past the tail read
+    // its last row, whose sums they do not store.
+    const bool has_tail = TAIL > 0 && mtail1 > mrow0 + BM_;
+    const uint8_t *xt = static_cast<const uint8_t *>(a.x);
+    if (has_tail) {
+        int64_t m = mrow0 + BM_ + li;
+        m = m < mtail1 ? m : mtail1 - 1;
+        xt += m * a.k + kb0;
+    }
 
     // ---- per-lane DMA sources (fixed across stages) ------------------------------
     // instruction j covers LDS bytes j*1024 .. +1023 of its operand tile:
@@ -297,16 +322,40 @@ __global__ __launch_bounds__(WN * WM * 64 + (DW ? 256 : 0)) void gemm3_kernel(Ge
         if (u + WS - 1 >= 0)
             issue_w(u + WS - 1);
     }
-    for (int64_t t = 0; t < ntk; ++t) {
-        if (issues)
+    if (DW && dma_wave) {
+        // the DMA waves' own loop keeps their source pointers out of the
+        // compute waves' registers (and the accumulators out of theirs)
+        for (int64_t t = 0; t < ntk; ++t) {
             DPS_WAIT_VMCNT(C::OUTSTANDING);  // tokens t and weights t have landed
-        stage_barrier();
-        if (issues) {
+            stage_barrier();
             issue_x(t + XS - 1);
             issue_w(t + WS - 1);
         }
-        if (dma_wave)
-            continue;
+        DPS_WAIT_VMCNT(0);  // no DMA may still target this block's LDS when it exits
+        return;
+    }
+    f32x4 tacc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+    const int wmu = __builtin_amdgcn_readfirstlane(wm);  // token half, wave-uniform
+    // one stage of a compute wave, which without DW also issues its share of
+    // the DMA (tail_c: std::true_type in blocks with tail rows)
+    auto stage = [&](int64_t t, auto tail_c) {
+        constexpr bool TL = decltype(tail_c)::value;
+        if (!DW)
+            DPS_WAIT_VMCNT(C::OUTSTANDING);  // tokens t and weights t have landed
+        stage_barrier();
+        if (!DW) {
+            issue_x(t + XS - 1);
+            issue_w(t + WS - 1);
+        }
+        u32x4 tp = {0u, 0u, 0u, 0u}, tq = {0u, 0u, 0u, 0u};
+        if constexpr (TL) {
+            const int64_t off = t * C::BK + 16 * lg;
+            const bool ok = kb0 + off < ke;
+            const uint32_t msk = 0u - (uint32_t)ok;
+            const uint8_t *pp = xt + (ok ? off : 0);
+            tp = load16(pp) & u32x4{msk, msk, msk, msk};
+            tq = load16(pp + (ok ? 64 : 0)) & u32x4{msk, msk, msk, msk};
+        }
         const uint8_t *st = smem + (int)(t % WS) * C::W_BYTES;
         const uint8_t *xs = smem + C::X_BASE + (int)(t % XS) * C::X_BYTES;
         i32x8 av[C::NT];
@@ -333,10 +382,26 @@ __global__ __launch_bounds__(WN * WM * 64 + (DW ? 256 : 0)) void gemm3_kernel(Ge
             for (int nt = 0; nt < C::NT; ++nt)
                 acc[nt][mt] = mfma16x16x128_fp8<ENC>(av[nt], bv, acc[nt][mt]);
         }
+        if constexpr (TL) {
+            const i32x8 tb = {(int)tp.x, (int)tp.y, (int)tp.z, (int)tp.w,
+                              (int)tq.x, (int)tq.y, (int)tq.z, (int)tq.w};
+            if (wmu == 0) {
+                tacc[0] = mfma16x16x128_fp8<ENC>(av[0], tb, tacc[0]);
+                tacc[1] = mfma16x16x128_fp8<ENC>(av[1], tb, tacc[1]);
+            } else {
+                tacc[0] = mfma16x16x128_fp8<ENC>(av[2], tb, tacc[0]);
+                tacc[1] = mfma16x16x128_fp8<ENC>(av[3], tb, tacc[1]);
+            }
+        }
+    };
+    if (has_tail) {
+        for (int64_t t = 0; t < ntk; ++t)
+            stage(t, std::integral_constant<bool, (TAIL > 0)>{});
+    } else {
+        for (int64_t t = 0; t < ntk; ++t)
+            stage(t, std::false_type{});
     }
     DPS_WAIT_VMCNT(0);  // no DMA may still target this block's LDS when it exits
-    if (dma_wave)
-        return;
 
     // E4M3 weights carry the fast-mode factor 2^-8 (exact in fp32)
     constexpr float wscale = ENC == ENC_E4M3 ? 0.00390625f : 1.f;
@@ -348,6 +413,14 @@ __global__ __launch_bounds__(WN * WM * 64 + (DW ? 256 : 0)) void gemm3_kernel(Ge
         for (int nt = 0; nt < C::NT; ++nt)
             store_tile_out(a, s, m, n0 + wn * C::TN + nt * 16 + lg * 4, acc[nt][mt] * sc,
                            mrow1);
+    }
+    if (TAIL > 0 && has_tail) {
+        const int64_t m = mrow0 + BM_ + li;
+        const float sc = m < mtail1 ? a.scale[m] * wscale : 0.f;
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+            store_tile_out(a, s, m, n0 + wn * C::TN + (2 * wmu + j) * 16 + lg * 4,
+                           tacc[j] * sc, mtail1);
     }
 }
 
@@ -1119,9 +1192,14 @@ hipError_t launch_g3(const GemmArgs &a, const LinearPlan &plan, hipStream_t stre
     const dim3 grid = a.offsets ? dim3((unsigned)(nt * plan.splits),
                                        (unsigned)token_tiles(a.rows, a.experts, true, BM_), 1)
                                 : dense_grid(nt * plan.splits * ((a.rows + BM_ - 1) / BM_));
-    hipLaunchKernelGGL((gemm3_kernel<ENC, BN_, BM_, WN, WM, WS, XS, DW>), grid,
-                       dim3(WN * WM * 64 + (DW ? 256 : 0)), 0,
-                       stream, a);
+    // grouped calls on the 256 x 128 tile take up to 16 tail rows per expert
+    constexpr int TL = DW && BM_ == 128 ? 16 : 0;
+    if (TL > 0 && a.offsets)
+        hipLaunchKernelGGL((gemm3_kernel<ENC, BN_, BM_, WN, WM, WS, XS, DW, TL>), grid,
+                           dim3(WN * WM * 64 + (DW ? 256 : 0)), 0, stream, a);
+    else
+        hipLaunchKernelGGL((gemm3_kernel<ENC, BN_, BM_, WN, WM, WS, XS, DW>), grid,
+                           dim3(WN * WM * 64 + (DW ? 256 : 0)), 0, stream, a);
     return hipGetLastError();
 }
 

@@ -449,6 +449,7 @@ def test_grouped_single_expert_workspace_and_values(m):
     ((100, 0, 300, 129, 7), 160, 1024),                # ragged 128-token tiles, weight-tile tail
     ((128, 140, 120, 133, 110, 125, 131, 137), 256, 256),
     ((300, 0, 41), 256, 4096),                         # few weight tiles: K split
+    ((129, 144, 145, 272, 273, 0), 256, 1040),         # tail rows (1-16) in last tiles, a K tail
 ])
 @pytest.mark.parametrize("enc", [dps.ENC_E5M2, dps.ENC_E4M3], ids=["e5m2", "e4m3"])
 def test_grouped_fp8_matches_oracle(counts, n, k, enc):
@@ -528,22 +529,22 @@ def test_grouped_tail_rows_match_oracle(counts, n, k, enc, mode):
 def test_grouped_tail_rows_equal_dense(m):
     """One expert of 257-272 rows is two 128-token tiles grouped (the second
     with 1-16 tail rows) and three dense; both plans split K alike, and the
-    tail rows go through the same MFMA and K-half order as a third tile's:
-    the outputs agree bit for bit in both modes."""
+    tail rows go through the same MFMA (and K-half) order as a third tile's:
+    the outputs agree bit for bit in both modes and with FP8 activations."""
     n, k = 300, 512
     w = workloads.weight_fp16(n, k, seed=141)
     x = workloads.activations_fp16(m, k, seed=142).to(DEV)
     nst = Nested(w, 12)
     off = torch.tensor([0, m], dtype=torch.int32, device=DEV)
     nw1 = dps.NestedWeight(nst.nw.hi.view(1, n, k), nst.res)
-    for mode in (FAST, FULL):
-        pd = dps.plan_info(mode, "fp16", m, n, k)
-        pg = dps.plan_info(mode, "fp16", m, n, k, experts=1)
+    for mode, act in ((FAST, "fp16"), (FULL, "fp16"), (FAST, "fp8")):
+        pd = dps.plan_info(mode, act, m, n, k)
+        pg = dps.plan_info(mode, act, m, n, k, experts=1)
         assert pd == pg and pd["tile_tokens"] == 128, (pd, pg)
-        a = dps.linear(x, nst.nw, mode)
-        b = dps.linear_grouped(x, off, nw1, mode)
+        a = dps.linear(x, nst.nw, mode, act=act)
+        b = dps.linear_grouped(x, off, nw1, mode, act=act)
         torch.cuda.synchronize()
-        assert torch.equal(a.view(torch.int16), b.view(torch.int16)), (m, mode)
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16)), (m, mode, act)
 
 
 # -----------------------------------------------------------------------------
