@@ -69,7 +69,10 @@ typedef enum {
  *                 (top bit 0 when written, ignored when read); exact only
  *                 when e's MSB is 0.  Fast-mode weight = OCP E4M3(upper) *
  *                 2^-8, a number only when |w| < 1.875.  dps_select_enc
- *                 says whether a whole layer qualifies. */
+ *                 says whether a whole layer qualifies.  The linear calls,
+ *                 in both modes, assume an E4M3 layer that qualifies: words
+ *                 of 1.875 <= |w| < 2 (upper byte an E4M3 NaN code) give
+ *                 NaN there; dps_merge restores every word. */
 enum { DPS_ENC_E5M2 = 0, DPS_ENC_E4M3 = 1 };
 
 /* Activation handling, `flags` argument of the linear calls.

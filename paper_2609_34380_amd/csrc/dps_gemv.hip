@@ -57,7 +57,7 @@ __device__ __forceinline__ void words16(u32x4 h, u32x4 l, uint32_t (&w)[8])
     const uint32_t ll[4] = {l.x, l.y, l.z, l.w};
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-        const u32x2 p = MODE == MODE_FULL ? merge4<ENC>(hh[j], ll[j]) : fast4<ENC>(hh[j]);
+        const u32x2 p = MODE == MODE_FULL ? merge4_lin<ENC>(hh[j], ll[j]) : fast4<ENC>(hh[j]);
         w[2 * j] = p.x;
         w[2 * j + 1] = p.y;
     }
