@@ -324,3 +324,41 @@ def test_e4m3_weights_near_the_bound_and_subnormal():
     back = dps.merge(nst.nw)
     torch.cuda.synchronize()
     assert np.array_equal(u16(back.cpu()), u16(w))
+
+
+@pytest.mark.parametrize("m", [1, 8, 64, 200, 272])
+def test_e4m3_linear_ignores_residual_top_bit(m):
+    """Full-mode linear reads only the residual byte's seven low bits (the
+    E4M3 layout): setting the top bit of every pool byte leaves Y unchanged,
+    bit for bit, on the one-token kernel (1), the small-token kernel (8),
+    the FP16 GEMM's 64- and 128-token tiles (64, 200) and a grouped call of
+    one expert with 272 rows and one with none (272)."""
+    n, k = 272, 1024
+    w = _wide_weight(n, k, seed=41)
+    nst = Nested(w, 10, n_slots=600, slot_seed=42, filler_seed=43, enc=E4M3)
+    x = _acts(m, k, 44, True).to(DEV)
+    grouped = m == 272
+    if grouped:
+        w2 = _wide_weight(n, k, seed=45)
+        w3 = torch.stack([w, w2])
+        nst = Nested(w3, 10, n_slots=1200, slot_seed=46, filler_seed=47, enc=E4M3)
+        off = torch.tensor([0, m, m], dtype=torch.int32, device=DEV)
+
+    def run():
+        if grouped:
+            return dps.linear_grouped(x, off, nst.nw, FULL)
+        return dps.linear(x, nst.nw, FULL)
+
+    y_clean = run()
+    pool = nst.res.pool.clone()
+    nst.res.pool |= 0x80
+    y_top = run()
+    torch.cuda.synchronize()
+    nst.res.pool.copy_(pool)
+    assert torch.equal(y_clean.view(torch.int16), y_top.view(torch.int16))
+    if grouped:
+        ref = oracle.linear_grouped(oracle.FULL, u16(x.cpu()), np.array([0, m, m]), nst.hi_ref,
+                                    nst.res_ref, enc=oracle.E4M3)
+    else:
+        ref = oracle.linear(oracle.FULL, u16(x.cpu()), nst.hi_ref, nst.res_ref, enc=oracle.E4M3)
+    assert_close(y_clean, ref, "m=%d" % m)
