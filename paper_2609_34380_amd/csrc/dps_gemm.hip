@@ -1173,12 +1173,6 @@ int gemm_tokens_per_block(int variant)
 
 namespace {
 
-// Instances that take grouped tail rows: all but E4M3 full mode, whose
-// longer merge leaves its compute waves no room for the tail's 16 registers
-// within the 168 that three waves per SIMD allow (it would spill).
-template <int MODE, int ENC>
-constexpr bool kGroupedTail = !(MODE == MODE_FULL && ENC == ENC_E4M3);
-
 // dense calls: a 1-D grid, padded to a multiple of the 8 XCDs
 dim3 dense_grid(int64_t tiles)
 {
@@ -1224,7 +1218,10 @@ hipError_t launch_g4(const GemmArgs &a, const LinearPlan &plan, bool grouped, hi
                                      (unsigned)token_tiles(a.rows, a.experts, true, BM), 1)
                               : dense_grid(nt * plan.splits * ((a.rows + BM - 1) / BM));
     const dim3 block(SPEC ? 768 : 512);
-    constexpr int TL = SPEC && BM == 128 && kGroupedTail<MODE, ENC> ? 16 : 0;
+    // every mode and encoding fits the tail's 16 registers within the 168
+    // that three waves per SIMD allow (E4M3 full mode since its conversion-
+    // based merge; the bit-move merge spilled)
+    constexpr int TL = SPEC && BM == 128 ? 16 : 0;
     if (MODE == MODE_FULL && plan.range_addr) {
         if (TL > 0 && grouped)
             hipLaunchKernelGGL((gemm4_kernel<MODE, ENC, BM, WS, XS, true, SPEC, TL>), grid, block,

@@ -503,8 +503,7 @@ def test_grouped_single_expert_equals_dense():
 def test_grouped_tail_rows_match_oracle(counts, n, k, enc, mode):
     """Grouped calls on the 128-token tile: an expert's last tile takes up to
     16 rows past its 128 (129 or 144 rows: one tile; 145: 128 + 17; 272: 128
-    + 144; 273: three tiles), against the oracle.  (E4M3 full mode keeps
-    separate tiles for such rows; it runs here too.)"""
+    + 144; 273: three tiles), against the oracle, in both nestings."""
     e = len(counts)
     rows = sum(counts)
     p = dps.plan_info(mode, "fp16", rows, n, k, experts=e)
@@ -525,18 +524,20 @@ def test_grouped_tail_rows_match_oracle(counts, n, k, enc, mode):
     assert_close(y, ref)
 
 
+@pytest.mark.parametrize("enc", [dps.ENC_E5M2, dps.ENC_E4M3], ids=["e5m2", "e4m3"])
 @pytest.mark.parametrize("m", [257, 270, 272])
-def test_grouped_tail_rows_equal_dense(m):
+def test_grouped_tail_rows_equal_dense(m, enc):
     """One expert of 257-272 rows is two 128-token tiles grouped (the second
     with 1-16 tail rows) and three dense; both plans split K alike, and the
     tail rows go through the same MFMA (and K-half) order as a third tile's:
-    the outputs agree bit for bit in both modes and with FP8 activations."""
+    the outputs agree bit for bit in both modes and with FP8 activations, in
+    both nestings."""
     n, k = 300, 512
     w = workloads.weight_fp16(n, k, seed=141)
     x = workloads.activations_fp16(m, k, seed=142).to(DEV)
-    nst = Nested(w, 12)
+    nst = Nested(w, 12, enc=enc)
     off = torch.tensor([0, m], dtype=torch.int32, device=DEV)
-    nw1 = dps.NestedWeight(nst.nw.hi.view(1, n, k), nst.res)
+    nw1 = dps.NestedWeight(nst.nw.hi.view(1, n, k), nst.res, enc)
     for mode, act in ((FAST, "fp16"), (FULL, "fp16"), (FAST, "fp8")):
         pd = dps.plan_info(mode, act, m, n, k)
         pg = dps.plan_info(mode, act, m, n, k, experts=1)
