@@ -524,6 +524,36 @@ def test_grouped_tail_rows_match_oracle(counts, n, k, enc, mode):
     assert_close(y, ref)
 
 
+@pytest.mark.parametrize("seed", range(24))
+def test_grouped_tail_rows_random(seed):
+    """Seeded random grouped calls whose experts hold 0-39, 120-160 or
+    250-290 rows (no tail, up to 16 tail rows past a 128-token tile, or a
+    second tile with a tail), random N, K and chunk size, alternating the
+    nesting and the mode, against the oracle."""
+    rng = np.random.default_rng(7700 + seed)
+    e = int(rng.integers(1, 5))
+    counts = [int(rng.choice([rng.integers(0, 40), rng.integers(120, 161),
+                              rng.integers(250, 291)])) for _ in range(e)]
+    counts[0] = max(counts[0], 129)  # at least one expert past a tile
+    rows = sum(counts)
+    k = 16 * int(rng.integers(8, 160))
+    n = int(rng.integers(1, 400))
+    enc = dps.ENC_E4M3 if seed % 2 else dps.ENC_E5M2
+    mode = FULL if (seed // 2) % 2 else FAST
+    w = workloads.weight_fp16(n, k, seed=8000 + seed, experts=e)
+    x = workloads.activations_fp16(rows, k, seed=9000 + seed)
+    offsets = np.zeros(e + 1, dtype=np.int64)
+    offsets[1:] = np.cumsum(counts)
+    nst = Nested(w, int(rng.integers(8, 22)), enc=enc)
+    off_dev = torch.from_numpy(offsets.astype(np.int32)).to(DEV)
+    y = dps.linear_grouped(x.to(DEV), off_dev, nst.nw, mode)
+    torch.cuda.synchronize()
+    oenc = oracle.E4M3 if enc == dps.ENC_E4M3 else oracle.E5M2
+    ref = oracle.linear_grouped(_omode(mode), u16(x), offsets, nst.hi_ref,
+                                nst.res_ref if mode == FULL else None, enc=oenc)
+    assert_close(y, ref, "counts=%s n=%d k=%d" % (counts, n, k))
+
+
 @pytest.mark.parametrize("enc", [dps.ENC_E5M2, dps.ENC_E4M3], ids=["e5m2", "e4m3"])
 @pytest.mark.parametrize("m", [257, 270, 272])
 def test_grouped_tail_rows_equal_dense(m, enc):
