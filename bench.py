@@ -60,6 +60,9 @@ def parse():
     ap.add_argument("--probe-slots", choices=("identity", "scattered"), default="identity",
                     help="residual chunk table of --probe-call: chunk c in slot c, or chunks at "
                          "seeded random slots of a pool twice the residual's size")
+    ap.add_argument("--probe-moe", default=None,
+                    help="LAYER:MODE[:fp8] of the MoE set (gate_up or down) -- run only that "
+                         "grouped call (for rocprofv3) and a copy kernel of known size, then exit")
     ap.add_argument("--ceilings", action="store_true",
                     help="measure only the HBM streaming-read and MFMA-loop ceilings "
                          "(libdps_probe), print them as JSON and exit")
@@ -98,6 +101,9 @@ def main():
         return
     if args.probe_call:
         probe(args, torch, dps, workloads, layers, dev, stream, enc)
+        return
+    if args.probe_moe:
+        probe_moe(args, torch, dps, workloads, dev, stream, enc)
         return
     ms = workloads.DECODE_M
     modes = (("fast", dps.MODE_FAST), ("full", dps.MODE_FULL))
@@ -458,6 +464,57 @@ def probe(args, torch, dps, workloads, layers, dev, stream, enc):
                       "slots": args.probe_slots, "us_per_call": round(t * 1e6, 2),
                       "kernels_per_call": 1 if need == 0 else 2,
                       "flops_per_call": 2.0 * m * n * k,
+                      "copy_bytes_each_way": 256 << 20}), flush=True)
+
+
+def probe_moe(args, torch, dps, workloads, dev, stream, enc):
+    """One grouped call of the MoE set (8 experts, hidden 4096, ffn 14336, 512
+    tokens routed top-2 as in the bench's MoE leg; one weight copy, 1.4-2.8 GB
+    of planes, beyond the Infinity Cache), launched back to back, then a
+    device-to-device copy of 256 MiB to calibrate rocprofv3's FETCH_SIZE /
+    WRITE_SIZE."""
+    parts = args.probe_moe.split(":")
+    name, mode_name = parts[:2]
+    act = parts[2] if len(parts) > 2 else "fp16"
+    mode = dps.MODE_FAST if mode_name == "fast" else dps.MODE_FULL
+    if act not in ("fp16", "fp8") or (act == "fp8" and mode != dps.MODE_FAST):
+        raise SystemExit("--probe-moe: FP8 activations need fast mode")
+    experts, tokens, topk = 8, 512, 2
+    rows = tokens * topk
+    token_of_row, offsets = workloads.moe_routing(tokens, experts, topk, seed=901)
+    li = [l[0] for l in workloads.MOE_SHAPES].index(name)
+    _, n, k = workloads.MOE_SHAPES[li]
+    with torch.cuda.stream(stream):
+        off_dev = offsets.to(torch.int32).to(dev)
+        w = workloads.weight_fp16(n, k, seed=910 + li, experts=experts, device=dev)
+        nw = dps.split(w, dps.make_residual(w.numel(), 21, dev), enc=enc)
+        del w
+        x = workloads.activations_fp16(tokens, k, seed=920 + li, device=dev)
+        x = x[token_of_row.to(dev)].contiguous()
+        y = torch.empty((rows, n), dtype=torch.float16, device=dev)
+        need = dps.workspace_bytes(mode, dps._act_flag(act), rows, n, k, experts)
+        ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+        for _ in range(2):
+            dps.linear_grouped(x, off_dev, nw, mode, act=act, out=y, workspace=ws)
+        stream.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.probe_reps):
+            dps.linear_grouped(x, off_dev, nw, mode, act=act, out=y, workspace=ws)
+        e1.record(stream)
+        stream.synchronize()
+        src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        stream.synchronize()
+    t = e0.elapsed_time(e1) * 1e-3 / args.probe_reps
+    wb = 1 if mode == dps.MODE_FAST else 2
+    print(json.dumps({"probe_moe": args.probe_moe, "rows": rows, "experts": experts,
+                      "expert_rows": [int(v) for v in (offsets[1:] - offsets[:-1]).tolist()],
+                      "us_per_call": round(t * 1e6, 2),
+                      "algorithmic_bytes_per_call": wb * experts * n * k + 2 * rows * (n + k),
                       "copy_bytes_each_way": 256 << 20}), flush=True)
 
 
